@@ -1,0 +1,212 @@
+/*
+ * specmemo.h - C ABI of the MI355X (gfx950) tree-verification library.
+ *
+ * One speculative step of Medusa-style decoding as SpecMemo runs it
+ * (arXiv 2506.01986): the heads propose, the base model verifies a whole
+ * candidate tree in one forward pass, the longest verified path is accepted,
+ * and the KV cache - a preallocated scratch space sized to a budget - is
+ * updated in place.  Four calls, one per stage, in this order on one stream:
+ *
+ *   specmemo_medusa_topk   (a) head projection, per-head top-k, tree tokens
+ *   specmemo_tree_attn     (b) tree-masked attention over the ragged batch
+ *   specmemo_accept        (c) greedy / typical acceptance of the longest path
+ *   specmemo_kv_compact    (d) in-place compaction of the accepted K/V
+ *
+ * Symbols follow the paper's memory model (Sec. 3.1): b = batch (B),
+ * k = KV heads (n_kv), d = head dim (head_dim), x = KV length
+ * (seq_len / seq_cap), l = Medusa heads = tree levels (n_heads),
+ * k = arity = top-k per head (topk[i]), N = tree nodes, w = vocabulary
+ * (vocab), tau = accept_len + 1 tokens committed per step.
+ *
+ * Conventions for every call
+ *  - Ownership: every buffer belongs to the caller.  Device pointers are
+ *    device memory; "_h" pointers are host memory that is read only during
+ *    the call.  The library never allocates, frees or synchronises; scratch
+ *    space comes only through the (ws, ws_bytes) arguments.
+ *  - Asynchrony: `stream` is a hipStream_t passed as void* (NULL = the null
+ *    stream).  Calls enqueue kernels and return; results are ordered on the
+ *    stream.
+ *  - Alignment: every device pointer must be 16-byte aligned.
+ *  - Errors: calls return a specmemo_status.  All argument, tree, budget and
+ *    workspace checks run on the host before anything is enqueued; on failure
+ *    nothing is enqueued and no output changes.  specmemo_last_error() then
+ *    describes the failure.  A launch failure returns SPECMEMO_E_HIP; faults
+ *    inside kernels surface at the caller's next synchronisation.
+ *  - Trees: one tree per sequence, nodes in BFS order with local ids
+ *    0..N_b-1, node 0 is the root, parent[n] < n, depth[n] =
+ *    depth[parent[n]] + 1, sibling ranks distinct, 1 <= N_b <= 128.
+ *    rank[n] indexes head depth[n]-1's top-k list (node tokens depend only on
+ *    depth and rank, Sec. 3.1 Eq. 2).
+ *  - KV pool: for one layer, K and V are [n_kv][cap_total][head_dim]; each
+ *    sequence owns the slab of rows [seq_base[b], seq_base[b] + seq_cap[b]);
+ *    its L_b = seq_len[b] committed rows come first, and before the step the
+ *    caller has written the K/V rows of the tree's N_b nodes at slab rows
+ *    L_b .. L_b + N_b - 1 (node order).  L_b + N_b <= seq_cap[b] is the
+ *    budget: this is SpecMemo's precise preallocation (Sec. 3.1, KV-cache
+ *    paragraph) instead of one sized for the full context.
+ */
+#ifndef SPECMEMO_H
+#define SPECMEMO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPECMEMO_ABI_VERSION 1
+#define SPECMEMO_MAX_TREE_NODES 128 /* nodes per sequence's tree */
+#define SPECMEMO_MAX_DEPTH 15       /* tree depth (= Medusa heads) */
+#define SPECMEMO_MAX_TOPK 32        /* top-k per head */
+#define SPECMEMO_MAX_BATCH 4096     /* sequences per call */
+
+typedef enum {
+  SPECMEMO_OK = 0,
+  SPECMEMO_E_ARG = -1,       /* null/misaligned pointer, bad size or shape */
+  SPECMEMO_E_DTYPE = -2,     /* unsupported dtype, or dtype/shape combination */
+  SPECMEMO_E_TREE = -3,      /* tree arrays violate the conventions above */
+  SPECMEMO_E_BUDGET = -4,    /* L_b + N_b > seq_cap[b], or slab outside the pool */
+  SPECMEMO_E_WORKSPACE = -5, /* ws is NULL or smaller than specmemo_workspace_bytes */
+  SPECMEMO_E_HIP = -6        /* a HIP launch failed */
+} specmemo_status;
+
+typedef enum { SPECMEMO_FP32 = 0, SPECMEMO_BF16 = 1 } specmemo_dtype;
+
+typedef enum { SPECMEMO_ACCEPT_GREEDY = 0, SPECMEMO_ACCEPT_TYPICAL = 1 } specmemo_accept_mode;
+
+/* Ragged batch of candidate trees, CSR over nodes.  Device arrays are read by
+ * kernels; the host mirrors (same contents) are read for validation and launch
+ * planning during the call. */
+typedef struct {
+  int32_t B;                  /* sequences */
+  const int32_t *node_off;    /* device [B+1], node_off[0] = 0, node_off[B] = sum N_b */
+  const int32_t *parent;      /* device [sum N_b], local ids, parent[root] = -1 */
+  const int32_t *depth;       /* device [sum N_b], root depth 0 */
+  const int32_t *rank;        /* device [sum N_b], root rank 0 */
+  const int32_t *node_off_h;  /* host mirrors of the four arrays above */
+  const int32_t *parent_h;
+  const int32_t *depth_h;
+  const int32_t *rank_h;
+} specmemo_trees;
+
+/* Budget-capped KV pool of one layer. */
+typedef struct {
+  void *k;                    /* device [n_kv][cap_total][head_dim], dtype */
+  void *v;                    /* device, same shape */
+  int64_t cap_total;          /* pool rows per KV head */
+  int32_t n_kv;               /* KV heads */
+  int32_t head_dim;           /* d */
+  int32_t *seq_len;           /* device [B]: written by specmemo_kv_compact */
+  const int64_t *seq_base_h;  /* host [B]: first pool row of each slab */
+  const int32_t *seq_cap_h;   /* host [B]: slab rows (the budget) */
+  const int32_t *seq_len_h;   /* host [B]: committed rows L_b before this step */
+} specmemo_kv;
+
+/* (a) Medusa-head projection and top-k tree assembly (Sec. 3.1: l heads read
+ * the last hidden state, head i's top-k tokens fill tree level i+1; Eq. 2).
+ *
+ *   z[b][i][v] = sum_c head_w[i][v][c] * h[b][c]     (fp32 accumulation)
+ *   topk_ids[b][i][0..topk_h[i]) = the topk_h[i] largest z[b][i][:], larger
+ *       value first, equal values by lower token id; entries past topk_h[i]
+ *       are set to -1 (values to -inf)
+ *   node_tok[node_off[b]] = root_tok[b];
+ *   node_tok[node_off[b] + n] = topk_ids[b][depth[n]-1][rank[n]]  (n > 0)
+ *
+ * h: device [B][hidden]; head_w: device [n_heads][vocab][hidden] (row-major,
+ * the nn.Linear out x in layout, no bias); both in `dt`.  root_tok: device [B]
+ * (the base model's own next token from the previous step).  logits_out:
+ * device fp32 [B][n_heads][vocab], or NULL.  topk_ids: device int32
+ * [B][n_heads][kmax] with kmax = max(topk_h); topk_vals: device fp32, same
+ * shape, or NULL.  node_tok: device int32 [sum N_b].  Requires hidden % 8 == 0,
+ * 1 <= n_heads <= SPECMEMO_MAX_DEPTH, 1 <= topk_h[i] <= min(SPECMEMO_MAX_TOPK,
+ * vocab), tree depth <= n_heads and rank[n] < topk_h[depth[n]-1].
+ * ws: at least specmemo_workspace_bytes(SPECMEMO_WS_TOPK, ...) bytes. */
+int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hidden,
+                         int32_t vocab, int32_t n_heads, const int32_t *topk_h, const void *h,
+                         const void *head_w, const int32_t *root_tok, float *logits_out,
+                         int32_t *topk_ids, float *topk_vals, int32_t *node_tok, void *ws,
+                         size_t ws_bytes, void *stream);
+
+/* (b) Tree-masked attention of one layer (Sec. 3.1: before verification the
+ * mask assumes full acceptance of every candidate sequence, so a node attends
+ * to its root path; App. A.1: one forward over all candidates; Sec. 3.3: a
+ * ragged batch, here without padding).
+ *
+ * For node n of sequence b and query head hq, with KV head kv = hq / (n_q/n_kv):
+ *   keys  = slab rows 0..L_b-1 (committed) and L_b + j for every j on the
+ *           path root..n (inclusive)
+ *   out[node][hq] = softmax(scale * q[node][hq] . K[kv][key]) . V[kv][key]
+ * q, out: device [sum N_b][n_q][head_dim] in `dt`.  scale <= 0 selects
+ * 1/sqrt(head_dim).  bf16 requires head_dim == 128; fp32 requires
+ * head_dim <= 128 and head_dim % 4 == 0.  n_q % n_kv == 0.  Rows of the slab
+ * past L_b + N_b are never read.  ws: at least
+ * specmemo_workspace_bytes(SPECMEMO_WS_ATTN, ...) bytes (may be 0). */
+int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
+                       int32_t n_q, float scale, const void *q, void *out, void *ws,
+                       size_t ws_bytes, void *stream);
+
+/* (c) Acceptance (App. A.1: each candidate token must pass a threshold,
+ * verification is cumulative along the sequence, the longest verified
+ * candidate is accepted; Sec. 3.2: verification of a continuation is
+ * cumulative).  base_logits: device [sum N_b][vocab] in `dt`, row u = the
+ * base model's next-token logits after node u.  node_tok: device int32.
+ *
+ * GREEDY:  a[u] = argmax_v base_logits[u][v] (ties: lower v).  From the root,
+ *          move to the child c with node_tok[c] == a[cur] while one exists.
+ * TYPICAL: pi_u = softmax(base_logits[u] / temperature), H_u its entropy;
+ *          edge u->c passes iff pi_u[node_tok[c]] > min(eps, delta*exp(-H_u));
+ *          a node is accepted iff every edge on its root path passes; the
+ *          deepest accepted node wins, ties by larger sum of log pi along the
+ *          path, then lower node id.
+ * Outputs (device int32): accept_len[B] = depth of the chosen node (the root
+ * is always accepted; tau = accept_len + 1); path[B][path_stride] = local
+ * node ids root..chosen, -1 padded, path_stride >= max tree depth + 1;
+ * next_tok[B] = argmax of the chosen node's row (ties: lower id).
+ * ws: SPECMEMO_WS_ACCEPT bytes (0 in greedy mode). */
+int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab,
+                    specmemo_accept_mode mode, float temperature, float eps, float delta,
+                    const void *base_logits, const int32_t *node_tok, int32_t *accept_len,
+                    int32_t *path, int32_t path_stride, int32_t *next_tok, void *ws,
+                    size_t ws_bytes, void *stream);
+
+/* (d) In-place KV compaction (Sec. 3.1 KV-cache paragraph: the preallocated
+ * cache is a scratch space updated during verification; Sec. 3.3: rejected
+ * candidates are discarded).  For every sequence b, KV head and both K and V:
+ *   slab row L_b + j <- slab row L_b + path[b][j],  j = 0..accept_len[b]
+ * with all sources read before any destination is written, then
+ *   kv->seq_len[b] = L_b + accept_len[b] + 1   (device).
+ * Rows below L_b and all other slabs are untouched; slab rows past the new
+ * length are scratch.  accept_len / path are the device outputs of
+ * specmemo_accept.  A sequence whose accept_len or path entries are out of
+ * range (negative, past its tree, or not increasing) is left untouched,
+ * including its seq_len. */
+int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
+                        const int32_t *accept_len, const int32_t *path, int32_t path_stride,
+                        void *stream);
+
+#define SPECMEMO_WS_TOPK 0
+#define SPECMEMO_WS_ATTN 1
+#define SPECMEMO_WS_ACCEPT 2
+
+/* Workspace bytes a call needs for these arguments (host-only; no HIP call).
+ *   SPECMEMO_WS_TOPK:   kv ignored; n_q_or_heads = n_heads; vocab used.
+ *   SPECMEMO_WS_ATTN:   kv required; n_q_or_heads = n_q; vocab ignored.
+ *   SPECMEMO_WS_ACCEPT: kv ignored; n_q_or_heads = accept mode; vocab ignored.
+ * Returns 0 for invalid arguments as well as when no workspace is needed;
+ * the call itself reports invalid arguments. */
+size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo_trees *t,
+                                const specmemo_kv *kv, int32_t n_q_or_heads, int32_t vocab);
+
+/* Description of the last failure on the calling thread (library-owned,
+ * valid until the thread's next call), or "" after a success. */
+const char *specmemo_last_error(void);
+
+/* SPECMEMO_ABI_VERSION of the loaded library. */
+int32_t specmemo_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECMEMO_H */

@@ -1,0 +1,308 @@
+/*
+ * CPU oracle for the SpecMemo tree-verification step.  TEST INFRASTRUCTURE.
+ *
+ * Plain, slow, obviously correct fp64 loops for the four stages of one
+ * speculative verify step.  Only the test-suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library; the product path never
+ * does.  It shares no code, header or table with the HIP library.
+ *
+ * Stored inputs are fp32 or bf16 (raw 16-bit patterns); every value is widened
+ * exactly to double before use, so the oracle sees the operands the GPU sees.
+ *
+ * Stages and the passages they follow (SpecMemo, arXiv 2506.01986):
+ *   head logits  - Sec. 3.1 (l parallel heads read the last hidden state;
+ *                  heads are plain linear maps hidden -> vocab),
+ *   top-k        - Sec. 3.1 / Sec. 3.2 (tree arity k = top-k per head),
+ *   tree tokens  - Sec. 3.1 Eq. 2 (level i of the tree holds head i's top-k),
+ *   tree attention - Sec. 3.1 (before verification the mask assumes every
+ *                  candidate sequence is fully accepted: a node sees its
+ *                  ancestors and itself) and App. A.1 (one forward over all
+ *                  candidates), with scaled dot-product attention,
+ *   acceptance   - App. A.1 (threshold per token, cumulative along the path,
+ *                  longest verified candidate wins; typical sampling) and
+ *                  Sec. 3.2 (verification of a continuation is cumulative),
+ *   compaction   - Sec. 3.1 KV-cache paragraph (the preallocated cache is a
+ *                  scratch space updated during verification) and Sec. 3.3
+ *                  (rejected candidates are discarded).
+ *
+ * Readings where the paper is silent: ties in top-k and argmax go to the
+ * lower token id; the root token is always accepted and its K/V is tree row 0;
+ * accept_len counts non-root nodes; a typical-mode edge u->c is accepted iff
+ * softmax(z_u/T)[tok c] > min(eps, delta * exp(-H_u)); among the deepest
+ * accepted nodes the larger summed log-probability wins, then the lower id.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define OR_FP32 0
+#define OR_BF16 1
+
+static double widen(const void *p, int dt, int64_t i) {
+  if (dt == OR_FP32) return (double)((const float *)p)[i];
+  uint32_t bits = (uint32_t)((const uint16_t *)p)[i] << 16;
+  float f;
+  memcpy(&f, &bits, sizeof f);
+  return (double)f;
+}
+
+/* Order of (value, id) pairs used by top-k and argmax: larger value first,
+ * equal values by lower id. */
+static int better(double va, int ia, double vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+
+/* ---- head logits: z[s][i][v] = sum_c W[i][v][c] * h[b_s][c] ------------- */
+void oracle_head_logits(int dt, int B, int hidden, int vocab, int n_heads, const void *h,
+                        const void *W, int nsel, const int *bsel, double *z) {
+  int nb = bsel ? nsel : B;
+  double *hd = (double *)malloc(sizeof(double) * (size_t)nb * hidden);
+  for (int s = 0; s < nb; ++s) {
+    int b = bsel ? bsel[s] : s;
+    for (int c = 0; c < hidden; ++c) hd[(size_t)s * hidden + c] = widen(h, dt, (int64_t)b * hidden + c);
+  }
+#pragma omp parallel
+  {
+    double *row = (double *)malloc(sizeof(double) * hidden);
+#pragma omp for schedule(static)
+    for (int64_t iv = 0; iv < (int64_t)n_heads * vocab; ++iv) {
+      int i = (int)(iv / vocab), v = (int)(iv % vocab);
+      for (int c = 0; c < hidden; ++c) row[c] = widen(W, dt, iv * hidden + c);
+      for (int s = 0; s < nb; ++s) {
+        double acc = 0.0;
+        for (int c = 0; c < hidden; ++c) acc += row[c] * hd[(size_t)s * hidden + c];
+        z[((int64_t)s * n_heads + i) * vocab + v] = acc;
+      }
+    }
+    free(row);
+  }
+  free(hd);
+}
+
+/* ---- top-k of each row by repeated selection ------------------------------ */
+void oracle_topk(int nrows, int vocab, int k, const double *z, int *ids, double *vals) {
+#pragma omp parallel for schedule(static)
+  for (int r = 0; r < nrows; ++r) {
+    const double *x = z + (int64_t)r * vocab;
+    int prev = -1;
+    for (int j = 0; j < k; ++j) {
+      int best = -1;
+      for (int v = 0; v < vocab; ++v) {
+        if (prev >= 0 && !better(x[prev], prev, x[v], v)) continue; /* already taken */
+        if (best < 0 || better(x[v], v, x[best], best)) best = v;
+      }
+      ids[(int64_t)r * k + j] = best;
+      if (vals) vals[(int64_t)r * k + j] = best >= 0 ? x[best] : -INFINITY;
+      prev = best;
+    }
+  }
+}
+
+/* ---- tree tokens: root = root_tok, node n = topk_ids[b][depth-1][rank] ---- */
+void oracle_tree_tokens(int B, const int *node_off, const int *depth, const int *rank,
+                        const int *root_tok, int n_heads, int kmax, const int *topk_ids,
+                        int *node_tok) {
+  for (int b = 0; b < B; ++b)
+    for (int n = node_off[b]; n < node_off[b + 1]; ++n) {
+      if (n == node_off[b]) {
+        node_tok[n] = root_tok[b];
+      } else {
+        int i = depth[n] - 1;
+        node_tok[n] = topk_ids[((int64_t)b * n_heads + i) * kmax + rank[n]];
+      }
+    }
+}
+
+/* ---- tree-masked attention ------------------------------------------------
+ * Node n (local id) of sequence b, query head h, KV head kv = h / (n_q/n_kv):
+ * keys are the L_b committed rows and the tree rows L_b + j for every j on the
+ * path from the root to n (both ends included).  out = softmax(scale * q K^T) V.
+ * sel: nsel (global node, head) pairs, or NULL for every (node, head). */
+static int seq_of(int B, const int *node_off, int node) {
+  for (int b = 0; b < B; ++b)
+    if (node < node_off[b + 1]) return b;
+  return -1;
+}
+
+void oracle_tree_attn(int dt, int B, const int *node_off, const int *parent, const int *seq_len,
+                      const int64_t *seq_base, int n_q, int n_kv, int d, int64_t cap_total,
+                      double scale, const void *q, const void *K, const void *V, int nsel,
+                      const int *sel, double *out) {
+  int total = node_off[B];
+  int64_t nrows = sel ? nsel : (int64_t)total * n_q;
+  int group = n_q / n_kv;
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int64_t r = 0; r < nrows; ++r) {
+    int node = sel ? sel[2 * r] : (int)(r / n_q);
+    int h = sel ? sel[2 * r + 1] : (int)(r % n_q);
+    int b = seq_of(B, node_off, node);
+    int n = node - node_off[b];
+    int L = seq_len[b];
+    int kv = h / group;
+    /* key rows: committed, then the ancestors-or-self of n */
+    int nanc = 0, anc[256];
+    for (int a = n; a >= 0; a = parent[node_off[b] + a]) anc[nanc++] = a;
+    int nkeys = L + nanc;
+    int64_t *rows = (int64_t *)malloc(sizeof(int64_t) * nkeys);
+    for (int t = 0; t < L; ++t) rows[t] = seq_base[b] + t;
+    for (int j = 0; j < nanc; ++j) rows[L + j] = seq_base[b] + L + anc[j];
+    double *s = (double *)malloc(sizeof(double) * nkeys);
+    double m = -INFINITY;
+    for (int t = 0; t < nkeys; ++t) {
+      double acc = 0.0;
+      for (int e = 0; e < d; ++e)
+        acc += widen(q, dt, ((int64_t)node * n_q + h) * d + e) *
+               widen(K, dt, ((int64_t)kv * cap_total + rows[t]) * d + e);
+      s[t] = scale * acc;
+      if (s[t] > m) m = s[t];
+    }
+    double zsum = 0.0;
+    for (int t = 0; t < nkeys; ++t) {
+      s[t] = exp(s[t] - m);
+      zsum += s[t];
+    }
+    for (int e = 0; e < d; ++e) {
+      double acc = 0.0;
+      for (int t = 0; t < nkeys; ++t) acc += s[t] * widen(V, dt, ((int64_t)kv * cap_total + rows[t]) * d + e);
+      out[r * d + e] = acc / zsum;
+    }
+    free(s);
+    free(rows);
+  }
+}
+
+/* ---- acceptance -------------------------------------------------------------
+ * Greedy: a[u] = argmax of node u's base-model row (lowest id on ties).  From
+ * the root, move to the child whose token equals a[cur] while one exists.
+ * accept_len = depth reached, path = root..cur (local ids, -1 padded),
+ * next_tok = a[cur]. */
+static int row_argmax(int dt, const void *logits, int64_t row, int vocab) {
+  int best = 0;
+  double bv = widen(logits, dt, row * vocab);
+  for (int v = 1; v < vocab; ++v) {
+    double x = widen(logits, dt, row * vocab + v);
+    if (better(x, v, bv, best)) {
+      best = v;
+      bv = x;
+    }
+  }
+  return best;
+}
+
+void oracle_accept_greedy(int dt, int B, const int *node_off, const int *parent, const int *depth,
+                          int vocab, const void *logits, const int *node_tok, int path_stride,
+                          int *accept_len, int *path, int *next_tok) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int b = 0; b < B; ++b) {
+    int o = node_off[b], N = node_off[b + 1] - o;
+    int cur = 0, len = 0;
+    int *pb = path + (int64_t)b * path_stride;
+    for (int j = 0; j < path_stride; ++j) pb[j] = -1;
+    pb[0] = 0;
+    int a = row_argmax(dt, logits, o + cur, vocab);
+    for (;;) {
+      int nxt = -1;
+      for (int c = 1; c < N; ++c)
+        if (parent[o + c] == cur && node_tok[o + c] == a) nxt = c;
+      if (nxt < 0) break;
+      cur = nxt;
+      pb[++len] = cur;
+      a = row_argmax(dt, logits, o + cur, vocab);
+    }
+    (void)depth;
+    accept_len[b] = len;
+    next_tok[b] = a;
+  }
+}
+
+/* Typical: pi_u = softmax(z_u / T), H_u = -sum pi_u log pi_u.  Edge u->c is
+ * accepted iff pi_u[tok c] > min(eps, delta * exp(-H_u)); a node is accepted
+ * iff every edge on its root path is.  The deepest accepted node wins; ties go
+ * to the larger sum of log pi along the path, then the lower node id.
+ * next_tok = argmax z_cur.  Optional per-node outputs (index = global node,
+ * root entries unused): log pi of the edge into the node and the log threshold
+ * of that edge. */
+void oracle_accept_typical(int dt, int B, const int *node_off, const int *parent, const int *depth,
+                           int vocab, const void *logits, const int *node_tok, double temperature,
+                           double eps, double delta, int path_stride, int *accept_len, int *path,
+                           int *next_tok, double *edge_logpi, double *edge_logthr) {
+  int total = node_off[B];
+  double *lse = (double *)malloc(sizeof(double) * total);
+  double *ent = (double *)malloc(sizeof(double) * total);
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int u = 0; u < total; ++u) {
+    double m = -INFINITY;
+    for (int v = 0; v < vocab; ++v) {
+      double x = widen(logits, dt, (int64_t)u * vocab + v) / temperature;
+      if (x > m) m = x;
+    }
+    double zs = 0.0;
+    for (int v = 0; v < vocab; ++v) zs += exp(widen(logits, dt, (int64_t)u * vocab + v) / temperature - m);
+    double l = m + log(zs);
+    double hsum = 0.0;
+    for (int v = 0; v < vocab; ++v) {
+      double lp = widen(logits, dt, (int64_t)u * vocab + v) / temperature - l;
+      hsum -= exp(lp) * lp;
+    }
+    lse[u] = l;
+    ent[u] = hsum;
+  }
+  for (int b = 0; b < B; ++b) {
+    int o = node_off[b], N = node_off[b + 1] - o;
+    int *acc = (int *)malloc(sizeof(int) * N);
+    double *score = (double *)malloc(sizeof(double) * N);
+    acc[0] = 1;
+    score[0] = 0.0;
+    int best = 0;
+    for (int c = 1; c < N; ++c) {
+      int u = parent[o + c];
+      double lp = widen(logits, dt, (int64_t)(o + u) * vocab + node_tok[o + c]) / temperature - lse[o + u];
+      double thr = eps < delta * exp(-ent[o + u]) ? eps : delta * exp(-ent[o + u]);
+      if (edge_logpi) edge_logpi[o + c] = lp;
+      if (edge_logthr) edge_logthr[o + c] = log(thr);
+      acc[c] = acc[u] && (exp(lp) > thr);
+      score[c] = score[u] + lp;
+      if (acc[c]) {
+        if (depth[o + c] > depth[o + best] ||
+            (depth[o + c] == depth[o + best] && score[c] > score[best]))
+          best = c; /* nodes are visited in increasing id: equal keys keep the lower id */
+      }
+    }
+    int *pb = path + (int64_t)b * path_stride;
+    for (int j = 0; j < path_stride; ++j) pb[j] = -1;
+    int len = depth[o + best];
+    for (int a = best, j = len; a >= 0; a = parent[o + a], --j) pb[j] = a;
+    accept_len[b] = len;
+    next_tok[b] = row_argmax(dt, logits, o + best, vocab);
+    free(acc);
+    free(score);
+  }
+  free(lse);
+  free(ent);
+}
+
+/* ---- in-place KV compaction -------------------------------------------------
+ * For j = 0..accept_len: slab row L_b + j <- slab row L_b + path[j] (K and V,
+ * every KV head): all sources are read before any destination is written.
+ * Then seq_len[b] += accept_len + 1.  Rows are copied as raw bytes. */
+void oracle_kv_compact(int elem_bytes, int B, int n_kv, int d, int64_t cap_total, uint8_t *K,
+                       uint8_t *V, const int64_t *seq_base, int *seq_len, const int *accept_len,
+                       const int *path, int path_stride) {
+  size_t rb = (size_t)elem_bytes * d;
+  uint8_t *tmp = (uint8_t *)malloc(rb * (size_t)path_stride);
+  for (int b = 0; b < B; ++b) {
+    int L = seq_len[b], a = accept_len[b];
+    const int *pb = path + (int64_t)b * path_stride;
+    for (int kv = 0; kv < n_kv; ++kv) {
+      uint8_t *pools[2] = {K, V};
+      for (int w = 0; w < 2; ++w) {
+        uint8_t *slab = pools[w] + ((size_t)kv * cap_total + seq_base[b]) * rb;
+        for (int j = 0; j <= a; ++j) memcpy(tmp + j * rb, slab + (size_t)(L + pb[j]) * rb, rb);
+        for (int j = 0; j <= a; ++j) memcpy(slab + (size_t)(L + j) * rb, tmp + j * rb, rb);
+      }
+    }
+    seq_len[b] = L + a + 1;
+  }
+  free(tmp);
+}

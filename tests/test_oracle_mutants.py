@@ -1,0 +1,75 @@
+"""The pins are sensitive: plausible mistakes planted in a copy of the oracle
+(compiled on the CPU into a temporary library) must each fail a pin test."""
+
+import os
+import subprocess
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+# (name, exact text in the oracle source, replacement, pin tests expected to fail)
+MUTANTS = [
+    ("self_not_in_mask", "for (int a = n; a >= 0; a = parent[node_off[b] + a])",
+     "for (int a = parent[node_off[b] + n]; a >= 0; a = parent[node_off[b] + a])",
+     ["test_random_trees_match_masked_sdpa"]),
+    ("gqa_mapping", "int kv = h / group;", "int kv = h % n_kv;",
+     ["test_gqa_equals_mha_with_repeated_kv"]),
+    ("scale_dropped", "s[t] = scale * acc;", "s[t] = acc;",
+     ["test_chain_tree_is_causal_attention"]),
+    ("values_from_keys", "acc += s[t] * widen(V, dt,", "acc += s[t] * widen(K, dt,",
+     ["test_single_node_is_decode_attention"]),
+    ("tie_to_higher_id", "(va == vb && ia < ib)", "(va == vb && ia > ib)",
+     ["test_topk_equals_stable_sort_with_ties", "test_greedy_acceptance_equals_brute_force"]),
+    ("operand_reversed", "row[c] = widen(W, dt, iv * hidden + c);",
+     "row[c] = widen(W, dt, iv * hidden + (hidden - 1 - c));",
+     ["test_head_logits_equal_float64_matmul"]),
+    ("rank_reversed", "* kmax + rank[n]];", "* kmax + (kmax - 1 - rank[n])];",
+     ["test_tree_tokens_level_i_holds_head_i"]),
+    ("threshold_max", "double thr = eps < delta", "double thr = eps > delta",
+     ["test_typical_acceptance_equals_brute_force"]),
+    ("entropy_sign", "hsum -= exp(lp) * lp;", "hsum += exp(lp) * lp;",
+     ["test_typical_acceptance_equals_brute_force"]),
+    ("no_move", "slab + (size_t)(L + pb[j]) * rb", "slab + (size_t)(L + j) * rb",
+     ["test_compaction_moves_accepted_rows_only"]),
+    ("seq_len_off_by_one", "seq_len[b] = L + a + 1;", "seq_len[b] = L + a;",
+     ["test_compaction_moves_accepted_rows_only"]),
+]
+
+
+def _call(name):
+    fn = getattr(pins, name)
+    marks = getattr(fn, "pytestmark", [])
+    params = [m for m in marks if m.name == "parametrize"]
+    if not params:
+        fn()
+        return
+    argnames = [a.strip() for a in params[0].args[0].split(",")]
+    for values in params[0].args[1]:
+        values = values if isinstance(values, tuple) else (values,)
+        fn(**dict(zip(argnames, values)))
+
+
+@pytest.mark.parametrize("name,old,new,tests", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, old, new, tests):
+    src = open(oracle.SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique"
+    mut = tmp_path / "mut.c"
+    mut.write_text(src.replace(old, new))
+    so = tmp_path / "libmut.so"
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-o", str(so),
+                           str(mut), "-lm"])
+    import ctypes
+    saved = oracle._lib
+    oracle._lib = ctypes.CDLL(str(so))
+    try:
+        caught = False
+        for t in tests:
+            try:
+                _call(t)
+            except AssertionError:
+                caught = True
+        assert caught, f"mutant {name} passed {tests}"
+    finally:
+        oracle._lib = saved

@@ -1,0 +1,392 @@
+"""Pins of the CPU oracle to facts that do not come from the oracle itself.
+
+Each stage is checked against a closed form, a library routine applied to a
+special case, an invariant, or brute-force enumeration on tiny inputs, so that
+a dropped term, a wrong sign or index, or a transposed operand fails a test.
+"""
+
+import itertools
+
+import numpy as np
+import pytest
+import scipy.special
+import scipy.stats
+import torch
+
+import oracle
+from paper_2506_01986_amd import configs, synth
+
+
+def small_cfg(dtype="fp32", B=2, n_q=4, n_kv=2, d=16, vocab=64, hidden=32, n_heads=4,
+              topk=(4, 3, 2, 2), seed=123):
+    return configs.Config(name="pin", dtype=dtype, B=B, n_q=n_q, n_kv=n_kv, head_dim=d,
+                          hidden=hidden, vocab=vocab, n_heads=n_heads, topk=topk, tree="T16",
+                          kv_len=(8, 8), seed=seed, w_std=1.0)
+
+
+def f64(x, dt):
+    return synth.storage_to_f64(x, dt)
+
+
+# ----------------------------------------------------------------------------
+# head logits and top-k
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_head_logits_equal_float64_matmul(dtype):
+    cfg = small_cfg(dtype=dtype, B=3, hidden=48, vocab=37, n_heads=3, topk=(4, 2, 2))
+    wl = synth.make(cfg, trees=[synth.t16()] * 3, lens=[5, 6, 7])
+    z = oracle.head_logits(wl.hidden, wl.head_w)
+    ref = np.matmul(f64(wl.hidden, dtype)[:, None, None, :],
+                    np.swapaxes(f64(wl.head_w, dtype), 1, 2)[None]).squeeze(2)
+    assert z.shape == (3, 3, 37)
+    assert np.allclose(z, ref, rtol=1e-12, atol=1e-12)
+    zs = oracle.head_logits(wl.hidden, wl.head_w, bsel=[2, 0])
+    assert np.array_equal(zs, z[[2, 0]])
+
+
+def test_topk_equals_stable_sort_with_ties():
+    rng = np.random.default_rng(0)
+    z = rng.integers(0, 6, size=(50, 40)).astype(np.float64)   # many equal values
+    z[:5] = rng.standard_normal((5, 40))
+    ids, vals = oracle.topk(z, 7)
+    ref = np.argsort(-z, axis=1, kind="stable")[:, :7]
+    assert np.array_equal(ids, ref)
+    assert np.array_equal(vals, np.take_along_axis(z, ref, 1))
+
+
+def test_topk_full_width():
+    z = np.array([[3.0, 1.0, 3.0, 2.0]])
+    ids, _ = oracle.topk(z, 4)
+    assert ids.tolist() == [[0, 2, 3, 1]]
+
+
+@pytest.mark.parametrize("tree,topk", [("T16", (4, 2, 2)), ("T64", (10, 10, 10, 10))])
+def test_tree_tokens_level_i_holds_head_i(tree, topk):
+    t = synth.t16() if tree == "T16" else synth.t64()
+    cfg = small_cfg(B=2, vocab=90, n_heads=len(topk), topk=topk)
+    wl = synth.make(cfg, trees=[t, t], lens=[4, 4])
+    z = oracle.head_logits(wl.hidden, wl.head_w)
+    ids, _ = oracle.heads_topk(z, topk, max(topk))
+    tok = oracle.tree_tokens(wl.node_off, wl.depth, wl.rank, wl.root_tok, ids)
+    for b in range(2):
+        o = wl.node_off[b]
+        assert tok[o] == wl.root_tok[b]
+        level1 = [n for n in range(t.n) if t.depth[n] == 1]
+        # the root's children, in BFS order, carry head 0's top-k in decreasing logit order
+        assert tok[o + np.array(level1)].tolist() == \
+            np.argsort(-z[b, 0], kind="stable")[:len(level1)].tolist()
+        for n in range(1, t.n):
+            if t.rank[n] == 0:     # rank 0 at depth i is head i-1's argmax
+                assert tok[o + n] == int(np.argmax(z[b, t.depth[n] - 1]))
+
+
+# ----------------------------------------------------------------------------
+# tree attention
+# ----------------------------------------------------------------------------
+
+def ancestor_closure(parent):
+    """anc_or_self[n, j] via powers of the child->parent adjacency matrix."""
+    n = len(parent)
+    P = np.zeros((n, n))
+    for c in range(1, n):
+        P[c, parent[c]] = 1.0
+    R, M = np.eye(n), np.eye(n)
+    for _ in range(n):
+        M = M @ P
+        R += M
+    return R > 0
+
+
+def sdpa(Q, K, V, mask):
+    out = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(Q)[None, None], torch.from_numpy(K)[None, None],
+        torch.from_numpy(V)[None, None], attn_mask=torch.from_numpy(mask))
+    return out[0, 0].numpy()
+
+
+def sdpa_tree(wl, b, h, tree_mask):
+    cfg = wl.cfg
+    kv = h // (cfg.n_q // cfg.n_kv)
+    o, N, L, s0 = int(wl.node_off[b]), wl.trees[b].n, int(wl.lens[b]), int(wl.seq_base[b])
+    dt = cfg.dtype
+    Q = f64(wl.q[o:o + N, h, :], dt)
+    K = f64(wl.pool_k[kv, s0:s0 + L + N, :], dt)
+    V = f64(wl.pool_v[kv, s0:s0 + L + N, :], dt)
+    mask = np.concatenate([np.ones((N, L), bool), tree_mask], axis=1)
+    return sdpa(Q, K, V, mask)
+
+
+def run_attn(wl, **kw):
+    return oracle.tree_attn(wl.q, wl.pool_k, wl.pool_v, wl.node_off, wl.parent, wl.lens,
+                            wl.seq_base, wl.cfg.n_kv, **kw)
+
+
+@pytest.mark.parametrize("dtype,n_q,n_kv", [("fp32", 4, 4), ("bf16", 8, 2)])
+def test_chain_tree_is_causal_attention(dtype, n_q, n_kv):
+    N = 5
+    cfg = small_cfg(dtype=dtype, B=2, n_q=n_q, n_kv=n_kv)
+    wl = synth.make(cfg, trees=[synth.chain_tree(N)] * 2, lens=[9, 0])
+    out = run_attn(wl)
+    causal = np.tril(np.ones((N, N), bool))
+    for b in range(2):
+        for h in range(n_q):
+            ref = sdpa_tree(wl, b, h, causal)
+            o = wl.node_off[b]
+            assert np.allclose(out[o:o + N, h], ref, rtol=1e-12, atol=1e-13)
+
+
+def test_single_node_is_decode_attention():
+    cfg = small_cfg(B=3, n_q=4, n_kv=1)
+    wl = synth.make(cfg, trees=[synth.tree_from_rank_paths([()])] * 3, lens=[1, 13, 40])
+    out = run_attn(wl)
+    for b in range(3):
+        L, s0 = int(wl.lens[b]), int(wl.seq_base[b])
+        for h in range(4):
+            Q = wl.q[b:b + 1, h].astype(np.float64)
+            K = wl.pool_k[0, s0:s0 + L + 1].astype(np.float64)
+            V = wl.pool_v[0, s0:s0 + L + 1].astype(np.float64)
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                *(torch.from_numpy(x)[None, None] for x in (Q, K, V)))[0, 0].numpy()
+            assert np.allclose(out[b, h], ref[0], rtol=1e-12, atol=1e-13)
+
+
+def test_star_tree_node_sees_root_and_itself():
+    N = 7
+    cfg = small_cfg(B=1, n_q=2, n_kv=2, topk=(8, 2, 2, 2))
+    wl = synth.make(cfg, trees=[synth.star_tree(N)], lens=[6])
+    out = run_attn(wl)
+    mask = np.eye(N, dtype=bool)
+    mask[:, 0] = True
+    for h in range(2):
+        assert np.allclose(out[:, h], sdpa_tree(wl, 0, h, mask), rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("n", [3, 16, 64, 128])
+def test_random_trees_match_masked_sdpa(n):
+    rng = np.random.default_rng(n)
+    trees = [synth.random_tree(rng, n), synth.random_tree(rng, max(1, n // 2))]
+    cfg = small_cfg(dtype="bf16", B=2, n_q=4, n_kv=2, topk=(10,) * 4)
+    wl = synth.make(cfg, trees=trees, lens=[3, 17])
+    out = run_attn(wl)
+    for b in range(2):
+        m = ancestor_closure(wl.trees[b].parent)
+        o, N = wl.node_off[b], wl.trees[b].n
+        for h in range(4):
+            assert np.allclose(out[o:o + N, h], sdpa_tree(wl, b, h, m), rtol=1e-12, atol=1e-13)
+
+
+def test_gqa_equals_mha_with_repeated_kv():
+    cfg = small_cfg(dtype="bf16", B=2, n_q=8, n_kv=2)
+    wl = synth.make(cfg, trees=[synth.t16(), synth.random_tree(np.random.default_rng(1), 9)],
+                    lens=[11, 4])
+    out = run_attn(wl)
+    K = np.ascontiguousarray(np.repeat(wl.pool_k, 4, axis=0))   # kv head j -> q heads 4j..4j+3
+    V = np.ascontiguousarray(np.repeat(wl.pool_v, 4, axis=0))
+    out_mha = oracle.tree_attn(wl.q, K, V, wl.node_off, wl.parent, wl.lens, wl.seq_base, 8)
+    assert np.array_equal(out, out_mha)
+
+
+def test_committed_row_permutation_invariance():
+    cfg = small_cfg(B=1)
+    wl = synth.make(cfg, trees=[synth.t16()], lens=[12])
+    out = run_attn(wl)
+    s0 = int(wl.seq_base[0])
+    perm = np.random.default_rng(3).permutation(12)
+    for pool in (wl.pool_k, wl.pool_v):
+        pool[:, s0:s0 + 12] = pool[:, s0 + perm]
+    assert np.allclose(run_attn(wl), out, rtol=1e-12, atol=1e-13)
+
+
+def test_uniform_values_give_uniform_output():
+    cfg = small_cfg(B=2)
+    wl = synth.make(cfg, trees=[synth.t16(), synth.chain_tree(4)], lens=[5, 0])
+    for b in range(2):
+        s0, L, N = int(wl.seq_base[b]), int(wl.lens[b]), wl.trees[b].n
+        wl.pool_v[:, s0:s0 + L + N] = 1.0
+    assert np.allclose(run_attn(wl), 1.0, rtol=0, atol=1e-14)
+
+
+def test_common_key_shift_invariance():
+    cfg = small_cfg(B=1)
+    wl = synth.make(cfg, trees=[synth.t16()], lens=[10])
+    out = run_attn(wl)
+    s0 = int(wl.seq_base[0])
+    u = np.random.default_rng(4).standard_normal((cfg.n_kv, 1, cfg.head_dim)).astype(np.float32)
+    wl.pool_k[:, s0:s0 + 10 + 16] += u      # every key of the slab moves by the same vector
+    assert np.allclose(run_attn(wl), out, rtol=1e-5, atol=1e-6)
+
+
+def test_explicit_scale_and_selection():
+    cfg = small_cfg(B=2)
+    wl = synth.make(cfg, trees=[synth.t16(), synth.chain_tree(3)], lens=[5, 2])
+    full = run_attn(wl, scale=0.3)
+    sel = np.array([[17, 3], [0, 0], [5, 1]])
+    part = run_attn(wl, scale=0.3, sel=sel)
+    for i, (n, h) in enumerate(sel):
+        assert np.array_equal(part[i], full[n, h])
+    # scale 0 makes every visible key equally likely: the output is their mean
+    z = run_attn(wl, scale=0.0)
+    s0, L = int(wl.seq_base[1]), int(wl.lens[1])
+    o = wl.node_off[1]
+    for n in range(3):                       # chain: node n sees tree rows 0..n
+        rows = list(range(L)) + [L + j for j in range(n + 1)]
+        ref = wl.pool_v[0, s0 + np.array(rows)].astype(np.float64).mean(0)
+        assert np.allclose(z[o + n, 0], ref, rtol=1e-12, atol=1e-13)
+
+
+# ----------------------------------------------------------------------------
+# acceptance
+# ----------------------------------------------------------------------------
+
+def brute_accept(logits, tok, parent, mode, T=1.0, eps=0.0, delta=0.0):
+    """Enumerate every root-to-leaf path; take its longest accepted prefix;
+    keep the best prefix by (length, sum log pi, -last node id)."""
+    N = len(parent)
+    kids = {u: [c for c in range(N) if parent[c] == u] for u in range(N)}
+    leaves = [u for u in range(N) if not kids[u]]
+    logp = logits / T - scipy.special.logsumexp(logits / T, axis=1, keepdims=True)
+    ent = scipy.stats.entropy(scipy.special.softmax(logits / T, axis=1), axis=1)
+    best = None
+    for leaf in leaves:
+        p = [leaf]
+        while p[-1] != 0:
+            p.append(parent[p[-1]])
+        p = p[::-1]
+        j, score = 0, 0.0
+        for u, c in zip(p[:-1], p[1:]):
+            if mode == "greedy":
+                ok = int(np.argmax(logits[u])) == tok[c]
+            else:
+                ok = np.exp(logp[u, tok[c]]) > min(eps, delta * np.exp(-ent[u]))
+            if not ok:
+                break
+            j += 1
+            score += logp[u, tok[c]]
+        key = (j, score if mode == "typical" else 0.0, -p[j])
+        if best is None or key > best[0]:
+            best = (key, p[:j + 1])
+    path = best[1]
+    return len(path) - 1, path, int(np.argmax(logits[path[-1]]))
+
+
+def tiny_case(rng, vocab, int_logits):
+    n = int(rng.integers(1, 13))
+    t = synth.random_tree(rng, n, max_depth=4, max_kids=min(4, vocab))
+    tok = np.zeros(n, np.int32)
+    tok[0] = rng.integers(vocab)
+    for u in range(n):
+        kids = synth.children(t, u)
+        tok[kids] = rng.choice(vocab, size=len(kids), replace=False)
+    if int_logits:
+        lg = rng.integers(0, 3, size=(n, vocab)).astype(np.float32)
+    else:
+        lg = (2.0 * rng.standard_normal((n, vocab))).astype(np.float32)
+    return t, tok, lg
+
+
+@pytest.mark.parametrize("int_logits", [True, False])
+def test_greedy_acceptance_equals_brute_force(int_logits):
+    rng = np.random.default_rng(11 + int_logits)
+    for _ in range(300):
+        vocab = int(rng.integers(2, 7))
+        t, tok, lg = tiny_case(rng, vocab, int_logits)
+        acc, path, nxt = oracle.accept_greedy(lg, tok, [0, t.n], t.parent, t.depth, 6)
+        ra, rp, rn = brute_accept(lg.astype(np.float64), tok, t.parent, "greedy")
+        assert acc[0] == ra and nxt[0] == rn
+        assert path[0, :ra + 1].tolist() == rp and np.all(path[0, ra + 1:] == -1)
+
+
+def test_typical_acceptance_equals_brute_force():
+    rng = np.random.default_rng(5)
+    for i in range(300):
+        vocab = int(rng.integers(3, 9))
+        t, tok, lg = tiny_case(rng, vocab, int_logits=False)
+        T, eps, delta = 0.7, float(rng.uniform(0.05, 0.4)), float(rng.uniform(0.1, 0.9))
+        acc, path, nxt = oracle.accept_typical(lg, tok, [0, t.n], t.parent, t.depth, 6, T, eps, delta)
+        ra, rp, rn = brute_accept(lg.astype(np.float64), tok, t.parent, "typical", T, eps, delta)
+        assert (acc[0], path[0, :ra + 1].tolist(), nxt[0]) == (ra, rp, rn), i
+
+
+def test_typical_tie_breaks():
+    # root -> children 1, 2 (depth 1, leaves).  Both edges pass.
+    parent = np.array([-1, 0, 0], np.int32)
+    depth = np.array([0, 1, 1], np.int32)
+    tok = np.array([0, 3, 1], np.int32)
+    lg = np.zeros((3, 6), np.float32)
+    lg[0, [1, 3]] = 4.0                  # equal probabilities: the lower node id (1) wins
+    acc, path, _ = oracle.accept_typical(lg, tok, [0, 3], parent, depth, 3, 1.0, 0.09, 0.3)
+    assert acc[0] == 1 and path[0].tolist() == [0, 1, -1]
+    lg[0, 1] = 4.5                       # node 2's token is now more likely: node 2 wins
+    acc, path, _ = oracle.accept_typical(lg, tok, [0, 3], parent, depth, 3, 1.0, 0.09, 0.3)
+    assert acc[0] == 1 and path[0].tolist() == [0, 2, -1]
+
+
+def node_tokens_distinct(wl, rng):
+    tok = np.zeros(wl.total_nodes, np.int32)
+    for b, t in enumerate(wl.trees):
+        o = wl.node_off[b]
+        tok[o] = wl.root_tok[b]
+        for u in range(t.n):
+            kids = synth.children(t, u)
+            tok[o + np.array(kids, int)] = rng.choice(wl.cfg.vocab, size=len(kids), replace=False)
+    return tok
+
+
+@pytest.mark.parametrize("mode", ["greedy", "typical"])
+def test_planted_walk_is_accepted(mode):
+    for cfg in (configs.TINY_FP32, configs.LLAMA2_13B):
+        wl = synth.make(cfg, with_heads=cfg is configs.TINY_FP32)
+        if wl.head_w is not None:
+            z = oracle.head_logits(wl.hidden, wl.head_w)
+            ids, _ = oracle.heads_topk(z, cfg.topk, cfg.kmax)
+            tok = oracle.tree_tokens(wl.node_off, wl.depth, wl.rank, wl.root_tok, ids)
+        else:
+            tok = node_tokens_distinct(wl, np.random.default_rng(0))
+        lg = synth.planted_logits(wl, tok)
+        stride = cfg.n_heads + 1
+        if mode == "greedy":
+            acc, path, nxt = oracle.accept_greedy(lg, tok, wl.node_off, wl.parent, wl.depth, stride)
+        else:
+            acc, path, nxt = oracle.accept_typical(lg, tok, wl.node_off, wl.parent, wl.depth,
+                                                   stride, 0.7, 0.09, 0.3)
+        full = synth.storage_to_f64(lg, cfg.dtype)
+        for b in range(cfg.B):
+            want = wl.plan_path[b]
+            assert acc[b] == len(want) - 1
+            assert path[b, :len(want)].tolist() == want
+            assert nxt[b] == int(np.argmax(full[wl.node_off[b] + want[-1]]))
+
+
+# ----------------------------------------------------------------------------
+# compaction
+# ----------------------------------------------------------------------------
+
+def _compaction_case(dtype):
+    cfg = small_cfg(dtype=dtype, B=3, n_kv=2, n_q=4)
+    wl = synth.make(cfg, trees=[synth.t16(), synth.chain_tree(5), synth.t16()], lens=[6, 0, 9])
+    paths = np.full((3, 5), -1, np.int32)
+    paths[0, :4] = [0, 2, 7, 14]          # overlapping: dest 2 is also the source of dest 1
+    paths[1, :5] = [0, 1, 2, 3, 4]        # identity
+    paths[2, :1] = [0]                    # root only
+    acc = np.array([3, 4, 0], np.int32)
+    return wl, acc, paths
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_compaction_moves_accepted_rows_only(dtype):
+    wl, acc, paths = _compaction_case(dtype)
+    K0, V0 = wl.pool_k.copy(), wl.pool_v.copy()
+    K, V = wl.pool_k.copy(), wl.pool_v.copy()
+    new_len = oracle.kv_compact(K, V, wl.seq_base, wl.lens, acc, paths)
+    assert new_len.tolist() == (wl.lens + acc + 1).tolist()
+    touched = np.zeros(wl.cap_total, bool)
+    for b in range(3):
+        s0, L = int(wl.seq_base[b]), int(wl.lens[b])
+        for j in range(acc[b] + 1):
+            for P, P0 in ((K, K0), (V, V0)):
+                assert np.array_equal(P[:, s0 + L + j].view(np.uint8),
+                                      P0[:, s0 + L + paths[b, j]].view(np.uint8))
+            touched[s0 + L + j] = True
+    for P, P0 in ((K, K0), (V, V0)):
+        assert np.array_equal(P[:, ~touched].view(np.uint8), P0[:, ~touched].view(np.uint8))
