@@ -1,0 +1,260 @@
+// Stage (c): acceptance of the longest verified root-to-leaf path.
+//
+// SpecMemo App. A.1: each candidate token must pass a threshold, verification
+// is cumulative along a candidate sequence and the longest verified candidate is
+// accepted; Medusa verifies with typical sampling.  Sec. 3.2: verification of a
+// continuation is cumulative.
+//
+// Greedy mode walks the tree from the root and scans only the logit rows of
+// nodes on the accepted path (at most depth + 1 rows per sequence instead of
+// all N rows), so the per-candidate retrieval buffers of the paper's memory
+// model (Eq. 3, second and third terms) are never materialised.  Typical mode
+// needs every node's softmax statistics: one block per row computes them, then
+// one block per sequence evaluates the edges and picks the path.
+#include "device.h"
+#include "internal.h"
+
+namespace specmemo {
+
+namespace {
+
+constexpr int kNT = 512;
+constexpr int kWaves = kNT / 64;
+
+template <int DT>
+__device__ __forceinline__ float ld(const void *p, int64_t i) {
+  if (DT == 0) return static_cast<const float *>(p)[i];
+  return bf16_to_f32(static_cast<const uint16_t *>(p)[i]);
+}
+
+// Arg-best (largest value, lowest id) of one logit row; result in every thread.
+template <int DT>
+__device__ void row_argbest(const void *logits, int64_t row, int vocab, float *sv, int *si,
+                            float &out_v, int &out_i) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  float bv = -INFINITY;
+  int bi = INT32_MAX;
+  const int64_t base = row * vocab;
+  if (DT == 1 && (vocab & 7) == 0) {
+    const uint4 *p = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(logits) + base);
+    for (int c = tid; c < vocab / 8; c += kNT) {
+      uint4 w = p[c];
+      uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float x = bf16_to_f32(static_cast<uint16_t>(ws[e >> 1] >> ((e & 1) * 16)));
+        int v = 8 * c + e;
+        if (better(x, v, bv, bi)) {
+          bv = x;
+          bi = v;
+        }
+      }
+    }
+  } else if (DT == 0 && (vocab & 3) == 0) {
+    const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(logits) + base);
+    for (int c = tid; c < vocab / 4; c += kNT) {
+      float4 w = p[c];
+      float ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (better(ws[e], 4 * c + e, bv, bi)) {
+          bv = ws[e];
+          bi = 4 * c + e;
+        }
+    }
+  } else {
+    for (int v = tid; v < vocab; v += kNT) {
+      float x = ld<DT>(logits, base + v);
+      if (better(x, v, bv, bi)) {
+        bv = x;
+        bi = v;
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    float ov = __shfl_xor(bv, off);
+    int oi = __shfl_xor(bi, off);
+    if (better(ov, oi, bv, bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  if (lane == 0) {
+    sv[wave] = bv;
+    si[wave] = bi;
+  }
+  __syncthreads();
+  bv = sv[0];
+  bi = si[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w)
+    if (better(sv[w], si[w], bv, bi)) {
+      bv = sv[w];
+      bi = si[w];
+    }
+  __syncthreads();
+  out_v = bv;
+  out_i = bi;
+}
+
+template <int DT>
+__global__ __launch_bounds__(kNT) void accept_greedy(AcceptArgs a) {
+  __shared__ float sv[kWaves];
+  __shared__ int si[kWaves];
+  __shared__ int s_next;
+  __shared__ int s_path[kMaxPath];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
+  int cur = 0, len = 0, tok = 0;
+  if (tid == 0) s_path[0] = 0;
+  for (;;) {
+    float v;
+    row_argbest<DT>(a.logits, n0 + cur, a.vocab, sv, si, v, tok);
+    if (tid == 0) s_next = -1;
+    __syncthreads();
+    for (int c = 1 + tid; c < N; c += kNT)
+      if (a.parent[n0 + c] == cur && a.node_tok[n0 + c] == tok) s_next = c;   // unique: sibling tokens differ
+    __syncthreads();
+    const int nxt = s_next;
+    __syncthreads();
+    if (nxt < 0 || len + 1 >= kMaxPath) break;
+    cur = nxt;
+    ++len;
+    if (tid == 0) s_path[len] = cur;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    a.accept_len[b] = len;
+    a.next_tok[b] = tok;
+  }
+  for (int j = tid; j < a.path_stride; j += kNT) a.path[(int64_t)b * a.path_stride + j] = j <= len ? s_path[j] : -1;
+}
+
+// Typical mode, pass 1: per row u, x = z_u / T: lse_u = log sum exp x and
+// H_u = lse_u - sum softmax(x) * x.
+template <int DT>
+__global__ __launch_bounds__(256) void row_softmax_stats(AcceptArgs a) {
+  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t base = (int64_t)u * a.vocab;
+  float m = -INFINITY, s = 0.f, t = 0.f;
+  for (int v = tid; v < a.vocab; v += 256) {
+    const float x = ld<DT>(a.logits, base + v) * a.inv_temp;
+    if (x > m) {
+      const float r = expf(m - x);
+      s *= r;
+      t *= r;
+      m = x;
+    }
+    const float e = expf(x - m);
+    s += e;
+    t += e * x;
+  }
+  auto merge = [](float &m1, float &s1, float &t1, float m2, float s2, float t2) {
+    const float M = fmaxf(m1, m2);
+    if (M == -INFINITY) return;
+    const float r1 = expf(m1 - M), r2 = expf(m2 - M);
+    s1 = s1 * r1 + s2 * r2;
+    t1 = t1 * r1 + t2 * r2;
+    m1 = M;
+  };
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1)
+    merge(m, s, t, __shfl_xor(m, off), __shfl_xor(s, off), __shfl_xor(t, off));
+  __shared__ float sm[4], ss[4], st[4];
+  if (lane == 0) {
+    sm[wave] = m;
+    ss[wave] = s;
+    st[wave] = t;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    m = sm[0];
+    s = ss[0];
+    t = st[0];
+    for (int w = 1; w < 4; ++w) merge(m, s, t, sm[w], ss[w], st[w]);
+    const float lse = m + logf(s);
+    a.stats[2 * (int64_t)u] = lse;
+    a.stats[2 * (int64_t)u + 1] = lse - t / s;
+  }
+}
+
+// Typical mode, pass 2: one block per sequence.
+template <int DT>
+__global__ __launch_bounds__(kNT) void accept_typical(AcceptArgs a) {
+  __shared__ float sv[kWaves];
+  __shared__ int si[kWaves];
+  __shared__ float lp[kMaxNodes];
+  __shared__ int pass[kMaxNodes];
+  __shared__ float score[kMaxNodes];
+  __shared__ int ok[kMaxNodes];
+  __shared__ int par[kMaxNodes], dep[kMaxNodes];
+  __shared__ int s_best;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
+  for (int c = tid; c < N; c += kNT) {
+    const int u = a.parent[n0 + c];
+    par[c] = u;
+    dep[c] = a.depth[n0 + c];
+    if (c == 0) continue;
+    const float lse = a.stats[2 * (int64_t)(n0 + u)], H = a.stats[2 * (int64_t)(n0 + u) + 1];
+    const int tok = a.node_tok[n0 + c];
+    const bool valid = tok >= 0 && tok < a.vocab;   // an out-of-range token never passes
+    const float x = valid ? ld<DT>(a.logits, (int64_t)(n0 + u) * a.vocab + tok) * a.inv_temp - lse : -INFINITY;
+    const float thr = fminf(a.log_eps, a.log_delta - H);
+    lp[c] = x;
+    pass[c] = valid && x > thr;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    // parent[c] < c: one pass in node order makes acceptance and path scores cumulative.
+    ok[0] = 1;
+    score[0] = 0.f;
+    int best = 0;
+    for (int c = 1; c < N; ++c) {
+      const int u = par[c];
+      ok[c] = ok[u] && pass[c];
+      score[c] = score[u] + lp[c];
+      if (ok[c]) {
+        const int dc = dep[c], db = dep[best];
+        if (dc > db || (dc == db && score[c] > score[best])) best = c;
+      }
+    }
+    s_best = best;
+  }
+  __syncthreads();
+  const int best = s_best;
+  float v;
+  int tok;
+  row_argbest<DT>(a.logits, n0 + best, a.vocab, sv, si, v, tok);
+  if (tid == 0) {
+    const int len = dep[best];
+    a.accept_len[b] = len;
+    a.next_tok[b] = tok;
+    int32_t *p = a.path + (int64_t)b * a.path_stride;
+    for (int j = 0; j < a.path_stride; ++j) p[j] = -1;
+    for (int u = best, j = len; u >= 0 && j >= 0; u = par[u], --j) p[j] = u;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_accept(int dt, const AcceptArgs &a, int total_nodes, hipStream_t st) {
+  if (a.mode == 0) {
+    if (dt == 1)
+      hipLaunchKernelGGL(accept_greedy<1>, dim3(a.B), dim3(kNT), 0, st, a);
+    else
+      hipLaunchKernelGGL(accept_greedy<0>, dim3(a.B), dim3(kNT), 0, st, a);
+  } else {
+    if (dt == 1) {
+      hipLaunchKernelGGL(row_softmax_stats<1>, dim3(total_nodes), dim3(256), 0, st, a);
+      hipLaunchKernelGGL(accept_typical<1>, dim3(a.B), dim3(kNT), 0, st, a);
+    } else {
+      hipLaunchKernelGGL(row_softmax_stats<0>, dim3(total_nodes), dim3(256), 0, st, a);
+      hipLaunchKernelGGL(accept_typical<0>, dim3(a.B), dim3(kNT), 0, st, a);
+    }
+  }
+  return hipGetLastError();
+}
+
+}  // namespace specmemo

@@ -1,0 +1,420 @@
+// C ABI of libspecmemo: argument, tree and budget validation on the host, launch
+// planning, and the four stage entry points declared in include/specmemo.h.
+//
+// Every check runs before the first HIP call, so a rejected call enqueues
+// nothing and changes no output; error paths need no GPU.
+#include "specmemo.h"
+
+#include <algorithm>
+#include <cstdarg>
+#include <cmath>
+#include <cstdio>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace specmemo;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return SPECMEMO_OK;
+}
+
+bool al(const void *p, uintptr_t a) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+struct TreeInfo {
+  int B = 0, total = 0, max_nodes = 0, max_depth = 0;
+};
+
+// Tree conventions of include/specmemo.h; n_heads/topk_h (optional) add the
+// head-count and rank < top-k constraints of the projection stage.
+int check_trees(const specmemo_trees *t, TreeInfo *ti, int n_heads = -1, const int32_t *topk_h = nullptr) {
+  if (!t) return fail(SPECMEMO_E_ARG, "trees is NULL");
+  if (t->B < 1 || t->B > SPECMEMO_MAX_BATCH) return fail(SPECMEMO_E_ARG, "B=%d outside [1, %d]", t->B, SPECMEMO_MAX_BATCH);
+  if (!al(t->node_off, 4) || !al(t->parent, 4) || !al(t->depth, 4) || !al(t->rank, 4))
+    return fail(SPECMEMO_E_ARG, "device tree arrays must be non-NULL and 4-byte aligned");
+  if (!t->node_off_h || !t->parent_h || !t->depth_h || !t->rank_h)
+    return fail(SPECMEMO_E_ARG, "host tree mirrors must be non-NULL");
+  const int32_t *off = t->node_off_h, *par = t->parent_h, *dep = t->depth_h, *rk = t->rank_h;
+  if (off[0] != 0) return fail(SPECMEMO_E_TREE, "node_off[0]=%d, expected 0", off[0]);
+  TreeInfo r;
+  r.B = t->B;
+  for (int b = 0; b < t->B; ++b) {
+    const int N = off[b + 1] - off[b];
+    if (N < 1 || N > SPECMEMO_MAX_TREE_NODES)
+      return fail(SPECMEMO_E_TREE, "sequence %d has %d tree nodes, expected 1..%d", b, N, SPECMEMO_MAX_TREE_NODES);
+    const int o = off[b];
+    if (par[o] != -1 || dep[o] != 0 || rk[o] != 0)
+      return fail(SPECMEMO_E_TREE, "sequence %d: root must have parent -1, depth 0, rank 0", b);
+    uint32_t used[SPECMEMO_MAX_TREE_NODES] = {0};
+    for (int n = 1; n < N; ++n) {
+      const int p = par[o + n], d = dep[o + n], k = rk[o + n];
+      if (p < 0 || p >= n) return fail(SPECMEMO_E_TREE, "sequence %d node %d: parent %d not in [0, %d)", b, n, p, n);
+      if (d != dep[o + p] + 1) return fail(SPECMEMO_E_TREE, "sequence %d node %d: depth %d != parent depth + 1", b, n, d);
+      if (d > SPECMEMO_MAX_DEPTH) return fail(SPECMEMO_E_TREE, "sequence %d node %d: depth %d > %d", b, n, d, SPECMEMO_MAX_DEPTH);
+      if (n_heads > 0 && d > n_heads)
+        return fail(SPECMEMO_E_TREE, "sequence %d node %d: depth %d exceeds n_heads=%d", b, n, d, n_heads);
+      if (k < 0 || k >= SPECMEMO_MAX_TOPK) return fail(SPECMEMO_E_TREE, "sequence %d node %d: rank %d outside [0, %d)", b, n, k, SPECMEMO_MAX_TOPK);
+      if (topk_h && k >= topk_h[d - 1])
+        return fail(SPECMEMO_E_TREE, "sequence %d node %d: rank %d >= top-k %d of head %d", b, n, k, topk_h[d - 1], d - 1);
+      if (used[p] & (1u << k)) return fail(SPECMEMO_E_TREE, "sequence %d node %d: duplicate sibling rank %d", b, n, k);
+      used[p] |= 1u << k;
+      r.max_depth = std::max(r.max_depth, d);
+    }
+    r.max_nodes = std::max(r.max_nodes, N);
+  }
+  r.total = off[t->B];
+  *ti = r;
+  return SPECMEMO_OK;
+}
+
+int check_dtype(int dt) {
+  if (dt != SPECMEMO_FP32 && dt != SPECMEMO_BF16) return fail(SPECMEMO_E_DTYPE, "unknown dtype %d", dt);
+  return SPECMEMO_OK;
+}
+
+int check_kv(int dt, const specmemo_kv *kv, const TreeInfo &ti, const int32_t *node_off_h) {
+  if (!kv) return fail(SPECMEMO_E_ARG, "kv is NULL");
+  if (!al(kv->k, 16) || !al(kv->v, 16)) return fail(SPECMEMO_E_ARG, "kv->k / kv->v must be non-NULL and 16-byte aligned");
+  if (!kv->seq_base_h || !kv->seq_cap_h || !kv->seq_len_h) return fail(SPECMEMO_E_ARG, "kv host mirrors must be non-NULL");
+  if (kv->n_kv < 1) return fail(SPECMEMO_E_ARG, "n_kv=%d", kv->n_kv);
+  if (kv->cap_total < 1) return fail(SPECMEMO_E_ARG, "cap_total=%lld", (long long)kv->cap_total);
+  if (dt == SPECMEMO_BF16 && kv->head_dim != kAttnHeadDim)
+    return fail(SPECMEMO_E_DTYPE, "bf16 path needs head_dim %d, got %d", kAttnHeadDim, kv->head_dim);
+  if (dt == SPECMEMO_FP32 && (kv->head_dim < 1 || kv->head_dim > 128 || kv->head_dim % 4))
+    return fail(SPECMEMO_E_DTYPE, "fp32 path needs head_dim in [4, 128], a multiple of 4; got %d", kv->head_dim);
+  std::vector<std::pair<int64_t, int64_t>> slabs;
+  for (int b = 0; b < ti.B; ++b) {
+    const int64_t base = kv->seq_base_h[b], cap = kv->seq_cap_h[b], L = kv->seq_len_h[b];
+    const int N = node_off_h[b + 1] - node_off_h[b];
+    if (L < 0 || cap < 0 || base < 0) return fail(SPECMEMO_E_ARG, "sequence %d: negative base/cap/len", b);
+    if (base + cap > kv->cap_total)
+      return fail(SPECMEMO_E_BUDGET, "sequence %d: slab [%lld, %lld) outside the pool of %lld rows", b, (long long)base,
+                  (long long)(base + cap), (long long)kv->cap_total);
+    if (L + N > cap)
+      return fail(SPECMEMO_E_BUDGET, "sequence %d: %lld committed + %d tree rows exceed the slab budget of %lld rows", b,
+                  (long long)L, N, (long long)cap);
+    if (L + N > (int64_t)INT32_MAX / 2) return fail(SPECMEMO_E_ARG, "sequence %d too long", b);
+    slabs.push_back({base, cap});
+  }
+  std::sort(slabs.begin(), slabs.end());
+  for (size_t i = 1; i < slabs.size(); ++i)
+    if (slabs[i - 1].first + slabs[i - 1].second > slabs[i].first)
+      return fail(SPECMEMO_E_BUDGET, "slabs overlap at pool row %lld", (long long)slabs[i].first);
+  return SPECMEMO_OK;
+}
+
+int hip_status(hipError_t e, const char *what) {
+  if (e != hipSuccess) return fail(SPECMEMO_E_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+// ---- tree attention planning ------------------------------------------------------
+constexpr int kTargetItems = 512;   // >= 2 work items per compute unit (256 CUs)
+constexpr int kMinChunk = 512;      // keys per chunk when splitting the KV range
+
+struct AttnPlan {
+  int waves = 4;
+  std::vector<std::vector<AttnSeq>> groups;   // sequences per launch, in launch order
+  std::vector<int> items, citems;
+  size_t ws_bytes = 0;
+};
+
+void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *kv, int n_q, AttnPlan *p) {
+  const int g = n_q / kv->n_kv;
+  p->waves = ti.max_nodes * g <= 64 ? 2 : 4;
+  const int RB = 32 * p->waves;
+  std::vector<int> order(ti.B);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return kv->seq_len_h[x] > kv->seq_len_h[y]; });
+  // Chunk length: split the committed range only when the unsplit grid is too small.
+  int64_t base_items = 0, weighted = 0;
+  for (int b = 0; b < ti.B; ++b) {
+    const int N = t->node_off_h[b + 1] - t->node_off_h[b];
+    const int nrb = (N * g + RB - 1) / RB;
+    base_items += (int64_t)kv->n_kv * nrb;
+    weighted += (int64_t)kv->n_kv * nrb * (kv->seq_len_h[b] + N);
+  }
+  int ch_len = INT32_MAX;
+  if (base_items < kTargetItems) {
+    int64_t c = (weighted + kTargetItems - 1) / kTargetItems;
+    c = std::max<int64_t>(kMinChunk, (c + kAttnKeyTile - 1) / kAttnKeyTile * kAttnKeyTile);
+    ch_len = (int)std::min<int64_t>(c, INT32_MAX / 2);
+  }
+  const int64_t pf = attn_partial_floats(RB);
+  for (size_t i0 = 0; i0 < order.size(); i0 += kMaxSeqPerLaunch) {
+    std::vector<AttnSeq> grp;
+    int item = 0, part = 0, citem = 0;
+    for (size_t i = i0; i < std::min(order.size(), i0 + kMaxSeqPerLaunch); ++i) {
+      const int b = order[i];
+      AttnSeq s{};
+      s.base = kv->seq_base_h[b];
+      s.L = kv->seq_len_h[b];
+      s.node0 = t->node_off_h[b];
+      s.N = t->node_off_h[b + 1] - s.node0;
+      s.nrb = (s.N * g + RB - 1) / RB;
+      s.nch = (ch_len == INT32_MAX || s.L <= ch_len) ? 1 : (s.L + ch_len - 1) / ch_len;
+      s.ch_len = s.nch == 1 ? s.L + s.N : ch_len;
+      s.item0 = item;
+      item += kv->n_kv * s.nrb * s.nch;
+      if (s.nch > 1) {
+        s.part0 = part;
+        part += kv->n_kv * s.nrb * s.nch;
+        s.citem0 = citem;
+        citem += kv->n_kv * s.nrb;
+      } else {
+        s.part0 = -1;
+        s.citem0 = -1;
+      }
+      grp.push_back(s);
+    }
+    p->groups.push_back(grp);
+    p->items.push_back(item);
+    p->citems.push_back(citem);
+    p->ws_bytes = std::max(p->ws_bytes, (size_t)part * (size_t)pf * sizeof(float));
+  }
+}
+
+int check_attn_args(int dt, const specmemo_trees *t, const specmemo_kv *kv, int n_q, TreeInfo *ti) {
+  int rc;
+  if ((rc = check_dtype(dt))) return rc;
+  if ((rc = check_trees(t, ti))) return rc;
+  if ((rc = check_kv(dt, kv, *ti, t->node_off_h))) return rc;
+  if (n_q < 1 || n_q % kv->n_kv) return fail(SPECMEMO_E_ARG, "n_q=%d must be a positive multiple of n_kv=%d", n_q, kv->n_kv);
+  return SPECMEMO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t specmemo_abi_version(void) { return SPECMEMO_ABI_VERSION; }
+
+const char *specmemo_last_error(void) { return g_err.c_str(); }
+
+size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
+                                int32_t n_q_or_heads, int32_t vocab) {
+  TreeInfo ti;
+  if (check_dtype(dt) || check_trees(t, &ti)) return 0;
+  if (which == SPECMEMO_WS_TOPK) {
+    if (n_q_or_heads < 1 || vocab < 1) return 0;
+    return (size_t)ti.B * (size_t)n_q_or_heads * (size_t)vocab * sizeof(float);
+  }
+  if (which == SPECMEMO_WS_ATTN) {
+    if (check_attn_args(dt, t, kv, n_q_or_heads, &ti)) return 0;
+    if (dt == SPECMEMO_FP32) return 0;
+    AttnPlan p;
+    plan_attn(ti, t, kv, n_q_or_heads, &p);
+    return p.ws_bytes;
+  }
+  if (which == SPECMEMO_WS_ACCEPT) {
+    return n_q_or_heads == SPECMEMO_ACCEPT_TYPICAL ? (size_t)ti.total * 2 * sizeof(float) : 0;
+  }
+  return 0;
+}
+
+int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hidden, int32_t vocab, int32_t n_heads,
+                         const int32_t *topk_h, const void *h, const void *head_w, const int32_t *root_tok,
+                         float *logits_out, int32_t *topk_ids, float *topk_vals, int32_t *node_tok, void *ws,
+                         size_t ws_bytes, void *stream) {
+  int rc;
+  if ((rc = check_dtype(dt))) return rc;
+  if (n_heads < 1 || n_heads > SPECMEMO_MAX_DEPTH) return fail(SPECMEMO_E_ARG, "n_heads=%d outside [1, %d]", n_heads, SPECMEMO_MAX_DEPTH);
+  if (!topk_h) return fail(SPECMEMO_E_ARG, "topk_h is NULL");
+  if (vocab < 1) return fail(SPECMEMO_E_ARG, "vocab=%d", vocab);
+  if (hidden < 8 || hidden % 8) return fail(SPECMEMO_E_ARG, "hidden=%d must be a positive multiple of 8", hidden);
+  int kmax = 0;
+  for (int i = 0; i < n_heads; ++i) {
+    if (topk_h[i] < 1 || topk_h[i] > SPECMEMO_MAX_TOPK || topk_h[i] > vocab)
+      return fail(SPECMEMO_E_ARG, "topk[%d]=%d outside [1, min(%d, vocab)]", i, topk_h[i], SPECMEMO_MAX_TOPK);
+    kmax = std::max(kmax, (int)topk_h[i]);
+  }
+  TreeInfo ti;
+  if ((rc = check_trees(t, &ti, n_heads, topk_h))) return rc;
+  if (!al(h, 16) || !al(head_w, 16)) return fail(SPECMEMO_E_ARG, "h / head_w must be non-NULL and 16-byte aligned");
+  if (!al(root_tok, 4) || !al(topk_ids, 4) || !al(node_tok, 4))
+    return fail(SPECMEMO_E_ARG, "root_tok / topk_ids / node_tok must be non-NULL and 4-byte aligned");
+  if (logits_out && !al(logits_out, 16)) return fail(SPECMEMO_E_ARG, "logits_out must be 16-byte aligned");
+  if (topk_vals && !al(topk_vals, 4)) return fail(SPECMEMO_E_ARG, "topk_vals must be 4-byte aligned");
+  float *z = logits_out;
+  if (!z) {
+    const size_t need = (size_t)ti.B * n_heads * vocab * sizeof(float);
+    if (!al(ws, 16) || ws_bytes < need)
+      return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
+    z = static_cast<float *>(ws);
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_head_logits(dt, h, head_w, z, ti.B, hidden, vocab, n_heads, st);
+  if (e != hipSuccess) return hip_status(e, "head projection launch");
+  TopkArgs a{};
+  a.z = z;
+  a.vocab = vocab;
+  a.n_heads = n_heads;
+  a.kmax = kmax;
+  for (int i = 0; i < n_heads; ++i) a.k[i] = topk_h[i];
+  a.node_off = t->node_off;
+  a.depth = t->depth;
+  a.rank = t->rank;
+  a.root_tok = root_tok;
+  a.ids = topk_ids;
+  a.vals = topk_vals;
+  a.node_tok = node_tok;
+  return hip_status(launch_topk(a, ti.B, st), "top-k launch");
+}
+
+int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, int32_t n_q, float scale,
+                       const void *q, void *out, void *ws, size_t ws_bytes, void *stream) {
+  TreeInfo ti;
+  int rc;
+  if ((rc = check_attn_args(dt, t, kv, n_q, &ti))) return rc;
+  if (!al(q, 16) || !al(out, 16)) return fail(SPECMEMO_E_ARG, "q / out must be non-NULL and 16-byte aligned");
+  if (!(scale > 0.f)) scale = 1.0f / std::sqrt((float)kv->head_dim);
+  if (!std::isfinite(scale)) return fail(SPECMEMO_E_ARG, "scale is not finite");
+  AttnArgs a{};
+  a.q = q;
+  a.out = out;
+  a.k = kv->k;
+  a.v = kv->v;
+  a.parent = t->parent;
+  a.cap_total = kv->cap_total;
+  a.n_q = n_q;
+  a.n_kv = kv->n_kv;
+  a.group = n_q / kv->n_kv;
+  a.head_dim = kv->head_dim;
+  a.scale = scale;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (dt == SPECMEMO_FP32) {
+    for (int b0 = 0; b0 < ti.B; b0 += kMaxSeqPerLaunch) {
+      const int nb = std::min(kMaxSeqPerLaunch, ti.B - b0);
+      a.nseq = nb;
+      for (int i = 0; i < nb; ++i) {
+        const int b = b0 + i;
+        AttnSeq s{};
+        s.base = kv->seq_base_h[b];
+        s.L = kv->seq_len_h[b];
+        s.node0 = t->node_off_h[b];
+        s.N = t->node_off_h[b + 1] - s.node0;
+        a.seq[i] = s;
+      }
+      const int nbeg = t->node_off_h[b0], ncnt = t->node_off_h[b0 + nb] - nbeg;
+      hipError_t e = launch_tree_attn_f32(a, nbeg, ncnt, st);
+      if (e != hipSuccess) return hip_status(e, "tree attention launch");
+    }
+    return ok();
+  }
+  AttnPlan p;
+  plan_attn(ti, t, kv, n_q, &p);
+  if (p.ws_bytes) {
+    if (!al(ws, 16) || ws_bytes < p.ws_bytes)
+      return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", p.ws_bytes,
+                  ws ? ws_bytes : 0);
+  }
+  a.part = static_cast<float *>(ws);
+  for (size_t gi = 0; gi < p.groups.size(); ++gi) {
+    a.nseq = (int)p.groups[gi].size();
+    for (int i = 0; i < a.nseq; ++i) a.seq[i] = p.groups[gi][i];
+    a.items = p.items[gi];
+    a.citems = p.citems[gi];
+    hipError_t e = launch_tree_attn_bf16(a, p.waves, st);
+    if (e != hipSuccess) return hip_status(e, "tree attention launch");
+  }
+  return ok();
+}
+
+int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, specmemo_accept_mode mode,
+                    float temperature, float eps, float delta, const void *base_logits, const int32_t *node_tok,
+                    int32_t *accept_len, int32_t *path, int32_t path_stride, int32_t *next_tok, void *ws,
+                    size_t ws_bytes, void *stream) {
+  int rc;
+  if ((rc = check_dtype(dt))) return rc;
+  TreeInfo ti;
+  if ((rc = check_trees(t, &ti))) return rc;
+  if (vocab < 1) return fail(SPECMEMO_E_ARG, "vocab=%d", vocab);
+  if (mode != SPECMEMO_ACCEPT_GREEDY && mode != SPECMEMO_ACCEPT_TYPICAL) return fail(SPECMEMO_E_ARG, "unknown mode %d", mode);
+  if (path_stride < ti.max_depth + 1) return fail(SPECMEMO_E_ARG, "path_stride=%d < max depth + 1 = %d", path_stride, ti.max_depth + 1);
+  if (!al(base_logits, 16)) return fail(SPECMEMO_E_ARG, "base_logits must be non-NULL and 16-byte aligned");
+  if (!al(node_tok, 4) || !al(accept_len, 4) || !al(path, 4) || !al(next_tok, 4))
+    return fail(SPECMEMO_E_ARG, "node_tok / accept_len / path / next_tok must be non-NULL and 4-byte aligned");
+  AcceptArgs a{};
+  a.logits = base_logits;
+  a.node_tok = node_tok;
+  a.node_off = t->node_off;
+  a.parent = t->parent;
+  a.depth = t->depth;
+  a.vocab = vocab;
+  a.mode = mode;
+  a.path_stride = path_stride;
+  a.B = ti.B;
+  a.accept_len = accept_len;
+  a.path = path;
+  a.next_tok = next_tok;
+  if (mode == SPECMEMO_ACCEPT_TYPICAL) {
+    if (!(temperature > 0.f) || !(eps > 0.f) || !(delta > 0.f) || !std::isfinite(temperature))
+      return fail(SPECMEMO_E_ARG, "typical mode needs temperature, eps, delta > 0");
+    const size_t need = (size_t)ti.total * 2 * sizeof(float);
+    if (!al(ws, 16) || ws_bytes < need)
+      return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
+    a.stats = static_cast<float *>(ws);
+    a.inv_temp = 1.0f / temperature;
+    a.log_eps = std::log(eps);
+    a.log_delta = std::log(delta);
+  }
+  return hip_status(launch_accept(dt, a, ti.total, static_cast<hipStream_t>(stream)), "acceptance launch");
+}
+
+int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, const int32_t *accept_len,
+                        const int32_t *path, int32_t path_stride, void *stream) {
+  int rc;
+  if ((rc = check_dtype(dt))) return rc;
+  TreeInfo ti;
+  if ((rc = check_trees(t, &ti))) return rc;
+  if ((rc = check_kv(dt, kv, ti, t->node_off_h))) return rc;
+  if (!al(kv->seq_len, 4)) return fail(SPECMEMO_E_ARG, "kv->seq_len must be non-NULL and 4-byte aligned");
+  if (!al(accept_len, 4) || !al(path, 4)) return fail(SPECMEMO_E_ARG, "accept_len / path must be non-NULL and 4-byte aligned");
+  if (path_stride < 1) return fail(SPECMEMO_E_ARG, "path_stride=%d", path_stride);
+  const int elem = dt == SPECMEMO_BF16 ? 2 : 4;
+  if ((kv->head_dim * elem) % 4) return fail(SPECMEMO_E_ARG, "row bytes must be a multiple of 4");
+  CompactArgs a{};
+  a.k = kv->k;
+  a.v = kv->v;
+  a.cap_total = kv->cap_total;
+  a.n_kv = kv->n_kv;
+  a.row_dwords = kv->head_dim * elem / 4;
+  a.path_stride = path_stride;
+  a.accept_len = accept_len;
+  a.path = path;
+  a.seq_len = kv->seq_len;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  for (int b0 = 0; b0 < ti.B; b0 += kMaxSeqPerLaunch) {
+    a.nseq = std::min(kMaxSeqPerLaunch, ti.B - b0);
+    a.b0 = b0;
+    for (int i = 0; i < a.nseq; ++i) {
+      const int b = b0 + i;
+      a.seq[i] = CompactSeq{kv->seq_base_h[b], kv->seq_len_h[b], t->node_off_h[b + 1] - t->node_off_h[b],
+                            kv->seq_cap_h[b], 0};
+    }
+    hipError_t e = launch_kv_compact(a, st);
+    if (e != hipSuccess) return hip_status(e, "compaction launch");
+  }
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,95 @@
+// Internal declarations shared by the HIP kernels and the C-ABI layer of
+// libspecmemo (gfx950).  Nothing here is part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace specmemo {
+
+constexpr int kMaxSeqPerLaunch = 32;   // per-sequence descriptors travel in kernel arguments
+constexpr int kMaxNodes = 128;
+constexpr int kMaxPath = 16;           // max depth + 1
+constexpr int kMaxTopk = 32;
+constexpr int kMaxHeads = 15;
+
+// ---- head projection + top-k -------------------------------------------------
+struct TopkArgs {
+  const float *z;          // [B][n_heads][vocab] fp32 logits
+  int32_t vocab, n_heads, kmax;
+  int32_t k[kMaxHeads];    // top-k per head
+  const int32_t *node_off, *depth, *rank, *root_tok;
+  int32_t *ids;            // [B][n_heads][kmax]
+  float *vals;             // same or null
+  int32_t *node_tok;
+};
+
+hipError_t launch_head_logits(int dt, const void *h, const void *w, float *z, int B, int hidden,
+                              int vocab, int n_heads, hipStream_t st);
+hipError_t launch_topk(const TopkArgs &a, int B, hipStream_t st);
+
+// ---- tree attention ------------------------------------------------------------
+struct AttnSeq {
+  int64_t base;      // first pool row of the slab
+  int32_t L;         // committed rows
+  int32_t node0;     // global id of the root node
+  int32_t N;         // tree nodes
+  int32_t nrb;       // row blocks (bf16 path)
+  int32_t nch;       // KV chunks
+  int32_t ch_len;    // keys per chunk (multiple of the key tile); last chunk takes the rest
+  int32_t item0;     // first work item of this sequence in the launch
+  int32_t part0;     // first partial slot (multi-chunk sequences), -1 if none
+  int32_t citem0;    // first combine item (multi-chunk sequences)
+  int32_t pad;
+};
+
+struct AttnArgs {
+  const void *q;
+  void *out;
+  const void *k, *v;
+  const int32_t *parent;
+  float *part;             // partial results workspace
+  int64_t cap_total;
+  int32_t n_q, n_kv, group, head_dim;
+  float scale_log2;        // scale * log2(e)
+  float scale;
+  int32_t nseq, items, citems;
+  AttnSeq seq[kMaxSeqPerLaunch];
+};
+
+constexpr int kAttnKeyTile = 64;
+constexpr int kAttnHeadDim = 128;
+// floats per partial slot of a row block: unnormalised O, running max, running sum
+__host__ __device__ constexpr int64_t attn_partial_floats(int rows_per_block) {
+  return (int64_t)rows_per_block * (kAttnHeadDim + 2);
+}
+hipError_t launch_tree_attn_bf16(const AttnArgs &a, int waves, hipStream_t st);
+hipError_t launch_tree_attn_f32(const AttnArgs &a, int node_begin, int node_count, hipStream_t st);
+
+// ---- acceptance ------------------------------------------------------------------
+struct AcceptArgs {
+  const void *logits;
+  const int32_t *node_tok, *node_off, *parent, *depth;
+  int32_t vocab, mode, path_stride, B;
+  float inv_temp, log_eps, log_delta;
+  float *stats;            // typical: [sum N][2] (lse, entropy) of z / T
+  int32_t *accept_len, *path, *next_tok;
+};
+hipError_t launch_accept(int dt, const AcceptArgs &a, int total_nodes, hipStream_t st);
+
+// ---- compaction ------------------------------------------------------------------
+struct CompactSeq {
+  int64_t base;
+  int32_t L, N, cap, pad;
+};
+struct CompactArgs {
+  void *k, *v;
+  int64_t cap_total;
+  int32_t n_kv, row_dwords, path_stride, nseq, b0;
+  const int32_t *accept_len, *path;
+  int32_t *seq_len;
+  CompactSeq seq[kMaxSeqPerLaunch];
+};
+hipError_t launch_kv_compact(const CompactArgs &a, hipStream_t st);
+
+}  // namespace specmemo

@@ -1,0 +1,194 @@
+"""ctypes binding of libspecmemo (include/specmemo.h).
+
+Argument marshalling only: torch tensors provide device memory and the stream,
+numpy arrays the host mirrors; every stage runs in the library's HIP kernels.
+The library is loaded on first use; if it has not been built, ``load()``
+raises instead of falling back to anything else.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+import re
+from typing import Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "_build", "libspecmemo.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "specmemo.h")
+
+FP32, BF16 = 0, 1
+GREEDY, TYPICAL = 0, 1
+WS_TOPK, WS_ATTN, WS_ACCEPT = 0, 1, 2
+
+STATUS = {0: "OK", -1: "E_ARG", -2: "E_DTYPE", -3: "E_TREE", -4: "E_BUDGET", -5: "E_WORKSPACE", -6: "E_HIP"}
+
+
+class SpecmemoError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+        self.name = STATUS.get(code, str(code))
+
+
+class _Trees(C.Structure):
+    _fields_ = [("B", C.c_int32), ("node_off", C.c_void_p), ("parent", C.c_void_p), ("depth", C.c_void_p),
+                ("rank", C.c_void_p), ("node_off_h", C.c_void_p), ("parent_h", C.c_void_p),
+                ("depth_h", C.c_void_p), ("rank_h", C.c_void_p)]
+
+
+class _KV(C.Structure):
+    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("cap_total", C.c_int64), ("n_kv", C.c_int32),
+                ("head_dim", C.c_int32), ("seq_len", C.c_void_p), ("seq_base_h", C.c_void_p),
+                ("seq_cap_h", C.c_void_p), ("seq_len_h", C.c_void_p)]
+
+
+_lib = None
+
+
+def load():
+    """Load libspecmemo.so; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"libspecmemo is not built ({LIB_PATH}); run __graft_entry__.build()")
+        lib = C.CDLL(LIB_PATH)
+        vp, i32, sz, f32 = C.c_void_p, C.c_int32, C.c_size_t, C.c_float
+        PT, PK = C.POINTER(_Trees), C.POINTER(_KV)
+        lib.specmemo_medusa_topk.argtypes = [i32, PT, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        lib.specmemo_tree_attn.argtypes = [i32, PT, PK, i32, f32, vp, vp, vp, sz, vp]
+        lib.specmemo_accept.argtypes = [i32, PT, i32, i32, f32, f32, f32, vp, vp, vp, vp, i32, vp, vp, sz, vp]
+        lib.specmemo_kv_compact.argtypes = [i32, PT, PK, vp, vp, i32, vp]
+        lib.specmemo_workspace_bytes.argtypes = [i32, i32, PT, PK, i32, i32]
+        lib.specmemo_workspace_bytes.restype = C.c_size_t
+        lib.specmemo_last_error.restype = C.c_char_p
+        lib.specmemo_abi_version.restype = C.c_int32
+        for f in ("specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"):
+            getattr(lib, f).restype = C.c_int
+        _lib = lib
+    return _lib
+
+
+def declared_functions() -> list:
+    """Names of the functions include/specmemo.h declares."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(specmemo_\w+)\s*\(", text)))
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise SpecmemoError(rc, load().specmemo_last_error().decode())
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        if not torch.cuda.is_available():
+            return None
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _i32(x) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+
+
+class Trees:
+    """Ragged batch of candidate trees: device arrays plus host mirrors."""
+
+    def __init__(self, node_off, parent, depth, rank, device=None, dev_arrays=None):
+        self.node_off_h, self.parent_h = _i32(node_off), _i32(parent)
+        self.depth_h, self.rank_h = _i32(depth), _i32(rank)
+        self.B = len(self.node_off_h) - 1
+        if dev_arrays is not None:
+            self.dev = dev_arrays
+        else:
+            import torch
+            self.dev = [torch.from_numpy(a.copy()).to(device) for a in
+                        (self.node_off_h, self.parent_h, self.depth_h, self.rank_h)]
+
+    @property
+    def total_nodes(self) -> int:
+        return int(self.node_off_h[-1])
+
+    @property
+    def max_depth(self) -> int:
+        return int(self.depth_h.max())
+
+    def struct(self) -> _Trees:
+        return _Trees(self.B, *[_ptr(t) for t in self.dev],
+                      *[a.ctypes.data for a in (self.node_off_h, self.parent_h, self.depth_h, self.rank_h)])
+
+
+class KVPool:
+    """One layer's budget-capped KV pool: device K, V and seq_len, host mirrors."""
+
+    def __init__(self, k, v, seq_len_dev, seq_base, seq_cap, seq_len):
+        self.k, self.v, self.seq_len = k, v, seq_len_dev
+        self.seq_base_h = np.ascontiguousarray(seq_base, dtype=np.int64)
+        self.seq_cap_h = _i32(seq_cap)
+        self.seq_len_h = _i32(seq_len)
+        self.n_kv, self.cap_total, self.head_dim = (int(s) for s in k.shape)
+
+    def struct(self) -> _KV:
+        return _KV(_ptr(self.k), _ptr(self.v), self.cap_total, self.n_kv, self.head_dim,
+                   _ptr(self.seq_len), self.seq_base_h.ctypes.data, self.seq_cap_h.ctypes.data,
+                   self.seq_len_h.ctypes.data)
+
+
+def abi_version() -> int:
+    return load().specmemo_abi_version()
+
+
+def workspace_bytes(which: int, dt: int, trees: Trees, kv: Optional[KVPool], n_q_or_heads: int, vocab: int = 0) -> int:
+    ts = trees.struct()
+    ks = kv.struct() if kv is not None else None
+    return load().specmemo_workspace_bytes(which, dt, C.byref(ts), C.byref(ks) if ks is not None else None,
+                                           n_q_or_heads, vocab)
+
+
+def medusa_topk(dt: int, trees: Trees, hidden: int, vocab: int, n_heads: int, topk: Sequence[int], h, head_w,
+                root_tok, topk_ids, node_tok, logits_out=None, topk_vals=None, ws=None, ws_bytes: int = 0,
+                stream=None):
+    ts = trees.struct()
+    tk = _i32(topk)
+    _check(load().specmemo_medusa_topk(dt, C.byref(ts), hidden, vocab, n_heads, tk.ctypes.data, _ptr(h),
+                                       _ptr(head_w), _ptr(root_tok), _ptr(logits_out), _ptr(topk_ids),
+                                       _ptr(topk_vals), _ptr(node_tok), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def tree_attn(dt: int, trees: Trees, kv: KVPool, n_q: int, q, out, scale: float = 0.0, ws=None,
+              ws_bytes: int = 0, stream=None):
+    ts, ks = trees.struct(), kv.struct()
+    _check(load().specmemo_tree_attn(dt, C.byref(ts), C.byref(ks), n_q, scale, _ptr(q), _ptr(out), _ptr(ws),
+                                     ws_bytes, _stream(stream)))
+
+
+def accept(dt: int, trees: Trees, vocab: int, mode: int, base_logits, node_tok, accept_len, path, path_stride: int,
+           next_tok, temperature: float = 1.0, eps: float = 0.09, delta: float = 0.3, ws=None, ws_bytes: int = 0,
+           stream=None):
+    ts = trees.struct()
+    _check(load().specmemo_accept(dt, C.byref(ts), vocab, mode, temperature, eps, delta, _ptr(base_logits),
+                                  _ptr(node_tok), _ptr(accept_len), _ptr(path), path_stride, _ptr(next_tok),
+                                  _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def kv_compact(dt: int, trees: Trees, kv: KVPool, accept_len, path, path_stride: int, stream=None):
+    ts, ks = trees.struct(), kv.struct()
+    _check(load().specmemo_kv_compact(dt, C.byref(ts), C.byref(ks), _ptr(accept_len), _ptr(path), path_stride,
+                                      _stream(stream)))

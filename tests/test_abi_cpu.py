@@ -1,0 +1,151 @@
+"""The C-ABI library loads, exports what include/specmemo.h declares, and
+rejects bad arguments on the host before any HIP call.
+
+The error-path calls pass fake (aligned, never dereferenced) device pointers;
+they run only where no GPU is visible, so that a validation bug can never
+launch a kernel on them.
+"""
+
+import ctypes as C
+
+import numpy as np
+import pytest
+
+from paper_2506_01986_amd import specmemo as sm
+from paper_2506_01986_amd import synth
+
+
+def _no_gpu():
+    import torch
+    return not torch.cuda.is_available()
+
+
+cpu_only = pytest.mark.skipif(not _no_gpu(), reason="fake device pointers: host validation tests run without a GPU")
+
+FAKE = 1 << 20          # 16-byte aligned, never dereferenced
+
+
+def test_library_loads_and_exports_every_declared_function():
+    lib = sm.load()
+    names = sm.declared_functions()
+    assert {"specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sm.abi_version() == 1
+
+
+class FakeTrees(sm.Trees):
+    def __init__(self, trees):
+        node_off = np.concatenate([[0], np.cumsum([t.n for t in trees])])
+        super().__init__(node_off, np.concatenate([t.parent for t in trees]),
+                         np.concatenate([t.depth for t in trees]), np.concatenate([t.rank for t in trees]),
+                         dev_arrays=[FAKE, FAKE, FAKE, FAKE])
+
+
+class FakeKV(sm.KVPool):
+    def __init__(self, lens, caps, bases, n_kv=2, d=128, cap_total=None):
+        self.k = self.v = self.seq_len = FAKE
+        self.seq_base_h = np.asarray(bases, np.int64)
+        self.seq_cap_h = np.asarray(caps, np.int32)
+        self.seq_len_h = np.asarray(lens, np.int32)
+        self.n_kv, self.head_dim = n_kv, d
+        self.cap_total = cap_total if cap_total is not None else int(max(np.add(bases, caps)))
+
+
+def expect(code, fn, *a, **k):
+    with pytest.raises(sm.SpecmemoError) as e:
+        fn(*a, **k)
+    assert e.value.name == code, str(e.value)
+    return str(e.value)
+
+
+def attn(trees, kv, n_q=4, dt=sm.BF16):
+    sm.tree_attn(dt, trees, kv, n_q, FAKE, FAKE, ws=FAKE, ws_bytes=1 << 30, stream=0)
+
+
+def topk(trees, hidden=256, vocab=1000, n_heads=3, k=(4, 2, 2), dt=sm.BF16, ws_bytes=1 << 30, logits=None):
+    sm.medusa_topk(dt, trees, hidden, vocab, n_heads, k, FAKE, FAKE, FAKE, FAKE, FAKE, logits_out=logits,
+                   ws=FAKE, ws_bytes=ws_bytes, stream=0)
+
+
+@cpu_only
+def test_tree_errors():
+    t = synth.t16()
+    bad = synth.Tree(t.parent.copy(), t.depth.copy(), t.rank.copy())
+    bad.parent[5] = 7                      # parent after child
+    msg = expect("E_TREE", topk, FakeTrees([bad]))
+    assert "parent" in msg
+    dup = synth.Tree(t.parent.copy(), t.depth.copy(), t.rank.copy())
+    dup.rank[2] = 0                        # duplicate sibling rank under the root
+    expect("E_TREE", topk, FakeTrees([dup]))
+    expect("E_TREE", topk, FakeTrees([t]), n_heads=2, k=(4, 2))          # depth 3 > 2 heads
+    expect("E_TREE", topk, FakeTrees([t]), k=(3, 2, 2))                 # rank 3 >= top-3
+    dep = synth.Tree(t.parent.copy(), t.depth.copy(), t.rank.copy())
+    dep.depth[6] = 3
+    expect("E_TREE", topk, FakeTrees([dep]))
+    big = synth.random_tree(np.random.default_rng(0), 129, max_depth=15, max_kids=30)
+    expect("E_TREE", attn, FakeTrees([big]), FakeKV([10], [200], [0]))
+
+
+@cpu_only
+def test_argument_errors():
+    t = FakeTrees([synth.t16()])
+    expect("E_DTYPE", topk, t, dt=7)
+    expect("E_ARG", topk, t, hidden=100)             # not a multiple of 8
+    expect("E_ARG", topk, t, k=(4, 2, 0))
+    expect("E_ARG", topk, t, k=(40, 2, 2))           # > 32
+    expect("E_ARG", topk, t, n_heads=16, k=(4,) * 16)
+    expect("E_DTYPE", attn, t, FakeKV([10], [40], [0], d=64))      # bf16 needs d = 128
+    expect("E_ARG", attn, t, FakeKV([10], [40], [0], n_kv=3), n_q=4)
+    with pytest.raises(sm.SpecmemoError) as e:
+        sm.accept(sm.BF16, t, 1000, sm.GREEDY, FAKE, FAKE, FAKE, FAKE, 2, FAKE, stream=0)
+    assert e.value.name == "E_ARG" and "path_stride" in str(e.value)
+    with pytest.raises(sm.SpecmemoError) as e:
+        sm.accept(sm.BF16, t, 1000, sm.TYPICAL, FAKE, FAKE, FAKE, FAKE, 4, FAKE, temperature=0.0, ws=FAKE,
+                  ws_bytes=1 << 20, stream=0)
+    assert e.value.name == "E_ARG"
+    with pytest.raises(sm.SpecmemoError) as e:       # misaligned device pointer
+        sm.tree_attn(sm.BF16, t, FakeKV([10], [40], [0]), 4, FAKE + 2, FAKE, stream=0)
+    assert e.value.name == "E_ARG"
+
+
+@cpu_only
+def test_budget_errors():
+    t = FakeTrees([synth.t16(), synth.t16()])
+    expect("E_BUDGET", attn, t, FakeKV([10, 10], [25, 26], [0, 30]))            # 10 + 16 > 25
+    expect("E_BUDGET", attn, t, FakeKV([10, 10], [26, 26], [0, 20]))            # slabs overlap
+    expect("E_BUDGET", attn, t, FakeKV([10, 10], [26, 26], [0, 30], cap_total=50))
+    with pytest.raises(sm.SpecmemoError) as e:
+        sm.kv_compact(sm.BF16, t, FakeKV([10, 10], [25, 26], [0, 30]), FAKE, FAKE, 5, stream=0)
+    assert e.value.name == "E_BUDGET"
+
+
+@cpu_only
+def test_workspace_errors_and_sizes():
+    t = FakeTrees([synth.t16()])
+    need = sm.workspace_bytes(sm.WS_TOPK, sm.BF16, t, None, 3, 1000)
+    assert need == 1 * 3 * 1000 * 4
+    expect("E_WORKSPACE", topk, t, ws_bytes=need - 1)
+    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.TYPICAL, 0) == 16 * 2 * 4
+    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.GREEDY, 0) == 0
+    # a long sequence alone on the device is split along its KV range: partials need workspace
+    big = FakeTrees([synth.t64()])
+    kv = FakeKV([100000], [100064], [0], n_kv=1, d=128)
+    assert sm.workspace_bytes(sm.WS_ATTN, sm.BF16, big, kv, 1) > 0
+    with pytest.raises(sm.SpecmemoError) as e:
+        sm.tree_attn(sm.BF16, big, kv, 1, FAKE, FAKE, ws=FAKE, ws_bytes=16, stream=0)
+    assert e.value.name == "E_WORKSPACE"
+    assert sm.workspace_bytes(sm.WS_ATTN, 9, big, kv, 1) == 0      # invalid arguments report 0
+
+
+@cpu_only
+def test_last_error_cleared_by_success_is_thread_local():
+    import threading
+    t = FakeTrees([synth.t16()])
+    expect("E_DTYPE", topk, t, dt=7)
+    msgs = []
+    th = threading.Thread(target=lambda: msgs.append(sm.load().specmemo_last_error()))
+    th.start()
+    th.join()
+    assert msgs == [b""]
+    assert sm.load().specmemo_last_error() != b""

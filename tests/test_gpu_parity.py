@@ -1,0 +1,306 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Integers (top-k ids, node tokens, accepted lengths, paths, next tokens,
+compaction results) must match bit-exactly; floats within |gpu - ref| <=
+atol + rtol * |ref| with (1e-2, 2e-2) for bf16 and (1e-5, 1e-5) for fp32.
+
+Top-k ids come from fp32 logits on the GPU and fp64 logits in the oracle: where
+two oracle logits lie closer than the fp32 accumulation error bound tau, either
+order is a correct result, so ids are compared exactly except inside such
+near-tie clusters, where the GPU's choice must be a valid top-k order.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2506_01986_amd import configs, synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": (1e-5, 1e-5), "bf16": (1e-2, 2e-2)}
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    from paper_2506_01986_amd import specmemo
+    specmemo.load()
+    return torch
+
+
+def close(gpu, ref, dtype):
+    atol, rtol = TOL[dtype]
+    err = np.abs(gpu - ref) - (atol + rtol * np.abs(ref))
+    return float(err.max()) if err.size else -1.0
+
+
+def tau_for(cfg, z):
+    # fp32 accumulation error bound used to call two logits a near-tie
+    return (1e-5 if cfg.dtype == "fp32" else 1e-3) * (1.0 + np.abs(z))
+
+
+def check_topk(cfg, z64, gpu_ids):
+    """gpu_ids[b, i, :k]: valid top-k of z64[b, i]; exact where unambiguous."""
+    B, nh, _ = z64.shape
+    exact = 0
+    for b in range(B):
+        for i in range(nh):
+            k = cfg.topk[i]
+            z = z64[b, i]
+            g = gpu_ids[b, i, :k]
+            assert np.all(gpu_ids[b, i, k:] == -1)
+            assert len(set(g.tolist())) == k and g.min() >= 0 and g.max() < cfg.vocab
+            ref = np.argsort(-z, kind="stable")[:k + 1]
+            t = tau_for(cfg, z[ref]).max()
+            if np.all(np.diff(-z[ref]) > 2 * t):
+                assert g.tolist() == ref[:k].tolist(), (b, i)
+                exact += 1
+            else:
+                zg = z[g]
+                assert np.all(zg[:-1] >= zg[1:] - 2 * t), (b, i)
+                rest = np.delete(z, g)
+                assert zg[-1] >= rest.max() - 2 * t, (b, i)
+    return exact
+
+
+def attn_sample(wl, max_rows, rng):
+    """(node, head) pairs: every row when small, else a sample that always covers
+    each sequence's root, deepest and last node."""
+    cfg = wl.cfg
+    total = wl.total_nodes * cfg.n_q
+    if total <= max_rows:
+        return None
+    pairs = set()
+    for b in range(cfg.B):
+        o, N = int(wl.node_off[b]), wl.trees[b].n
+        deep = o + int(np.argmax(wl.trees[b].depth))
+        for n in (o, deep, o + N - 1):
+            for h in rng.choice(cfg.n_q, size=min(cfg.n_q, 4), replace=False):
+                pairs.add((n, int(h)))
+    while len(pairs) < max_rows:
+        pairs.add((int(rng.integers(wl.total_nodes)), int(rng.integers(cfg.n_q))))
+    return np.array(sorted(pairs), dtype=np.int32)
+
+
+def distinct_sibling_tokens(wl, rng):
+    tok = np.zeros(wl.total_nodes, np.int32)
+    for b, t in enumerate(wl.trees):
+        o = int(wl.node_off[b])
+        tok[o] = wl.root_tok[b]
+        for u in range(t.n):
+            kids = synth.children(t, u)
+            if kids:
+                tok[o + np.array(kids)] = rng.choice(wl.cfg.vocab, size=len(kids), replace=False)
+    return tok
+
+
+def run_parity(torch, wl, max_attn_rows=None, typical=True, label=""):
+    from paper_2506_01986_amd import runner, specmemo as sm
+    cfg = wl.cfg
+    say(f"[parity] {label or cfg.name}: B={cfg.B} sumN={wl.total_nodes} L={wl.lens.tolist()[:8]}")
+    rng = np.random.default_rng(1234)
+    step = runner.VerifyStep(wl, keep_logits=True)
+
+    # (a) head projection, top-k, tree tokens
+    say("[parity]   stage a")
+    step.medusa_topk()
+    torch.cuda.synchronize()
+    z_gpu = step.logits.cpu().numpy()
+    ids_gpu = step.topk_ids.cpu().numpy()
+    tok_gpu = step.node_tok.cpu().numpy()
+    z64 = oracle.head_logits(wl.hidden, wl.head_w)
+    assert close(z_gpu, z64, cfg.dtype) <= 0
+    tau = tau_for(cfg, z64)
+    assert np.all(np.abs(z_gpu - z64) <= tau), float((np.abs(z_gpu - z64) / tau).max())
+    exact = check_topk(cfg, z64, ids_gpu)
+    ids64, _ = oracle.heads_topk(z64, cfg.topk, cfg.kmax)
+    tok64 = oracle.tree_tokens(wl.node_off, wl.depth, wl.rank, wl.root_tok, ids64)
+    same = np.all(ids_gpu == ids64, axis=2)
+    for b in range(cfg.B):
+        o, n1 = int(wl.node_off[b]), int(wl.node_off[b + 1])
+        if same[b].all():
+            assert np.array_equal(tok_gpu[o:n1], tok64[o:n1]), b
+    say(f"[parity]   stage a ok: exact top-k rows {exact}/{cfg.B * cfg.n_heads}")
+
+    # (b) tree attention
+    say("[parity]   stage b")
+    step.tree_attn()
+    torch.cuda.synchronize()
+    out_gpu = runner.to_host_storage(step.out, cfg.dtype)
+    out_gpu = synth.storage_to_f64(out_gpu, cfg.dtype)
+    sel = attn_sample(wl, max_attn_rows or 10 ** 9, rng)
+    ref = oracle.tree_attn(wl.q, wl.pool_k, wl.pool_v, wl.node_off, wl.parent, wl.lens, wl.seq_base,
+                           cfg.n_kv, sel=sel)
+    got = out_gpu if sel is None else out_gpu[sel[:, 0], sel[:, 1]]
+    worst = close(got, ref, cfg.dtype)
+    say(f"[parity]   stage b rows={ref.shape[0] if sel is not None else ref.shape[0] * ref.shape[1]} "
+        f"max|err|={np.abs(got - ref).max():.3g} margin={worst:.3g}")
+    assert worst <= 0
+
+    # (c) acceptance on planted logits (oracle node tokens plant the walk)
+    lg = synth.planted_logits(wl, tok64)
+    step.set_base_logits(lg)
+    stride = step.path_stride
+    modes = [(sm.GREEDY, "greedy")] + ([(sm.TYPICAL, "typical")] if typical else [])
+    for mode, name in modes:
+        say(f"[parity]   stage c {name}")
+        step.mode = mode
+        if mode == sm.TYPICAL:
+            need = sm.workspace_bytes(sm.WS_ACCEPT, step.dt, step.trees, None, mode)
+            assert need <= step.ws_bytes or step.ws.numel() >= need
+            if step.ws.numel() < need:
+                step.ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+                step.ws_bytes = need
+        step.accept()
+        torch.cuda.synchronize()
+        if mode == sm.GREEDY:
+            ra, rp, rn = oracle.accept_greedy(lg, tok64, wl.node_off, wl.parent, wl.depth, stride)
+        else:
+            ra, rp, rn = oracle.accept_typical(lg, tok64, wl.node_off, wl.parent, wl.depth, stride,
+                                               step.temperature, step.eps, step.delta)
+        assert np.array_equal(step.accept_len.cpu().numpy(), ra)
+        assert np.array_equal(step.path.cpu().numpy(), rp)
+        assert np.array_equal(step.next_tok.cpu().numpy(), rn)
+        for b in range(cfg.B):
+            assert rp[b, :ra[b] + 1].tolist() == wl.plan_path[b]
+    step.mode = sm.GREEDY
+
+    # (d) compaction, after a greedy acceptance
+    say("[parity]   stage d")
+    step.accept()
+    K0, V0 = wl.pool_k.copy(), wl.pool_v.copy()
+    step.kv_compact()
+    torch.cuda.synchronize()
+    acc, path = step.accept_len.cpu().numpy(), step.path.cpu().numpy()
+    new_len = oracle.kv_compact(K0, V0, wl.seq_base, wl.lens, acc, path)
+    Kg = runner.to_host_storage(step.k, cfg.dtype)
+    Vg = runner.to_host_storage(step.v, cfg.dtype)
+    assert np.array_equal(Kg.view(np.uint8), K0.view(np.uint8))
+    assert np.array_equal(Vg.view(np.uint8), V0.view(np.uint8))
+    assert np.array_equal(step.seq_len.cpu().numpy(), new_len)
+    say(f"[parity]   stage d ok: accepted {acc.tolist()[:10]}")
+    return step
+
+
+CONFIG_ROWS = {"tiny_fp32": None, "llama2_7b_b1": None, "llama2_13b_b4": None, "llama2_70b_b10": None,
+               "stress_b32": 6000}
+
+
+@pytest.mark.parametrize("name", list(CONFIG_ROWS))
+def test_config_parity(torch_cuda, name):
+    cfg = configs.get(name)
+    wl = synth.make(cfg)
+    run_parity(torch_cuda, wl, max_attn_rows=CONFIG_ROWS[name])
+
+
+def edge_cfg(**kw):
+    base = dict(name="edge", dtype="bf16", B=3, n_q=8, n_kv=1, head_dim=128, hidden=136, vocab=1000,
+                n_heads=4, topk=(10, 10, 10, 10), tree="T64", kv_len=(1, 1), seed=77, w_std=0.05)
+    base.update(kw)
+    return configs.Config(**base)
+
+
+EDGES = {
+    # empty committed range, single-node tree, 128-node GQA tree (1024 query rows), ragged short L
+    "mixed_gqa": (edge_cfg(B=4, n_q=8, n_kv=1),
+                  lambda r: [synth.random_tree(r, 128), synth.tree_from_rank_paths([()]), synth.t64(),
+                             synth.chain_tree(5)], [0, 37, 64, 1]),
+    # MHA (2-wave row blocks), 17 sequences (two 16-wide batch tiles in the head GEMM)
+    "mha_b17": (edge_cfg(B=17, n_q=2, n_kv=2, hidden=64, vocab=520),
+                lambda r: [synth.random_tree(r, int(r.integers(1, 65))) for _ in range(17)],
+                list(range(0, 17 * 70, 70))),
+    # more than 32 sequences: several launch groups
+    "b40": (edge_cfg(B=40, n_q=4, n_kv=2, hidden=32, vocab=256, topk=(4, 3, 2, 2)),
+            lambda r: [synth.random_tree(r, int(r.integers(1, 20)), max_kids=2) for _ in range(40)],
+            [int(x) for x in np.random.default_rng(5).integers(0, 300, 40)]),
+    # one long sequence alone: the KV range is split into chunks and merged
+    "split_kv": (edge_cfg(B=1, n_q=1, n_kv=1, hidden=64, vocab=300),
+                 lambda r: [synth.t64()], [20011]),
+    # fp32 with GQA and head_dim 64
+    "fp32_gqa": (edge_cfg(dtype="fp32", B=3, n_q=6, n_kv=2, head_dim=64, hidden=40, vocab=333, w_std=1.0),
+                 lambda r: [synth.t16(), synth.random_tree(r, 30), synth.tree_from_rank_paths([()])],
+                 [5, 0, 200]),
+}
+
+
+@pytest.mark.parametrize("name", list(EDGES))
+def test_edge_parity(torch_cuda, name):
+    cfg, trees, lens = EDGES[name]
+    rng = np.random.default_rng(len(name))
+    wl = synth.make(cfg, trees=trees(rng), lens=lens)
+    run_parity(torch_cuda, wl, label=name)
+
+
+def test_acceptance_small_vocab_random(torch_cuda):
+    """Random tiny trees and logits with many ties: greedy and typical vs oracle."""
+    import torch
+    from paper_2506_01986_amd import specmemo as sm
+    rng = np.random.default_rng(3)
+    trees = [synth.random_tree(rng, int(rng.integers(1, 13)), max_depth=4, max_kids=4) for _ in range(64)]
+    vocab = 8
+    node_off = np.concatenate([[0], np.cumsum([t.n for t in trees])]).astype(np.int32)
+    parent = np.concatenate([t.parent for t in trees])
+    depth = np.concatenate([t.depth for t in trees])
+    rank = np.concatenate([t.rank for t in trees])
+    tok = np.zeros(node_off[-1], np.int32)
+    for b, t in enumerate(trees):
+        for u in range(t.n):
+            kids = synth.children(t, u)
+            if kids:
+                tok[node_off[b] + np.array(kids)] = rng.choice(vocab, size=len(kids), replace=False)
+    tr = sm.Trees(node_off, parent, depth, rank, device="cuda")
+    B, stride = len(trees), 5
+    for dtype in ("fp32", "bf16"):
+        raw = rng.integers(0, 3, size=(node_off[-1], vocab)).astype(np.float32)
+        raw[::3] = (2 * rng.standard_normal((len(raw[::3]), vocab))).astype(np.float32)
+        lg = raw if dtype == "fp32" else synth.to_bf16_bits(raw)
+        from paper_2506_01986_amd.runner import to_device
+        dlg = to_device(lg, dtype, "cuda")
+        dtok = torch.from_numpy(tok).cuda()
+        out = [torch.empty(B, dtype=torch.int32, device="cuda"), torch.empty((B, stride), dtype=torch.int32, device="cuda"),
+               torch.empty(B, dtype=torch.int32, device="cuda")]
+        dt = sm.FP32 if dtype == "fp32" else sm.BF16
+        sm.accept(dt, tr, vocab, sm.GREEDY, dlg, dtok, out[0], out[1], stride, out[2])
+        ra, rp, rn = oracle.accept_greedy(lg, tok, node_off, parent, depth, stride)
+        assert np.array_equal(out[0].cpu().numpy(), ra)
+        assert np.array_equal(out[1].cpu().numpy(), rp)
+        assert np.array_equal(out[2].cpu().numpy(), rn)
+        # typical: compare where no edge that can matter sits within fp32 error of its threshold
+        ws = torch.empty(sm.workspace_bytes(sm.WS_ACCEPT, dt, tr, None, sm.TYPICAL), dtype=torch.uint8, device="cuda")
+        sm.accept(dt, tr, vocab, sm.TYPICAL, dlg, dtok, out[0], out[1], stride, out[2], temperature=0.7,
+                  eps=0.09, delta=0.3, ws=ws, ws_bytes=ws.numel())
+        ra, rp, rn, lp, lt = oracle.accept_typical(lg, tok, node_off, parent, depth, stride, 0.7, 0.09, 0.3,
+                                                   edges=True)
+        ga, gp, gn = (o.cpu().numpy() for o in out)
+        checked = 0
+        for b in range(B):
+            o, n1 = node_off[b], node_off[b + 1]
+            margin = np.abs(lp[o + 1:n1] - lt[o + 1:n1])
+            if margin.size and margin.min() < 1e-4:
+                continue
+            checked += 1
+            assert ga[b] == ra[b] and np.array_equal(gp[b], rp[b]) and gn[b] == rn[b], b
+        assert checked > B // 2
+
+
+def test_run_to_run_determinism(torch_cuda):
+    import torch
+    from paper_2506_01986_amd import runner
+    cfg, trees, lens = EDGES["split_kv"]
+    wl = synth.make(cfg, trees=trees(np.random.default_rng(0)), lens=lens)
+    step = runner.VerifyStep(wl, keep_logits=True)
+    outs = []
+    for _ in range(2):
+        step.medusa_topk()
+        step.tree_attn()
+        torch.cuda.synchronize()
+        outs.append((step.logits.clone(), step.out.clone(), step.topk_ids.clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a.view(torch.uint8) if a.dtype != torch.int32 else a,
+                           b.view(torch.uint8) if b.dtype != torch.int32 else b)
