@@ -138,94 +138,112 @@ __global__ __launch_bounds__(256) void head_logits_f32(const float *__restrict__
   }
 }
 
-// Top-k of one (sequence, head) logit row, then the tree tokens of that head's
-// level.  Each thread keeps a sorted list of its KM best (value, id) pairs in
-// registers; k rounds of a block-wide arg-best then pop the global order.
-template <int KM>
-__global__ __launch_bounds__(256) void topk_assemble(TopkArgs a) {
-  const int row = blockIdx.x;              // b * n_heads + head
+// Top-k in two levels.  Level 1: each block takes a 2048-wide slice of one
+// (sequence, head) logit row and emits the slice's kmax best (value, id) pairs.
+// Level 2: one block per row merges the slices' candidates into the top-k and
+// writes the tree tokens of that head's level.  Both levels pick k times the
+// block-wide best remaining pair (larger value, then lower id).
+constexpr int kSel = 256;        // threads per selection block
+constexpr int kPer = 8;          // pairs held per thread
+
+__device__ __forceinline__ void block_best(float &bv, int &bi, float *sv, int *si) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float ov = __shfl_xor(bv, off);
+    const int oi = __shfl_xor(bi, off);
+    if (better(ov, oi, bv, bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  if (lane == 0) {
+    sv[wave] = bv;
+    si[wave] = bi;
+  }
+  __syncthreads();
+  bv = sv[0];
+  bi = si[0];
+#pragma unroll
+  for (int w = 1; w < kSel / 64; ++w)
+    if (better(sv[w], si[w], bv, bi)) {
+      bv = sv[w];
+      bi = si[w];
+    }
+  __syncthreads();
+}
+
+// Emit the k best of the thread-held pairs, in order, to (ov, oi) by thread 0.
+__device__ __forceinline__ void select_k(float (&v)[kPer], int (&id)[kPer], int k, float *ov, int *oi) {
+  __shared__ float sv[kSel / 64];
+  __shared__ int si[kSel / 64];
+  for (int j = 0; j < k; ++j) {
+    float bv = -INFINITY;
+    int bi = INT32_MAX;
+#pragma unroll
+    for (int p = 0; p < kPer; ++p)
+      if (better(v[p], id[p], bv, bi)) {
+        bv = v[p];
+        bi = id[p];
+      }
+    block_best(bv, bi, sv, si);
+    if (threadIdx.x == 0) {
+      ov[j] = bv;
+      oi[j] = bi;
+    }
+#pragma unroll
+    for (int p = 0; p < kPer; ++p)       // ids are unique: only the winner's slot is cleared
+      if (id[p] == bi) {
+        v[p] = -INFINITY;
+        id[p] = INT32_MAX;
+      }
+  }
+}
+
+__global__ __launch_bounds__(kSel) void topk_partial(TopkArgs a) {
+  const int row = blockIdx.x / a.nsplit, split = blockIdx.x % a.nsplit;
+  const float *x = a.z + (int64_t)row * a.vocab;
+  float v[kPer];
+  int id[kPer];
+#pragma unroll
+  for (int p = 0; p < kPer; ++p) {
+    const int i = split * kSel * kPer + p * kSel + threadIdx.x;
+    const bool in = i < a.vocab;
+    v[p] = in ? x[i] : -INFINITY;
+    id[p] = in ? i : INT32_MAX;
+  }
+  const int64_t c0 = ((int64_t)row * a.nsplit + split) * a.kmax;
+  select_k(v, id, a.kmax, a.cand_v + c0, a.cand_i + c0);
+}
+
+__global__ __launch_bounds__(kSel) void topk_merge(TopkArgs a) {
+  const int row = blockIdx.x;                 // b * n_heads + head
   const int b = row / a.n_heads, head = row % a.n_heads;
   const int k = a.k[head];
-  const float *x = a.z + (int64_t)row * a.vocab;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-
-  float lv[KM];
-  int li[KM];
+  const int ncand = a.nsplit * a.kmax;
+  const float *cv = a.cand_v + (int64_t)row * ncand;
+  const int *ci = a.cand_i + (int64_t)row * ncand;
+  float v[kPer];
+  int id[kPer];
 #pragma unroll
-  for (int j = 0; j < KM; ++j) {
-    lv[j] = -INFINITY;
-    li[j] = INT32_MAX;
+  for (int p = 0; p < kPer; ++p) {
+    const int i = p * kSel + threadIdx.x;
+    const bool in = i < ncand;
+    v[p] = in ? cv[i] : -INFINITY;
+    id[p] = in ? ci[i] : INT32_MAX;
   }
-  for (int v = tid; v < a.vocab; v += 256) {
-    float xv = x[v];
-    if (!better(xv, v, lv[KM - 1], li[KM - 1])) continue;
-    float cv = xv;
-    int ci = v;
-#pragma unroll
-    for (int j = 0; j < KM; ++j) {         // insertion by compare-exchange down the list
-      if (better(cv, ci, lv[j], li[j])) {
-        float tv = lv[j];
-        int ti = li[j];
-        lv[j] = cv;
-        li[j] = ci;
-        cv = tv;
-        ci = ti;
-      }
-    }
-  }
-
-  __shared__ float sv[4];
-  __shared__ int si[4];
-  __shared__ int sel[KM];
-  __shared__ float selv[KM];
-  for (int j = 0; j < k; ++j) {
-    float bv = lv[0];
-    int bi = li[0];
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      float ov = __shfl_xor(bv, off);
-      int oi = __shfl_xor(bi, off);
-      if (better(ov, oi, bv, bi)) {
-        bv = ov;
-        bi = oi;
-      }
-    }
-    if (lane == 0) {
-      sv[wave] = bv;
-      si[wave] = bi;
-    }
-    __syncthreads();
-    bv = sv[0];
-    bi = si[0];
-#pragma unroll
-    for (int w = 1; w < 4; ++w)
-      if (better(sv[w], si[w], bv, bi)) {
-        bv = sv[w];
-        bi = si[w];
-      }
-    if (tid == 0) {
-      sel[j] = bi < a.vocab ? bi : -1;
-      selv[j] = bv;
-    }
-    if (li[0] == bi) {                       // ids are unique: exactly one thread pops
-#pragma unroll
-      for (int t = 0; t < KM - 1; ++t) {
-        lv[t] = lv[t + 1];
-        li[t] = li[t + 1];
-      }
-      lv[KM - 1] = -INFINITY;
-      li[KM - 1] = INT32_MAX;
-    }
-    __syncthreads();
-  }
-
+  __shared__ float selv[kMaxTopk];
+  __shared__ int sel[kMaxTopk];
+  select_k(v, id, k, selv, sel);
+  __syncthreads();
+  const int tid = threadIdx.x;
   int32_t *ids = a.ids + (int64_t)row * a.kmax;
-  for (int j = tid; j < a.kmax; j += 256) {
+  for (int j = tid; j < a.kmax; j += kSel) {
     ids[j] = j < k ? sel[j] : -1;
     if (a.vals) a.vals[(int64_t)row * a.kmax + j] = j < k ? selv[j] : -INFINITY;
   }
   const int n0 = a.node_off[b], n1 = a.node_off[b + 1];
-  for (int n = n0 + tid; n < n1; n += 256) {
+  for (int n = n0 + tid; n < n1; n += kSel) {
     if (n == n0) {
       if (head == 0) a.node_tok[n] = a.root_tok[b];
     } else if (a.depth[n] == head + 1) {
@@ -254,11 +272,8 @@ hipError_t launch_head_logits(int dt, const void *h, const void *w, float *z, in
 }
 
 hipError_t launch_topk(const TopkArgs &a, int B, hipStream_t st) {
-  dim3 grid(B * a.n_heads);
-  if (a.kmax <= 16)
-    hipLaunchKernelGGL(topk_assemble<16>, grid, dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL(topk_assemble<32>, grid, dim3(256), 0, st, a);
+  hipLaunchKernelGGL(topk_partial, dim3(B * a.n_heads * a.nsplit), dim3(kSel), 0, st, a);
+  hipLaunchKernelGGL(topk_merge, dim3(B * a.n_heads), dim3(kSel), 0, st, a);
   return hipGetLastError();
 }
 

@@ -55,7 +55,7 @@ __device__ __forceinline__ Item decode_item(const AttnArgs &a, int idx) {
 }
 
 template <int WAVES>
-__global__ __launch_bounds__(WAVES * 64) void tree_attn_bf16(AttnArgs a) {
+__global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void tree_attn_bf16(AttnArgs a) {
   constexpr int NT = WAVES * 64;
   constexpr int RB = 32 * WAVES;
   __shared__ __attribute__((aligned(16))) uint16_t Ks[TK * KPITCH];
@@ -193,22 +193,23 @@ __global__ __launch_bounds__(WAVES * 64) void tree_attn_bf16(AttnArgs a) {
       }
     }
     // Accumulator entry r of sub-block sb is key kt + 32sb + 8(r/4) + 4h + r%4.
+    // Scores stay unscaled; the running max m is kept in scaled log2 units.
     const bool full = kt + TK <= min(k1, L);
     float tmax = -INFINITY;
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float s = sc[sb][r] * a.scale_log2;
+        float s = sc[sb][r];
         if (!full) {
-          int t = kt + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
-          bool vis = t < k1 && (t < L || ((my_anc[(t - L) >> 5] >> ((t - L) & 31)) & 1u));
+          const int t = kt + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
+          const bool vis = t < k1 && (t < L || ((my_anc[(t - L) >> 5] >> ((t - L) & 31)) & 1u));
           s = vis ? s : -INFINITY;
         }
         sc[sb][r] = s;
         tmax = fmaxf(tmax, s);
       }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    tmax = max_with_other_half(tmax) * a.scale_log2;
     const float m_new = fmaxf(m, tmax);
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
     const float alpha = fast_exp2(m - m_use);
@@ -221,16 +222,18 @@ __global__ __launch_bounds__(WAVES * 64) void tree_attn_bf16(AttnArgs a) {
       for (int mh = 0; mh < 2; ++mh)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          float p0 = fast_exp2(sc[sb][8 * mh + 2 * j] - m_use);
-          float p1 = fast_exp2(sc[sb][8 * mh + 2 * j + 1] - m_use);
+          const float p0 = fast_exp2(fmaf(sc[sb][8 * mh + 2 * j], a.scale_log2, -m_use));
+          const float p1 = fast_exp2(fmaf(sc[sb][8 * mh + 2 * j + 1], a.scale_log2, -m_use));
           psum += p0 + p1;
           pk[sb][mh][j] = pack_bf16x2(p0, p1);
         }
     lsum = lsum * alpha + psum;
+    if (__any(alpha != 1.f)) {          // the running max moved for some row of this wave
 #pragma unroll
-    for (int i = 0; i < D / 32; ++i)
+      for (int i = 0; i < D / 32; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) O[i][r] *= alpha;
+        for (int r = 0; r < 16; ++r) O[i][r] *= alpha;
+    }
 
     // O^T += V^T P^T.  B operand slot 8h + i <-> key 16mh + 8(i/4) + 4h + i%4 of
     // sub-block sb; the A operand reads V^T in the same key order.
@@ -251,7 +254,7 @@ __global__ __launch_bounds__(WAVES * 64) void tree_attn_bf16(AttnArgs a) {
       }
   }
 
-  const float ltot = lsum + __shfl_xor(lsum, 32);
+  const float ltot = sum_with_other_half(lsum);
   if (!row_ok) return;
   // O^T entry r of d-block i is d = 32i + 8(r/4) + 4h + r%4 of this lane's row.
   if (S.nch == 1) {
@@ -283,12 +286,16 @@ __global__ __launch_bounds__(WAVES * 64) void tree_attn_bf16(AttnArgs a) {
   }
 }
 
-// Merge the chunk partials of one (sequence, KV head, row block) in chunk order.
+// Merge the chunk partials of one (sequence, KV head, row block) in chunk order;
+// each block handles kCombineRows rows of the row block.
+constexpr int kCombineRows = 256 / (D / 4);   // 8 rows x 32 float4 columns per block
+
 template <int WAVES>
 __global__ __launch_bounds__(256) void tree_attn_combine(AttnArgs a) {
   constexpr int RB = 32 * WAVES;
-  const int idx = blockIdx.x;
-  int s = -1;
+  constexpr int PARTS = RB / kCombineRows;
+  const int idx = blockIdx.x / PARTS, part = blockIdx.x % PARTS;
+  int s = 0;
   for (int j = 0; j < a.nseq; ++j)
     if (a.seq[j].nch > 1 && a.seq[j].citem0 <= idx) s = j;
   const AttnSeq &S = a.seq[s];
@@ -297,28 +304,27 @@ __global__ __launch_bounds__(256) void tree_attn_combine(AttnArgs a) {
   const int rows = S.N * a.group;
   const int64_t pf = attn_partial_floats(RB);
   const float *base = a.part + ((int64_t)S.part0 + ((int64_t)kvh * S.nrb + rb) * S.nch) * pf;
-  for (int e = threadIdx.x; e < RB * (D / 4); e += 256) {
-    const int r = e / (D / 4), d4 = (e % (D / 4)) * 4;
-    const int row = rb * RB + r;
-    if (row >= rows) continue;
-    float M = -INFINITY;
-    for (int c = 0; c < S.nch; ++c) M = fmaxf(M, base[c * pf + (int64_t)RB * D + r]);
-    float l = 0.f, o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
-    for (int c = 0; c < S.nch; ++c) {
-      const float *sl = base + c * pf;
-      const float w = fast_exp2(sl[(int64_t)RB * D + r] - M);
-      l += w * sl[(int64_t)RB * D + RB + r];
-      float4 o = *reinterpret_cast<const float4 *>(sl + (int64_t)r * D + d4);
-      o0 += w * o.x;
-      o1 += w * o.y;
-      o2 += w * o.z;
-      o3 += w * o.w;
-    }
-    const float inv = 1.f / l;
-    const int node = row / a.group, hq = kvh * a.group + row % a.group;
-    uint16_t *op = static_cast<uint16_t *>(a.out) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D + d4;
-    *reinterpret_cast<uint2 *>(op) = uint2{pack_bf16x2(o0 * inv, o1 * inv), pack_bf16x2(o2 * inv, o3 * inv)};
+  const int r = part * kCombineRows + threadIdx.x / (D / 4);
+  const int d4 = (threadIdx.x % (D / 4)) * 4;
+  const int row = rb * RB + r;
+  if (row >= rows) return;
+  float M = -INFINITY;
+  for (int c = 0; c < S.nch; ++c) M = fmaxf(M, base[c * pf + (int64_t)RB * D + r]);
+  float l = 0.f, o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
+  for (int c = 0; c < S.nch; ++c) {
+    const float *sl = base + c * pf;
+    const float w = fast_exp2(sl[(int64_t)RB * D + r] - M);
+    l += w * sl[(int64_t)RB * D + RB + r];
+    const float4 o = *reinterpret_cast<const float4 *>(sl + (int64_t)r * D + d4);
+    o0 += w * o.x;
+    o1 += w * o.y;
+    o2 += w * o.z;
+    o3 += w * o.w;
   }
+  const float inv = 1.f / l;
+  const int node = row / a.group, hq = kvh * a.group + row % a.group;
+  uint16_t *op = static_cast<uint16_t *>(a.out) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D + d4;
+  *reinterpret_cast<uint2 *>(op) = uint2{pack_bf16x2(o0 * inv, o1 * inv), pack_bf16x2(o2 * inv, o3 * inv)};
 }
 
 // fp32 path: one wave per (node, query head); lanes own head-dimension elements
@@ -362,10 +368,10 @@ __global__ __launch_bounds__(256) void tree_attn_f32(AttnArgs a, int node_begin,
 hipError_t launch_tree_attn_bf16(const AttnArgs &a, int waves, hipStream_t st) {
   if (waves == 2) {
     hipLaunchKernelGGL(tree_attn_bf16<2>, dim3(a.items), dim3(128), 0, st, a);
-    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<2>, dim3(a.citems), dim3(256), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<2>, dim3(a.citems * (64 / kCombineRows)), dim3(256), 0, st, a);
   } else {
     hipLaunchKernelGGL(tree_attn_bf16<4>, dim3(a.items), dim3(256), 0, st, a);
-    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<4>, dim3(a.citems), dim3(256), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<4>, dim3(a.citems * (128 / kCombineRows)), dim3(256), 0, st, a);
   }
   return hipGetLastError();
 }

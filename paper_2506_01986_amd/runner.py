@@ -58,7 +58,7 @@ class VerifyStep:
         self.path = torch.empty((B, self.path_stride), **i32)
         self.next_tok = torch.empty(B, **i32)
         self.base_logits = None
-        ws = max(sm.workspace_bytes(sm.WS_TOPK, self.dt, self.trees, None, nh, cfg.vocab) if not keep_logits else 0,
+        ws = max(sm.workspace_bytes(sm.WS_TOPK, self.dt, self.trees, None, nh, cfg.vocab),
                  sm.workspace_bytes(sm.WS_ATTN, self.dt, self.trees, self.kv, cfg.n_q),
                  sm.workspace_bytes(sm.WS_ACCEPT, self.dt, self.trees, None, mode))
         self.ws_bytes = ws
