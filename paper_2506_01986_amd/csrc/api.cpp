@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <numeric>
 #include <string>
 #include <vector>
@@ -130,8 +131,16 @@ int hip_status(hipError_t e, const char *what) {
 constexpr int kTargetItems = 512;   // >= 2 work items per compute unit (256 CUs)
 constexpr int kMinChunk = 512;      // keys per chunk when splitting the KV range
 
+// Tuning overrides (they change the work split, never the result beyond
+// rounding): SPECMEMO_ATTN_ITEMS = target work items, SPECMEMO_ATTN_CHUNK = fixed
+// chunk length in keys (a multiple of 64; 0 disables splitting).
+int env_int(const char *name, int dflt) {
+  const char *v = getenv(name);
+  return v && *v ? atoi(v) : dflt;
+}
+
 struct AttnPlan {
-  int waves = 4;
+  int rb = 128;        // query rows per work item: 64 (MHA-sized trees) or 128
   std::vector<std::vector<AttnSeq>> groups;   // sequences per launch, in launch order
   std::vector<int> items, citems;
   size_t ws_bytes = 0;
@@ -139,8 +148,8 @@ struct AttnPlan {
 
 void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *kv, int n_q, AttnPlan *p) {
   const int g = n_q / kv->n_kv;
-  p->waves = ti.max_nodes * g <= 64 ? 2 : 4;
-  const int RB = 32 * p->waves;
+  p->rb = ti.max_nodes * g <= 64 ? 64 : 128;
+  const int RB = p->rb;
   std::vector<int> order(ti.B);
   std::iota(order.begin(), order.end(), 0);
   std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return kv->seq_len_h[x] > kv->seq_len_h[y]; });
@@ -152,9 +161,13 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
     base_items += (int64_t)kv->n_kv * nrb;
     weighted += (int64_t)kv->n_kv * nrb * (kv->seq_len_h[b] + N);
   }
+  static const int target = std::max(1, env_int("SPECMEMO_ATTN_ITEMS", kTargetItems));
+  static const int fixed_chunk = env_int("SPECMEMO_ATTN_CHUNK", -1);
   int ch_len = INT32_MAX;
-  if (base_items < kTargetItems) {
-    int64_t c = (weighted + kTargetItems - 1) / kTargetItems;
+  if (fixed_chunk > 0) {
+    ch_len = std::max(kAttnKeyTile, fixed_chunk / kAttnKeyTile * kAttnKeyTile);
+  } else if (fixed_chunk < 0 && base_items < target) {
+    int64_t c = (weighted + target - 1) / target;
     c = std::max<int64_t>(kMinChunk, (c + kAttnKeyTile - 1) / kAttnKeyTile * kAttnKeyTile);
     ch_len = (int)std::min<int64_t>(c, INT32_MAX / 2);
   }
@@ -346,7 +359,7 @@ int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmem
     for (int i = 0; i < a.nseq; ++i) a.seq[i] = p.groups[gi][i];
     a.items = p.items[gi];
     a.citems = p.citems[gi];
-    hipError_t e = launch_tree_attn_bf16(a, p.waves, st);
+    hipError_t e = launch_tree_attn_bf16(a, p.rb, st);
     if (e != hipSuccess) return hip_status(e, "tree attention launch");
   }
   return ok();

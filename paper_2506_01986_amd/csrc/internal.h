@@ -64,11 +64,12 @@ struct AttnArgs {
 
 constexpr int kAttnKeyTile = 64;
 constexpr int kAttnHeadDim = 128;
-// floats per partial slot of a row block: unnormalised O, running max, running sum
+// 4-byte words per partial slot of a row block: unnormalised O in bf16
+// ([rows][head_dim]), then the running max and running sum in fp32 ([rows] each)
 __host__ __device__ constexpr int64_t attn_partial_floats(int rows_per_block) {
-  return (int64_t)rows_per_block * (kAttnHeadDim + 2);
+  return (int64_t)rows_per_block * (kAttnHeadDim / 2 + 2);
 }
-hipError_t launch_tree_attn_bf16(const AttnArgs &a, int waves, hipStream_t st);
+hipError_t launch_tree_attn_bf16(const AttnArgs &a, int rows_per_block, hipStream_t st);
 hipError_t launch_tree_attn_f32(const AttnArgs &a, int node_begin, int node_count, hipStream_t st);
 
 // ---- acceptance ------------------------------------------------------------------

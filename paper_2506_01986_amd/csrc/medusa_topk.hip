@@ -19,7 +19,7 @@ namespace {
 
 constexpr int kRowsPerWave = 64;   // four 16-row A tiles
 constexpr int kWaves = 4;
-constexpr int kUnroll = 4;         // k-steps of 32 issued before their MFMAs
+constexpr int kUnroll = 2;         // k-steps of 32 issued before their MFMAs
 
 template <int NB>   // 16-wide batch tiles contracted per weight load
 __global__ __launch_bounds__(kWaves * 64) void head_logits_bf16(
@@ -27,7 +27,8 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_bf16(
     int hidden, int vocab, int n_heads) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int head = blockIdx.y, b0 = blockIdx.z * 16 * NB;
-  const int row0 = (blockIdx.x * kWaves + wave) * kRowsPerWave;
+  const int gwave = blockIdx.x * kWaves + wave;
+  const int row0 = gwave * kRowsPerWave;
   if (row0 >= vocab) return;
   const int r16 = lane & 15, kq = lane >> 4;
 
@@ -52,8 +53,12 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_bf16(
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[n][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  int k = 0;
-  for (; k + 32 * kUnroll <= hidden; k += 32 * kUnroll) {
+  // Every wave starts its k sweep at a different step: all waves reading their
+  // rows (16 KB apart) at the same offset would load the same HBM channels.
+  const int steps = hidden / (32 * kUnroll);
+  const int rot = steps ? (gwave + head * 977) % steps : 0;
+  for (int s0 = 0; s0 < steps; ++s0) {
+    const int k = (s0 + rot < steps ? s0 + rot : s0 + rot - steps) * 32 * kUnroll;
     uint4 a[kUnroll][4], bq[kUnroll][NB];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
@@ -74,6 +79,7 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_bf16(
                                                               bv, acc[n][t], 0, 0, 0);
       }
   }
+  int k = steps * 32 * kUnroll;
   for (; k < hidden; k += 32) {   // tail: hidden % 8 == 0, so a lane's 8 elements are all in or all out
     const bool in = k + kq * 8 < hidden;
     uint4 a[4];

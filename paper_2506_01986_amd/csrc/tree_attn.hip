@@ -33,8 +33,7 @@ namespace {
 
 constexpr int D = kAttnHeadDim;
 constexpr int TK = kAttnKeyTile;
-constexpr int KPITCH = D + 8;      // bf16 elements per K row in LDS (272 B)
-constexpr int VPITCH = TK + 4;     // bf16 elements per V^T row in LDS (136 B)
+constexpr float kRescaleSlack = 8.f;   // log2 units: softmax weights stay <= 256 between rescales
 
 struct Item {
   int s, kvh, rb, ch;
@@ -54,12 +53,27 @@ __device__ __forceinline__ Item decode_item(const AttnArgs &a, int idx) {
   return it;
 }
 
-template <int WAVES>
-__global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void tree_attn_bf16(AttnArgs a) {
-  constexpr int NT = WAVES * 64;
-  constexpr int RB = 32 * WAVES;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[TK * KPITCH];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VPITCH];
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short s16x4_t __attribute__((__vector_size__(8)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+
+// LDS swizzles (16-byte chunk index c of tile row r).  K rows are read 16 rows
+// at a time at one chunk (MFMA A operand): chunk c of row r sits at c ^ (r % 16).
+// V rows are read by the transposing load 4 rows x 4 chunks at a time:
+// chunk c of row r sits at c ^ 4 (r % 4).
+__device__ __forceinline__ int kswz(int r, int c) { return c ^ (r & 15); }
+__device__ __forceinline__ int vswz(int r, int c) { return c ^ ((r & 3) << 2); }
+
+// WAVES waves per block, each owning NRB2 x 32 query rows; STAGES-deep ring of
+// K/V tiles filled by direct loads.  With NRB2 = 2 every K/V fragment read from
+// LDS feeds two matrix-core products.
+// MINB: blocks that must fit on one compute unit (bounds the registers).
+template <int WAVES, int NRB2, int STAGES, int MINB>
+__global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
+  constexpr int RB = 32 * NRB2 * WAVES;
+  constexpr int TILE = TK * D * 2;            // bytes of one K or V tile (16 KB)
+  constexpr int IPW = TILE / 1024 / WAVES;    // 1 KB direct loads per wave per tile and operand
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[STAGES][2][TILE];
   __shared__ uint32_t anc[kMaxNodes][4];
 
   const Item it = decode_item(a, blockIdx.x);
@@ -70,11 +84,11 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void tree_attn_bf16
   const int rows = N * g;
 
   // Ancestor-or-self bitmask of every node of this tree (local ids).
-  for (int n = tid; n < N; n += NT) {
+  for (int n = tid; n < N; n += WAVES * 64) {
     uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
     for (int u = n; u >= 0; u = a.parent[S.node0 + u]) {
-      uint32_t bit = 1u << (u & 31);
-      int w = u >> 5;
+      const uint32_t bit = 1u << (u & 31);
+      const int w = u >> 5;
       m0 |= w == 0 ? bit : 0u;
       m1 |= w == 1 ? bit : 0u;
       m2 |= w == 2 ? bit : 0u;
@@ -86,202 +100,239 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void tree_attn_bf16
     anc[n][3] = m3;
   }
 
-  // This lane's query row.
-  const int my_row = it.rb * RB + wave * 32 + (lane & 31);
-  const bool row_ok = my_row < rows;
-  const int node = row_ok ? my_row / g : 0;
-  const int hq = it.kvh * g + (row_ok ? my_row % g : 0);
-  const uint16_t *qbase = static_cast<const uint16_t *>(a.q) +
-                          ((int64_t)(S.node0 + node) * a.n_q + hq) * D + 8 * h;
-  bf16x8 qf[D / 16];
+  // This lane's query rows (one per 32-row block of the wave).
+  int my_row[NRB2], node[NRB2], hq[NRB2];
+  bool row_ok[NRB2];
+  bf16x8 qf[NRB2][D / 16];
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks)
-    qf[ks] = __builtin_bit_cast(bf16x8, ld16_or_zero(row_ok, qbase + 16 * ks));
+  for (int b2 = 0; b2 < NRB2; ++b2) {
+    my_row[b2] = it.rb * RB + (wave * NRB2 + b2) * 32 + (lane & 31);
+    row_ok[b2] = my_row[b2] < rows;
+    node[b2] = row_ok[b2] ? my_row[b2] / g : 0;
+    hq[b2] = it.kvh * g + (row_ok[b2] ? my_row[b2] % g : 0);
+    const uint16_t *qbase = static_cast<const uint16_t *>(a.q) +
+                            ((int64_t)(S.node0 + node[b2]) * a.n_q + hq[b2]) * D + 8 * h;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks)
+      qf[b2][ks] = __builtin_bit_cast(bf16x8, ld16_or_zero(row_ok[b2], qbase + 16 * ks));
+  }
 
   // Key range of this chunk: chunk boundaries lie inside the committed region and
   // the last chunk runs to the end of the tree rows, so every chunk holds at
   // least one key visible to every row.
   const int k0 = it.ch * S.ch_len;
   const int k1 = it.ch == S.nch - 1 ? L + N : k0 + S.ch_len;
-
+  const int ntiles = (k1 - k0 + TK - 1) / TK;
   const uint16_t *Kg = static_cast<const uint16_t *>(a.k) + ((int64_t)it.kvh * a.cap_total + S.base) * D;
   const uint16_t *Vg = static_cast<const uint16_t *>(a.v) + ((int64_t)it.kvh * a.cap_total + S.base) * D;
 
-  // Tile loaders.  K: 1024 16-byte chunks per tile.  V: per thread 4 keys x 8 d,
-  // written transposed (8 x 8-byte stores).
-  constexpr int KCH = TK * D / 8 / NT;        // K chunks per thread
-  constexpr int VIT = (TK / 4) * (D / 8) / NT;  // V items per thread
-  uint4 kr[KCH];
-  uint4 vr[VIT][4];
-  auto load_tile = [&](int kt) {
+  // Direct loads of tile j into its ring slot: lane l of load i writes LDS bytes
+  // [1024 i + 16 l, +16), i.e. tile row r = 4 i + l / 16 at physical chunk l % 16.
+  // Rows past the chunk end repeat its last row (finite values, masked out).
+  // Per-lane byte offsets of this wave's loads inside a tile (row r, swizzled
+  // chunk), fixed for the whole chunk; full tiles add a wave-uniform tile base.
+  int koff[IPW], voff[IPW], lrow[IPW];
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) {
-      int q = tid + c * NT;
-      int key = q >> 4, col = (q & 15) * 8;
-      int t = kt + key;
-      kr[c] = ld16_or_zero(t < k1, Kg + (int64_t)t * D + col);
-    }
+  for (int u = 0; u < IPW; ++u) {
+    const int i = wave * IPW + u;
+    const int r = 4 * i + (lane >> 4), pc = lane & 15;
+    lrow[u] = r;
+    koff[u] = r * (D * 2) + 16 * kswz(r, pc);
+    voff[u] = r * (D * 2) + 16 * vswz(r, pc);
+  }
+  const uint8_t *Kb = reinterpret_cast<const uint8_t *>(Kg);
+  const uint8_t *Vb = reinterpret_cast<const uint8_t *>(Vg);
+  auto issue = [&](int j) {
+    const int kt = k0 + j * TK;
+    uint8_t *ks = ring[j % STAGES][0];
+    uint8_t *vs = ring[j % STAGES][1];
+    if (kt + TK <= k1) {
+      const uint8_t *kb = Kb + (int64_t)kt * (D * 2), *vb = Vb + (int64_t)kt * (D * 2);
 #pragma unroll
-    for (int c = 0; c < VIT; ++c) {
-      int q = tid + c * NT;
-      int kg = q & 15, dc = q >> 4;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        int t = kt + 4 * kg + j;
-        vr[c][j] = ld16_or_zero(t < k1, Vg + (int64_t)t * D + dc * 8);
+      for (int u = 0; u < IPW; ++u) {
+        const int i = wave * IPW + u;
+        __builtin_amdgcn_global_load_lds((const void *)(kb + koff[u]), (lds_void_t *)(ks + 1024 * i), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void *)(vb + voff[u]), (lds_void_t *)(vs + 1024 * i), 16, 0, 0);
       }
-    }
-  };
-  auto store_tile = [&]() {
+    } else {                             // last tile: rows past the chunk end repeat its last row
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) {
-      int q = tid + c * NT;
-      int key = q >> 4, col = (q & 15) * 8;
-      *reinterpret_cast<uint4 *>(&Ks[key * KPITCH + col]) = kr[c];
-    }
-#pragma unroll
-    for (int c = 0; c < VIT; ++c) {
-      int q = tid + c * NT;
-      int kg = q & 15, dc = q >> 4;
-      const uint32_t w0[4] = {vr[c][0].x, vr[c][0].y, vr[c][0].z, vr[c][0].w};
-      const uint32_t w1[4] = {vr[c][1].x, vr[c][1].y, vr[c][1].z, vr[c][1].w};
-      const uint32_t w2[4] = {vr[c][2].x, vr[c][2].y, vr[c][2].z, vr[c][2].w};
-      const uint32_t w3[4] = {vr[c][3].x, vr[c][3].y, vr[c][3].z, vr[c][3].w};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        // element e of keys 4kg..4kg+3 packed as one 8-byte row segment of V^T
-        const int wi = e >> 1;
-        uint2 pk;
-        if (e & 1) {
-          pk.x = (w0[wi] >> 16) | (w1[wi] & 0xFFFF0000u);
-          pk.y = (w2[wi] >> 16) | (w3[wi] & 0xFFFF0000u);
-        } else {
-          pk.x = (w0[wi] & 0xFFFFu) | (w1[wi] << 16);
-          pk.y = (w2[wi] & 0xFFFFu) | (w3[wi] << 16);
-        }
-        *reinterpret_cast<uint2 *>(&Vt[(dc * 8 + e) * VPITCH + 4 * kg]) = pk;
+      for (int u = 0; u < IPW; ++u) {
+        const int i = wave * IPW + u;
+        const int64_t t = min(kt + lrow[u], k1 - 1);
+        const int cofs = koff[u] - lrow[u] * (D * 2), vcofs = voff[u] - lrow[u] * (D * 2);
+        __builtin_amdgcn_global_load_lds((const void *)(Kb + t * (D * 2) + cofs), (lds_void_t *)(ks + 1024 * i), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void *)(Vb + t * (D * 2) + vcofs), (lds_void_t *)(vs + 1024 * i), 16, 0, 0);
       }
     }
   };
 
-  float m = -INFINITY, lsum = 0.f;
-  f32x16 O[D / 32];
+  float m[NRB2], lsum[NRB2];
+  f32x16 O[NRB2][D / 32];
 #pragma unroll
-  for (int i = 0; i < D / 32; ++i)
+  for (int b2 = 0; b2 < NRB2; ++b2) {
+    m[b2] = -INFINITY;
+    lsum[b2] = 0.f;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) O[i][r] = 0.f;
+    for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) O[b2][i][r] = 0.f;
+  }
 
-  const uint32_t *my_anc = anc[node];
-  load_tile(k0);
-  for (int kt = k0; kt < k1; kt += TK) {
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (kt + TK < k1) load_tile(kt + TK);
+  // Transposing-load source role of this lane within its 16-lane group:
+  // source lane 4j + q supplies keys row j, head-dim columns 4q..4q+3 of the
+  // group's 16 columns; destination lane o then holds 4 keys of column o.
+  const int tr_j = (lane & 15) >> 2, tr_q = lane & 3;
+  const int tr_d = 16 * ((lane >> 4) & 1) + 4 * tr_q;   // column within a 32-wide d block
 
-    // S^T for two 32-key sub-blocks.
-    f32x16 sc[2];
+  // One tile, one 32-key sub-block at a time: S^T (K rows as the A operand),
+  // online softmax, then O^T += V^T P^T with V^T from the transposing loads.
+  auto compute = [&](int j) {
+    const int kt0 = k0 + j * TK;
+    const uint8_t *ks = ring[j % STAGES][0];
+    const uint8_t *vs = ring[j % STAGES][1];
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
+      const int kt = kt0 + 32 * sb;
+      const int r = sb * 32 + (lane & 31);
+      bf16x8 kf[D / 16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sc[sb][r] = 0.f;
-      const uint16_t *kp = &Ks[(sb * 32 + (lane & 31)) * KPITCH + 8 * h];
+      for (int ks8 = 0; ks8 < D / 16; ++ks8)
+        kf[ks8] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const uint4 *>(ks + r * (D * 2) + 16 * kswz(r, 2 * ks8 + h)));
+      f32x16 sc[NRB2];
 #pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(kp + 16 * ks));
-        sc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc[sb], 0, 0, 0);
+      for (int b2 = 0; b2 < NRB2; ++b2) {
+#pragma unroll
+        for (int r2 = 0; r2 < 16; ++r2) sc[b2][r2] = 0.f;
+#pragma unroll
+        for (int ks8 = 0; ks8 < D / 16; ++ks8)
+          sc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks8], qf[b2][ks8], sc[b2], 0, 0, 0);
+      }
+      // Accumulator entry r of the sub-block is key kt + 8(r/4) + 4h + r%4.
+      // Scores stay unscaled; the running max m is kept in scaled log2 units.
+      const bool full = kt + 32 <= min(k1, L);
+      uint32_t pk[NRB2][2][4];
+#pragma unroll
+      for (int b2 = 0; b2 < NRB2; ++b2) {
+        float tmax = -INFINITY;
+        if (full) {
+#pragma unroll
+          for (int r2 = 0; r2 < 16; ++r2) tmax = fmaxf(tmax, sc[b2][r2]);
+        } else {
+          const uint32_t *my_anc = anc[node[b2]];
+#pragma unroll
+          for (int r2 = 0; r2 < 16; ++r2) {
+            float sv = sc[b2][r2];
+            const int t = kt + 8 * (r2 >> 2) + 4 * h + (r2 & 3);
+            const bool vis = t < k1 && (t < L || ((my_anc[(t - L) >> 5] >> ((t - L) & 31)) & 1u));
+            sv = vis ? sv : -INFINITY;
+            sc[b2][r2] = sv;
+            tmax = fmaxf(tmax, sv);
+          }
+        }
+        tmax = max_with_other_half(tmax) * a.scale_log2;
+        // Lazy rescaling: the reference max m moves only when a score exceeds it
+        // by more than kRescaleSlack (log2 units), so p <= 2^kRescaleSlack and
+        // O is rescaled in the rare tiles where that happens.
+        if (tmax > m[b2] + kRescaleSlack) {
+          const float m_new = tmax;
+          const float alpha = m[b2] == -INFINITY ? 0.f : fast_exp2(m[b2] - m_new);
+          m[b2] = m_new;
+          lsum[b2] *= alpha;
+#pragma unroll
+          for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+            for (int r2 = 0; r2 < 16; ++r2) O[b2][i][r2] *= alpha;
+        }
+        const float m_use = m[b2] == -INFINITY ? 0.f : m[b2];
+        float psum = 0.f;
+#pragma unroll
+        for (int mh = 0; mh < 2; ++mh)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float p0 = fast_exp2(fmaf(sc[b2][8 * mh + 2 * q], a.scale_log2, -m_use));
+            const float p1 = fast_exp2(fmaf(sc[b2][8 * mh + 2 * q + 1], a.scale_log2, -m_use));
+            psum += p0 + p1;
+            pk[b2][mh][q] = pack_bf16x2(p0, p1);
+          }
+        lsum[b2] += psum;
+      }
+      // B operand slot 8h + s <-> key 16mh + 8(s/4) + 4h + s%4 of the sub-block;
+      // the transposing loads return V^T in the same key order.
+#pragma unroll
+      for (int mh = 0; mh < 2; ++mh) {
+        const int r0 = 32 * sb + 16 * mh + 4 * h + tr_j;
+        bf16x8 vf[D / 32];
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i) {
+          const int d = 32 * i + tr_d;
+          const int c = d >> 3, cb = (d & 7) * 2;
+          const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_s16x4_t *)(vs + r0 * (D * 2) + 16 * vswz(r0, c) + cb));
+          const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_s16x4_t *)(vs + (r0 + 8) * (D * 2) + 16 * vswz(r0 + 8, c) + cb));
+          vf[i] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+#pragma unroll
+        for (int b2 = 0; b2 < NRB2; ++b2) {
+          const bf16x8 pf = __builtin_bit_cast(bf16x8, uint4{pk[b2][mh][0], pk[b2][mh][1], pk[b2][mh][2], pk[b2][mh][3]});
+#pragma unroll
+          for (int i = 0; i < D / 32; ++i)
+            O[b2][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pf, O[b2][i], 0, 0, 0);
+        }
       }
     }
-    // Accumulator entry r of sub-block sb is key kt + 32sb + 8(r/4) + 4h + r%4.
-    // Scores stay unscaled; the running max m is kept in scaled log2 units.
-    const bool full = kt + TK <= min(k1, L);
-    float tmax = -INFINITY;
+  };
+
+  // STAGES-deep pipeline: tiles j+1 .. j+STAGES-1 are in flight while tile j is
+  // computed.  Every wave issues 2 * IPW direct loads per tile, so "tile j
+  // landed" is "at most 2 * IPW * (tiles issued after j) loads outstanding".
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
+  for (int j = 0; j < STAGES - 1; ++j)
+    if (j < ntiles) issue(j);
+  for (int j = 0; j < ntiles; ++j) {
+    const int after = min(ntiles - 1 - j, STAGES - 2);   // tiles issued after j so far
+    if (STAGES == 3 && after == 1)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * IPW) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();                    // tile j visible to all waves; all waves are done with tile j-1
+    if (j + STAGES - 1 < ntiles) issue(j + STAGES - 1);
+    compute(j);
+  }
+
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float s = sc[sb][r];
-        if (!full) {
-          const int t = kt + 32 * sb + 8 * (r >> 2) + 4 * h + (r & 3);
-          const bool vis = t < k1 && (t < L || ((my_anc[(t - L) >> 5] >> ((t - L) & 31)) & 1u));
-          s = vis ? s : -INFINITY;
-        }
-        sc[sb][r] = s;
-        tmax = fmaxf(tmax, s);
-      }
-    tmax = max_with_other_half(tmax) * a.scale_log2;
-    const float m_new = fmaxf(m, tmax);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m - m_use);
-    m = m_new;
-    float psum = 0.f;
-    uint32_t pk[2][2][4];
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int mh = 0; mh < 2; ++mh)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float p0 = fast_exp2(fmaf(sc[sb][8 * mh + 2 * j], a.scale_log2, -m_use));
-          const float p1 = fast_exp2(fmaf(sc[sb][8 * mh + 2 * j + 1], a.scale_log2, -m_use));
-          psum += p0 + p1;
-          pk[sb][mh][j] = pack_bf16x2(p0, p1);
-        }
-    lsum = lsum * alpha + psum;
-    if (__any(alpha != 1.f)) {          // the running max moved for some row of this wave
+  for (int b2 = 0; b2 < NRB2; ++b2) {
+    const float ltot = sum_with_other_half(lsum[b2]);
+    if (!row_ok[b2]) continue;
+    // O^T entry r of d-block i is d = 32i + 8(r/4) + 4h + r%4 of this lane's row.
+    if (S.nch == 1) {
+      const float inv = 1.f / ltot;
+      uint16_t *op = static_cast<uint16_t *>(a.out) + ((int64_t)(S.node0 + node[b2]) * a.n_q + hq[b2]) * D;
 #pragma unroll
       for (int i = 0; i < D / 32; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) O[i][r] *= alpha;
-    }
-
-    // O^T += V^T P^T.  B operand slot 8h + i <-> key 16mh + 8(i/4) + 4h + i%4 of
-    // sub-block sb; the A operand reads V^T in the same key order.
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int mh = 0; mh < 2; ++mh) {
-        bf16x8 pf = __builtin_bit_cast(bf16x8, uint4{pk[sb][mh][0], pk[sb][mh][1], pk[sb][mh][2], pk[sb][mh][3]});
-        const int kofs = 32 * sb + 16 * mh + 4 * h;
-#pragma unroll
-        for (int i = 0; i < D / 32; ++i) {
-          const uint16_t *vp = &Vt[(32 * i + (lane & 31)) * VPITCH + kofs];
-          uint2 lo = *reinterpret_cast<const uint2 *>(vp);
-          uint2 hi = *reinterpret_cast<const uint2 *>(vp + 8);
-          bf16x8 vf = __builtin_bit_cast(bf16x8, uint4{lo.x, lo.y, hi.x, hi.y});
-          O[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, O[i], 0, 0, 0);
+        for (int q4 = 0; q4 < 4; ++q4) {
+          uint2 v = {pack_bf16x2(O[b2][i][4 * q4] * inv, O[b2][i][4 * q4 + 1] * inv),
+                     pack_bf16x2(O[b2][i][4 * q4 + 2] * inv, O[b2][i][4 * q4 + 3] * inv)};
+          *reinterpret_cast<uint2 *>(op + 32 * i + 8 * q4 + 4 * h) = v;
         }
+    } else {
+      const int local_row = my_row[b2] - it.rb * RB;
+      float *slot = a.part + ((int64_t)S.part0 + ((int64_t)it.kvh * S.nrb + it.rb) * S.nch + it.ch) *
+                                 (int64_t)attn_partial_floats(RB);
+      uint16_t *po = reinterpret_cast<uint16_t *>(slot) + (int64_t)local_row * D;
+#pragma unroll
+      for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+          *reinterpret_cast<uint2 *>(po + 32 * i + 8 * q4 + 4 * h) =
+              uint2{pack_bf16x2(O[b2][i][4 * q4], O[b2][i][4 * q4 + 1]),
+                    pack_bf16x2(O[b2][i][4 * q4 + 2], O[b2][i][4 * q4 + 3])};
+      if (h == 0) {
+        slot[(int64_t)RB * D / 2 + local_row] = m[b2];
+        slot[(int64_t)RB * D / 2 + RB + local_row] = ltot;
       }
-  }
-
-  const float ltot = sum_with_other_half(lsum);
-  if (!row_ok) return;
-  // O^T entry r of d-block i is d = 32i + 8(r/4) + 4h + r%4 of this lane's row.
-  if (S.nch == 1) {
-    const float inv = 1.f / ltot;
-    uint16_t *op = static_cast<uint16_t *>(a.out) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D;
-#pragma unroll
-    for (int i = 0; i < D / 32; ++i)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        uint2 v = {pack_bf16x2(O[i][4 * q4] * inv, O[i][4 * q4 + 1] * inv),
-                   pack_bf16x2(O[i][4 * q4 + 2] * inv, O[i][4 * q4 + 3] * inv)};
-        *reinterpret_cast<uint2 *>(op + 32 * i + 8 * q4 + 4 * h) = v;
-      }
-  } else {
-    const int local_row = my_row - it.rb * RB;
-    float *slot = a.part + ((int64_t)S.part0 + ((int64_t)it.kvh * S.nrb + it.rb) * S.nch + it.ch) *
-                               (int64_t)attn_partial_floats(RB);
-    float *po = slot + (int64_t)local_row * D;
-#pragma unroll
-    for (int i = 0; i < D / 32; ++i)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4)
-        *reinterpret_cast<float4 *>(po + 32 * i + 8 * q4 + 4 * h) =
-            float4{O[i][4 * q4], O[i][4 * q4 + 1], O[i][4 * q4 + 2], O[i][4 * q4 + 3]};
-    if (h == 0) {
-      slot[(int64_t)RB * D + local_row] = m;
-      slot[(int64_t)RB * D + RB + local_row] = ltot;
     }
   }
 }
@@ -290,9 +341,8 @@ __global__ __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) void tree_attn_bf16
 // each block handles kCombineRows rows of the row block.
 constexpr int kCombineRows = 256 / (D / 4);   // 8 rows x 32 float4 columns per block
 
-template <int WAVES>
+template <int RB>
 __global__ __launch_bounds__(256) void tree_attn_combine(AttnArgs a) {
-  constexpr int RB = 32 * WAVES;
   constexpr int PARTS = RB / kCombineRows;
   const int idx = blockIdx.x / PARTS, part = blockIdx.x % PARTS;
   int s = 0;
@@ -309,17 +359,17 @@ __global__ __launch_bounds__(256) void tree_attn_combine(AttnArgs a) {
   const int row = rb * RB + r;
   if (row >= rows) return;
   float M = -INFINITY;
-  for (int c = 0; c < S.nch; ++c) M = fmaxf(M, base[c * pf + (int64_t)RB * D + r]);
+  for (int c = 0; c < S.nch; ++c) M = fmaxf(M, base[c * pf + (int64_t)RB * D / 2 + r]);
   float l = 0.f, o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
   for (int c = 0; c < S.nch; ++c) {
     const float *sl = base + c * pf;
-    const float w = fast_exp2(sl[(int64_t)RB * D + r] - M);
-    l += w * sl[(int64_t)RB * D + RB + r];
-    const float4 o = *reinterpret_cast<const float4 *>(sl + (int64_t)r * D + d4);
-    o0 += w * o.x;
-    o1 += w * o.y;
-    o2 += w * o.z;
-    o3 += w * o.w;
+    const float w = fast_exp2(sl[(int64_t)RB * D / 2 + r] - M);
+    l += w * sl[(int64_t)RB * D / 2 + RB + r];
+    const uint2 o = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(sl) + (int64_t)r * D + d4);
+    o0 += w * __uint_as_float(o.x << 16);
+    o1 += w * __uint_as_float(o.x & 0xFFFF0000u);
+    o2 += w * __uint_as_float(o.y << 16);
+    o3 += w * __uint_as_float(o.y & 0xFFFF0000u);
   }
   const float inv = 1.f / l;
   const int node = row / a.group, hq = kvh * a.group + row % a.group;
@@ -365,13 +415,13 @@ __global__ __launch_bounds__(256) void tree_attn_f32(AttnArgs a, int node_begin,
 
 }  // namespace
 
-hipError_t launch_tree_attn_bf16(const AttnArgs &a, int waves, hipStream_t st) {
-  if (waves == 2) {
-    hipLaunchKernelGGL(tree_attn_bf16<2>, dim3(a.items), dim3(128), 0, st, a);
-    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<2>, dim3(a.citems * (64 / kCombineRows)), dim3(256), 0, st, a);
+hipError_t launch_tree_attn_bf16(const AttnArgs &a, int rows_per_block, hipStream_t st) {
+  if (rows_per_block == 64) {
+    hipLaunchKernelGGL((tree_attn_bf16<2, 1, 2, 2>), dim3(a.items), dim3(128), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<64>, dim3(a.citems * (64 / kCombineRows)), dim3(256), 0, st, a);
   } else {
-    hipLaunchKernelGGL(tree_attn_bf16<4>, dim3(a.items), dim3(256), 0, st, a);
-    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<4>, dim3(a.citems * (128 / kCombineRows)), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((tree_attn_bf16<4, 1, 2, 2>), dim3(a.items), dim3(256), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<128>, dim3(a.citems * (128 / kCombineRows)), dim3(256), 0, st, a);
   }
   return hipGetLastError();
 }
