@@ -28,10 +28,52 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 METRIC = "verified tree tokens/sec per verify step; achieved HBM GB/s vs peak"
+# Kernels each stage launches through the C ABI (for matching rocprofv3 traces).
+STAGE_KERNELS = {"medusa_topk": ["head_logits_bf16", "topk_partial", "topk_merge"],
+                 "tree_attn": ["tree_attn_bf16", "tree_attn_combine"],
+                 "accept": ["accept_greedy"], "kv_compact": ["kv_compact_kernel"]}
+STAGE_SOURCES = {"medusa_topk": "medusa_topk.hip", "tree_attn": "tree_attn.hip",
+                 "accept": "accept.hip", "kv_compact": "kv_compact.hip"}
+
+
+def source_sha(stage):
+    import hashlib
+    path = os.path.join(ROOT, "paper_2506_01986_amd", "csrc", STAGE_SOURCES[stage])
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(stage, workload):
+    """HBM bytes per launch of a stage from a committed counter summary, or None.
+
+    profiles/<stage>_<workload>_traffic.txt holds "key: value" lines written from
+    two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) scaled by the same counters
+    on a device copy of known size; it is used only while the stage's kernel
+    source still has the recorded hash.
+    """
+    path = os.path.join(ROOT, "profiles", f"{stage}_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256_16") != source_sha(stage):
+        return None
+    return int(float(kv["hbm_bytes_per_launch"]))
 
 
 def algorithmic_bytes(wl, acc):
-    """Bytes each stage must move at minimum (per-unit figures)."""
+    """Bytes each stage must move at minimum.
+
+    medusa_topk: the l*w*hidden head weights, the hidden states, the top-k
+      lists and the tree tokens.
+    tree_attn: each sequence's committed and tree K/V rows once (2 * n_kv *
+      head_dim elements per row) plus the queries read and outputs written.
+    accept: the logit rows of the nodes on the accepted paths (greedy walk)
+      and the node tokens.
+    kv_compact: the accepted rows of K and V, read and written once.
+    """
     cfg = wl.cfg
     s = cfg.elem_bytes
     sumN = wl.total_nodes
@@ -79,10 +121,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="llama2_70b_b10")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="also run a device-to-device copy of BYTES (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the verify step is a single-GPU path here (asked for --gpus {args.gpus}). "
-              "Sharding by sequence or KV head is described in DESIGN.md; run with --gpus 1.", file=sys.stderr)
+              "The batch shards by sequence with no exchange; run one process per GPU with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -132,6 +176,12 @@ def main():
     st["tree_attn+kv_compact"] = {"ms": round(float(at), 5), "GBps": round(ab / (at * 1e-3) / 1e9, 1),
                                   "hbm_frac": round(ab / (at * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     dom = max(names, key=lambda n: st[n]["ms"])
+    if args.copy_calibration:
+        src = torch.empty(args.copy_calibration, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
     result = {
         "metric": METRIC, "value": round(wl.total_nodes / (ms * 1e-3), 1), "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
@@ -142,8 +192,9 @@ def main():
                                f"KV {cfg.kv_len_dist} {list(cfg.kv_len)}, pool {cfg.pool}",
                    "batch": cfg.B, "tree_tokens": wl.total_nodes, "kv_tokens": int(np.sum(wl.lens)),
                    "accepted_tokens": int(np.sum(acc + 1))},
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": st[dom]["GBps"], "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": st[dom]["hbm_frac"], "traffic": None},
+        "roofline": {"bound": "hbm", "kernel": dom, "kernels": STAGE_KERNELS[dom], "achieved": st[dom]["GBps"],
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": st[dom]["hbm_frac"],
+                     "traffic": measured_traffic(dom, cfg.name), "source_sha256_16": source_sha(dom)},
         "accepted_tokens_per_s": round(float(np.sum(acc + 1)) / (ms * 1e-3), 1),
         "wall_ms_per_step": round(wall / args.steps * 1e3, 5),
         "stages": st,

@@ -36,17 +36,29 @@ __device__ void row_argbest(const void *logits, int64_t row, int vocab, float *s
   int bi = INT32_MAX;
   const int64_t base = row * vocab;
   if (DT == 1 && (vocab & 7) == 0) {
+    // All of this thread's 16-byte loads of a pass are issued before any compare.
+    constexpr int U = 8;
     const uint4 *p = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(logits) + base);
-    for (int c = tid; c < vocab / 8; c += kNT) {
-      uint4 w = p[c];
-      uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+    const int nch = vocab / 8;
+    for (int c0 = 0; c0 < nch; c0 += kNT * U) {
+      uint4 w[U];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float x = bf16_to_f32(static_cast<uint16_t>(ws[e >> 1] >> ((e & 1) * 16)));
-        int v = 8 * c + e;
-        if (better(x, v, bv, bi)) {
-          bv = x;
-          bi = v;
+      for (int u = 0; u < U; ++u) {
+        const int c = c0 + u * kNT + tid;
+        w[u] = c < nch ? p[c] : uint4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};  // -inf
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c = c0 + u * kNT + tid;
+        const uint32_t ws[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x = bf16_to_f32(static_cast<uint16_t>(ws[e >> 1] >> ((e & 1) * 16)));
+          const int v = 8 * c + e;
+          if (c < nch && better(x, v, bv, bi)) {
+            bv = x;
+            bi = v;
+          }
         }
       }
     }

@@ -147,7 +147,7 @@ __global__ __launch_bounds__(256) void head_logits_f32(const float *__restrict__
 // Top-k in two levels.  Level 1: each block takes a 2048-wide slice of one
 // (sequence, head) logit row and emits the slice's kmax best (value, id) pairs.
 // Level 2: one block per row merges the slices' candidates into the top-k and
-// writes the tree tokens of that head's level.  Both levels pick k times the
+// writes the tree tokens of that head's level.  Level 1 picks k times the
 // block-wide best remaining pair (larger value, then lower id).
 constexpr int kSel = 256;        // threads per selection block
 constexpr int kPer = 8;          // pairs held per thread
@@ -222,27 +222,57 @@ __global__ __launch_bounds__(kSel) void topk_partial(TopkArgs a) {
   select_k(v, id, a.kmax, a.cand_v + c0, a.cand_i + c0);
 }
 
+// Number of pairs among (cv, ci)[0..n) that beat (v, id).  The arrays are
+// 16-byte aligned and padded to a multiple of 4 with (-inf, INT32_MAX), which
+// beats nothing; reads are 4 pairs wide and unrolled so LDS latency overlaps.
+__device__ __forceinline__ int count_better(const float *cv, const int *ci, int n, float v, int id) {
+  const float4 *cv4 = reinterpret_cast<const float4 *>(cv);
+  const int4 *ci4 = reinterpret_cast<const int4 *>(ci);
+  int rank = 0;
+  const int n4 = (n + 3) >> 2;
+#pragma unroll 8
+  for (int j = 0; j < n4; ++j) {
+    const float4 a4 = cv4[j];
+    const int4 b4 = ci4[j];
+    rank += (better(a4.x, b4.x, v, id) ? 1 : 0) + (better(a4.y, b4.y, v, id) ? 1 : 0) +
+            (better(a4.z, b4.z, v, id) ? 1 : 0) + (better(a4.w, b4.w, v, id) ? 1 : 0);
+  }
+  return rank;
+}
+
+// Level 2 by rank counting: a candidate's output slot is the number of
+// candidates that beat it (ids are unique across slices), so the k winners
+// are placed in one pass without sequential selection rounds.
 __global__ __launch_bounds__(kSel) void topk_merge(TopkArgs a) {
   const int row = blockIdx.x;                 // b * n_heads + head
   const int b = row / a.n_heads, head = row % a.n_heads;
   const int k = a.k[head];
   const int ncand = a.nsplit * a.kmax;
-  const float *cv = a.cand_v + (int64_t)row * ncand;
-  const int *ci = a.cand_i + (int64_t)row * ncand;
-  float v[kPer];
-  int id[kPer];
-#pragma unroll
-  for (int p = 0; p < kPer; ++p) {
-    const int i = p * kSel + threadIdx.x;
-    const bool in = i < ncand;
-    v[p] = in ? cv[i] : -INFINITY;
-    id[p] = in ? ci[i] : INT32_MAX;
-  }
+  __shared__ __attribute__((aligned(16))) float cv[kTopkMaxCand + 4];
+  __shared__ __attribute__((aligned(16))) int ci[kTopkMaxCand + 4];
   __shared__ float selv[kMaxTopk];
   __shared__ int sel[kMaxTopk];
-  select_k(v, id, k, selv, sel);
-  __syncthreads();
   const int tid = threadIdx.x;
+  for (int i = tid; i < ncand; i += kSel) {
+    cv[i] = a.cand_v[(int64_t)row * ncand + i];
+    ci[i] = a.cand_i[(int64_t)row * ncand + i];
+  }
+  if (tid < 4) {                              // pad to a multiple of 4 with pairs that beat nothing
+    cv[ncand + tid] = -INFINITY;
+    ci[ncand + tid] = INT32_MAX;
+  }
+  __syncthreads();
+  for (int i = tid; i < ncand; i += kSel) {
+    const float v = cv[i];
+    const int id = ci[i];
+    if (id == INT32_MAX) continue;            // empty slot of a short slice
+    const int rank = count_better(cv, ci, ncand, v, id);
+    if (rank < k) {
+      sel[rank] = id;
+      selv[rank] = v;
+    }
+  }
+  __syncthreads();
   int32_t *ids = a.ids + (int64_t)row * a.kmax;
   for (int j = tid; j < a.kmax; j += kSel) {
     ids[j] = j < k ? sel[j] : -1;

@@ -119,8 +119,13 @@ def run_parity(torch, wl, max_attn_rows=None, typical=True, label=""):
     tau = tau_for(cfg, z64)
     assert np.all(np.abs(z_gpu - z64) <= tau), float((np.abs(z_gpu - z64) / tau).max())
     exact = check_topk(cfg, z64, ids_gpu)
+    # the same decision taken in the kernel's precision: the oracle's top-k over
+    # the GPU's own fp32 logits must pick exactly the GPU's ids
+    ids32, _ = oracle.heads_topk(z_gpu.astype(np.float64), cfg.topk, cfg.kmax)
+    assert np.array_equal(ids_gpu, ids32)
     ids64, _ = oracle.heads_topk(z64, cfg.topk, cfg.kmax)
     tok64 = oracle.tree_tokens(wl.node_off, wl.depth, wl.rank, wl.root_tok, ids64)
+    assert np.array_equal(tok_gpu, oracle.tree_tokens(wl.node_off, wl.depth, wl.rank, wl.root_tok, ids_gpu))
     same = np.all(ids_gpu == ids64, axis=2)
     for b in range(cfg.B):
         o, n1 = int(wl.node_off[b]), int(wl.node_off[b + 1])
