@@ -128,53 +128,87 @@ int hip_status(hipError_t e, const char *what) {
 }
 
 // ---- tree attention planning ------------------------------------------------------
-constexpr int kTargetItems = 512;   // >= 2 work items per compute unit (256 CUs)
-constexpr int kMinChunk = 512;      // keys per chunk when splitting the KV range
+constexpr int kMinChunk = 256;      // fewest keys per chunk when splitting the KV range
 
 // Tuning overrides (they change the work split, never the result beyond
-// rounding): SPECMEMO_ATTN_ITEMS = target work items, SPECMEMO_ATTN_CHUNK = fixed
-// chunk length in keys (a multiple of 64; 0 disables splitting).
+// rounding): SPECMEMO_ATTN_CHUNK = fixed
+// chunk length in keys (a multiple of 64; 0 disables splitting), SPECMEMO_ATTN_ROWS =
+// query rows per work item (64, 128 or 256), SPECMEMO_ATTN_XCD = 0 to keep block order.
 int env_int(const char *name, int dflt) {
   const char *v = getenv(name);
   return v && *v ? atoi(v) : dflt;
 }
 
 struct AttnPlan {
-  int rb = 128;        // query rows per work item: 64 (MHA-sized trees) or 128
+  int rb = 128;        // query rows per work item: 64, 128 or 256
+  bool xcd_order = true;
   std::vector<std::vector<AttnSeq>> groups;   // sequences per launch, in launch order
   std::vector<int> items, citems;
   size_t ws_bytes = 0;
 };
 
+// Compute units of the current device (256 on MI355X; also the fallback when no
+// device is visible, so that workspace sizes can be planned on a host).
+int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  return n;
+}
+
+// Work items of one launch for a chunk length c (INT32_MAX: no split).
+int64_t attn_items(const std::vector<AttnSeq> &grp, int n_kv, int c) {
+  int64_t items = 0;
+  for (const AttnSeq &s : grp) items += (int64_t)n_kv * s.nrb * (s.L <= c ? 1 : (s.L + c - 1) / c);
+  return items;
+}
+
+// Chunk length of one launch.  If every work item fits in one round of
+// resident blocks, the smallest chunk that still fits (largest item smallest);
+// otherwise long sequences are split down to the average work of one block slot.
+int attn_chunk(const std::vector<AttnSeq> &grp, int n_kv, int slots) {
+  static const int fixed_chunk = env_int("SPECMEMO_ATTN_CHUNK", -1);
+  if (fixed_chunk == 0) return INT32_MAX;
+  if (fixed_chunk > 0) return std::max(kAttnKeyTile, fixed_chunk / kAttnKeyTile * kAttnKeyTile);
+  int maxL = 0;
+  int64_t work = 0;
+  for (const AttnSeq &s : grp) {
+    maxL = std::max(maxL, s.L);
+    work += (int64_t)n_kv * s.nrb * (s.L + s.N);
+  }
+  if (attn_items(grp, n_kv, INT32_MAX) <= slots) {
+    int lo = kMinChunk / kAttnKeyTile, hi = (maxL + kAttnKeyTile - 1) / kAttnKeyTile;   // in tiles
+    if (lo >= hi) return INT32_MAX;
+    while (lo < hi) {                  // smallest chunk with items <= slots
+      const int mid = (lo + hi) / 2;
+      if (attn_items(grp, n_kv, mid * kAttnKeyTile) <= slots) hi = mid; else lo = mid + 1;
+    }
+    return lo * kAttnKeyTile >= maxL ? INT32_MAX : lo * kAttnKeyTile;
+  }
+  const int64_t c = (work + slots - 1) / slots;
+  const int64_t ct = std::max<int64_t>(kMinChunk, (c + kAttnKeyTile - 1) / kAttnKeyTile * kAttnKeyTile);
+  return ct >= maxL ? INT32_MAX : (int)ct;
+}
+
 void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *kv, int n_q, AttnPlan *p) {
   const int g = n_q / kv->n_kv;
-  p->rb = ti.max_nodes * g <= 64 ? 64 : 128;
+  const int max_rows = ti.max_nodes * g;
+  static const int rows_env = env_int("SPECMEMO_ATTN_ROWS", 0);
+  static const int xcd_env = env_int("SPECMEMO_ATTN_XCD", 1);
+  p->rb = max_rows <= 64 ? 64 : max_rows <= 128 ? 128 : 256;
+  if (rows_env == 64 || rows_env == 128 || rows_env == 256) p->rb = rows_env;
+  p->xcd_order = xcd_env != 0;
   const int RB = p->rb;
+  const int slots = device_cus() * (RB == 256 ? 1 : 2);   // resident blocks of the launch
   std::vector<int> order(ti.B);
   std::iota(order.begin(), order.end(), 0);
   std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return kv->seq_len_h[x] > kv->seq_len_h[y]; });
-  // Chunk length: split the committed range only when the unsplit grid is too small.
-  int64_t base_items = 0, weighted = 0;
-  for (int b = 0; b < ti.B; ++b) {
-    const int N = t->node_off_h[b + 1] - t->node_off_h[b];
-    const int nrb = (N * g + RB - 1) / RB;
-    base_items += (int64_t)kv->n_kv * nrb;
-    weighted += (int64_t)kv->n_kv * nrb * (kv->seq_len_h[b] + N);
-  }
-  static const int target = std::max(1, env_int("SPECMEMO_ATTN_ITEMS", kTargetItems));
-  static const int fixed_chunk = env_int("SPECMEMO_ATTN_CHUNK", -1);
-  int ch_len = INT32_MAX;
-  if (fixed_chunk > 0) {
-    ch_len = std::max(kAttnKeyTile, fixed_chunk / kAttnKeyTile * kAttnKeyTile);
-  } else if (fixed_chunk < 0 && base_items < target) {
-    int64_t c = (weighted + target - 1) / target;
-    c = std::max<int64_t>(kMinChunk, (c + kAttnKeyTile - 1) / kAttnKeyTile * kAttnKeyTile);
-    ch_len = (int)std::min<int64_t>(c, INT32_MAX / 2);
-  }
   const int64_t pf = attn_partial_floats(RB);
   for (size_t i0 = 0; i0 < order.size(); i0 += kMaxSeqPerLaunch) {
     std::vector<AttnSeq> grp;
-    int item = 0, part = 0, citem = 0;
     for (size_t i = i0; i < std::min(order.size(), i0 + kMaxSeqPerLaunch); ++i) {
       const int b = order[i];
       AttnSeq s{};
@@ -183,23 +217,34 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
       s.node0 = t->node_off_h[b];
       s.N = t->node_off_h[b + 1] - s.node0;
       s.nrb = (s.N * g + RB - 1) / RB;
+      grp.push_back(s);
+    }
+    const int ch_len = attn_chunk(grp, kv->n_kv, slots);
+    int item = 0, part = 0, citem = 0, unit = 0;
+    int per_xcd[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (AttnSeq &s : grp) {
       s.nch = (ch_len == INT32_MAX || s.L <= ch_len) ? 1 : (s.L + ch_len - 1) / ch_len;
       s.ch_len = s.nch == 1 ? s.L + s.N : ch_len;
       s.item0 = item;
-      item += kv->n_kv * s.nrb * s.nch;
+      s.unit0 = unit;
+      const int units = kv->n_kv * s.nch;
+      for (int u = 0; u < units; ++u) per_xcd[(unit + u) & 7] += s.nrb;
+      unit += units;
+      item += units * s.nrb;
       if (s.nch > 1) {
         s.part0 = part;
-        part += kv->n_kv * s.nrb * s.nch;
+        part += units * s.nrb;
         s.citem0 = citem;
         citem += kv->n_kv * s.nrb;
       } else {
         s.part0 = -1;
         s.citem0 = -1;
       }
-      grp.push_back(s);
     }
     p->groups.push_back(grp);
-    p->items.push_back(item);
+    // XCD order: XCD x runs units x, x + 8, ... (all their row blocks); the grid
+    // is padded to 8 x the busiest XCD's blocks, surplus blocks exit at once.
+    p->items.push_back(p->xcd_order ? 8 * *std::max_element(per_xcd, per_xcd + 8) : item);
     p->citems.push_back(citem);
     p->ws_bytes = std::max(p->ws_bytes, (size_t)part * (size_t)pf * sizeof(float));
   }
@@ -359,6 +404,7 @@ int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmem
     for (int i = 0; i < a.nseq; ++i) a.seq[i] = p.groups[gi][i];
     a.items = p.items[gi];
     a.citems = p.citems[gi];
+    a.xcd_order = p.xcd_order ? 1 : 0;
     hipError_t e = launch_tree_attn_bf16(a, p.rb, st);
     if (e != hipSuccess) return hip_status(e, "tree attention launch");
   }

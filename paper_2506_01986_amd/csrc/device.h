@@ -32,9 +32,18 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 // Value of lane l combined with lane l^32 (the two halves of a wave hold the
-// same rows).
-__device__ __forceinline__ float max_with_other_half(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
-__device__ __forceinline__ float sum_with_other_half(float x) { return x + __shfl_xor(x, 32); }
+// same rows).  v_permlane32_swap of x with itself leaves the low half of x in
+// both halves of the first result and the high half in both halves of the
+// second, so every lane combines (x of lane l mod 32, x of lane l mod 32 + 32)
+// in that order.
+__device__ __forceinline__ float max_with_other_half(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_with_other_half(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 // Larger value first; equal values by lower id.
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {

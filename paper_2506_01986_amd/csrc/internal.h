@@ -45,7 +45,7 @@ struct AttnSeq {
   int32_t item0;     // first work item of this sequence in the launch
   int32_t part0;     // first partial slot (multi-chunk sequences), -1 if none
   int32_t citem0;    // first combine item (multi-chunk sequences)
-  int32_t pad;
+  int32_t unit0;     // first (KV head, chunk) unit of this sequence in the launch
 };
 
 struct AttnArgs {
@@ -58,7 +58,8 @@ struct AttnArgs {
   int32_t n_q, n_kv, group, head_dim;
   float scale_log2;        // scale * log2(e)
   float scale;
-  int32_t nseq, items, citems;
+  int32_t nseq, items, citems;   // items: blocks of the launch (XCD order: padded)
+  int32_t xcd_order;        // nonzero: consecutive work items share an XCD
   AttnSeq seq[kMaxSeqPerLaunch];
 };
 

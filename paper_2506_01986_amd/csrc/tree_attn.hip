@@ -39,6 +39,7 @@ struct Item {
   int s, kvh, rb, ch;
 };
 
+// Work items in launch order: sequence, then KV head, chunk, row block.
 __device__ __forceinline__ Item decode_item(const AttnArgs &a, int idx) {
   int s = 0;
   while (s + 1 < a.nseq && a.seq[s + 1].item0 <= idx) ++s;
@@ -53,6 +54,33 @@ __device__ __forceinline__ Item decode_item(const AttnArgs &a, int idx) {
   return it;
 }
 
+// XCD order.  Blocks reach the eight XCDs round-robin by block id, so block
+// 8 k + x is the k-th block of XCD x.  A unit is one (sequence, KV head,
+// chunk) with all its row blocks, which read the same K/V; unit u (launch
+// order, longest sequences first) runs on XCD u mod 8, so those row blocks
+// share one L2 and every XCD gets long and short units alike.  Returns false
+// for the padding blocks past the busiest XCD's work.
+__device__ __forceinline__ bool decode_item_xcd(const AttnArgs &a, int bid, Item &it) {
+  const int x = bid & 7;
+  int k = bid >> 3;
+  for (int s = 0; s < a.nseq; ++s) {
+    const AttnSeq &S = a.seq[s];
+    const int u0 = S.unit0, nu = a.n_kv * S.nch;
+    const int first = u0 + ((x - (u0 & 7)) & 7);            // first unit >= u0 on XCD x
+    const int cnt = first < u0 + nu ? (u0 + nu - 1 - first) / 8 + 1 : 0;
+    if (k < cnt * S.nrb) {
+      const int u = first + 8 * (k / S.nrb) - u0;
+      it.s = s;
+      it.rb = k % S.nrb;
+      it.ch = u % S.nch;
+      it.kvh = u / S.nch;
+      return true;
+    }
+    k -= cnt * S.nrb;
+  }
+  return false;
+}
+
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short s16x4_t __attribute__((__vector_size__(8)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
@@ -64,19 +92,27 @@ typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 __device__ __forceinline__ int kswz(int r, int c) { return c ^ (r & 15); }
 __device__ __forceinline__ int vswz(int r, int c) { return c ^ ((r & 3) << 2); }
 
-// WAVES waves per block, each owning NRB2 x 32 query rows; STAGES-deep ring of
-// K/V tiles filled by direct loads.  With NRB2 = 2 every K/V fragment read from
-// LDS feeds two matrix-core products.
+// WAVES waves per block, 32 query rows per wave (one per lane pair l, l^32);
+// K and V each have a SLOTS-deep ring of 64-key tiles filled by direct loads;
+// iteration j computes S, the weights and O for tile j, its two 32-key
+// products S^T = K Q^T being independent accumulation chains.
 // MINB: blocks that must fit on one compute unit (bounds the registers).
-template <int WAVES, int NRB2, int STAGES, int MINB>
+template <int WAVES, int SLOTS, int MINB>
 __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
-  constexpr int RB = 32 * NRB2 * WAVES;
+  static_assert(SLOTS == 2 || SLOTS == 3, "ring depth");
+  constexpr int RB = 32 * WAVES;
   constexpr int TILE = TK * D * 2;            // bytes of one K or V tile (16 KB)
   constexpr int IPW = TILE / 1024 / WAVES;    // 1 KB direct loads per wave per tile and operand
-  __shared__ __attribute__((aligned(1024))) uint8_t ring[STAGES][2][TILE];
+  __shared__ __attribute__((aligned(1024))) uint8_t kring[SLOTS][TILE];
+  __shared__ __attribute__((aligned(1024))) uint8_t vring[SLOTS][TILE];
   __shared__ uint32_t anc[kMaxNodes][4];
 
-  const Item it = decode_item(a, blockIdx.x);
+  Item it;
+  if (a.xcd_order) {
+    if (!decode_item_xcd(a, blockIdx.x, it)) return;   // padding block: no work, no barrier reached
+  } else {
+    it = decode_item(a, blockIdx.x);
+  }
   const AttnSeq &S = a.seq[it.s];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5;              // which half of the wave
@@ -100,21 +136,16 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
     anc[n][3] = m3;
   }
 
-  // This lane's query rows (one per 32-row block of the wave).
-  int my_row[NRB2], node[NRB2], hq[NRB2];
-  bool row_ok[NRB2];
-  bf16x8 qf[NRB2][D / 16];
+  // This lane's query row and its Q fragments (B operand of S^T = K Q^T).
+  const int my_row = it.rb * RB + wave * 32 + (lane & 31);
+  const bool row_ok = my_row < rows;
+  const int node = row_ok ? my_row / g : 0;
+  const int hq = it.kvh * g + (row_ok ? my_row % g : 0);
+  bf16x8 qf[D / 16];
+  {
+    const uint16_t *qbase = static_cast<const uint16_t *>(a.q) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D + 8 * h;
 #pragma unroll
-  for (int b2 = 0; b2 < NRB2; ++b2) {
-    my_row[b2] = it.rb * RB + (wave * NRB2 + b2) * 32 + (lane & 31);
-    row_ok[b2] = my_row[b2] < rows;
-    node[b2] = row_ok[b2] ? my_row[b2] / g : 0;
-    hq[b2] = it.kvh * g + (row_ok[b2] ? my_row[b2] % g : 0);
-    const uint16_t *qbase = static_cast<const uint16_t *>(a.q) +
-                            ((int64_t)(S.node0 + node[b2]) * a.n_q + hq[b2]) * D + 8 * h;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks)
-      qf[b2][ks] = __builtin_bit_cast(bf16x8, ld16_or_zero(row_ok[b2], qbase + 16 * ks));
+    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, ld16_or_zero(row_ok, qbase + 16 * ks));
   }
 
   // Key range of this chunk: chunk boundaries lie inside the committed region and
@@ -126,11 +157,9 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   const uint16_t *Kg = static_cast<const uint16_t *>(a.k) + ((int64_t)it.kvh * a.cap_total + S.base) * D;
   const uint16_t *Vg = static_cast<const uint16_t *>(a.v) + ((int64_t)it.kvh * a.cap_total + S.base) * D;
 
-  // Direct loads of tile j into its ring slot: lane l of load i writes LDS bytes
+  // Direct loads of a tile into its ring slot: lane l of load i writes LDS bytes
   // [1024 i + 16 l, +16), i.e. tile row r = 4 i + l / 16 at physical chunk l % 16.
   // Rows past the chunk end repeat its last row (finite values, masked out).
-  // Per-lane byte offsets of this wave's loads inside a tile (row r, swizzled
-  // chunk), fixed for the whole chunk; full tiles add a wave-uniform tile base.
   int koff[IPW], voff[IPW], lrow[IPW];
 #pragma unroll
   for (int u = 0; u < IPW; ++u) {
@@ -142,197 +171,201 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   }
   const uint8_t *Kb = reinterpret_cast<const uint8_t *>(Kg);
   const uint8_t *Vb = reinterpret_cast<const uint8_t *>(Vg);
-  auto issue = [&](int j) {
+  auto issue = [&](const uint8_t *src, const int (&off)[IPW], uint8_t *dst, int j) {
     const int kt = k0 + j * TK;
-    uint8_t *ks = ring[j % STAGES][0];
-    uint8_t *vs = ring[j % STAGES][1];
     if (kt + TK <= k1) {
-      const uint8_t *kb = Kb + (int64_t)kt * (D * 2), *vb = Vb + (int64_t)kt * (D * 2);
+      const uint8_t *sb = src + (int64_t)kt * (D * 2);
 #pragma unroll
-      for (int u = 0; u < IPW; ++u) {
-        const int i = wave * IPW + u;
-        __builtin_amdgcn_global_load_lds((const void *)(kb + koff[u]), (lds_void_t *)(ks + 1024 * i), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void *)(vb + voff[u]), (lds_void_t *)(vs + 1024 * i), 16, 0, 0);
-      }
+      for (int u = 0; u < IPW; ++u)
+        __builtin_amdgcn_global_load_lds((const void *)(sb + off[u]), (lds_void_t *)(dst + 1024 * (wave * IPW + u)), 16, 0, 0);
     } else {                             // last tile: rows past the chunk end repeat its last row
 #pragma unroll
       for (int u = 0; u < IPW; ++u) {
-        const int i = wave * IPW + u;
         const int64_t t = min(kt + lrow[u], k1 - 1);
-        const int cofs = koff[u] - lrow[u] * (D * 2), vcofs = voff[u] - lrow[u] * (D * 2);
-        __builtin_amdgcn_global_load_lds((const void *)(Kb + t * (D * 2) + cofs), (lds_void_t *)(ks + 1024 * i), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void *)(Vb + t * (D * 2) + vcofs), (lds_void_t *)(vs + 1024 * i), 16, 0, 0);
+        const int cofs = off[u] - lrow[u] * (D * 2);
+        __builtin_amdgcn_global_load_lds((const void *)(src + t * (D * 2) + cofs),
+                                         (lds_void_t *)(dst + 1024 * (wave * IPW + u)), 16, 0, 0);
+      }
+    }
+  };
+  auto issue_k = [&](int j) { issue(Kb, koff, kring[j % SLOTS], j); };
+  auto issue_v = [&](int j) { issue(Vb, voff, vring[j % SLOTS], j); };
+
+  // K operand: row (lane & 31) of a 32-key sub-block, 16-byte chunk 2 ks + h.
+  int kro[D / 16];
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) kro[ks] = (lane & 31) * (D * 2) + 16 * ((2 * ks + h) ^ (lane & 15));
+  // Transposing-load source role of this lane within its 16-lane group: source
+  // lane 4 tj + tq supplies key row tj, head-dim columns 4 tq .. 4 tq + 3 of the
+  // group's 16 columns; destination lane o then holds 4 keys of column o.  With
+  // the V swizzle the byte offset of d-block i is a per-lane constant.
+  const int tj = (lane & 15) >> 2, tq = lane & 3;
+  const int te = 2 * ((lane >> 4) & 1) + (tq >> 1);
+  int vro[D / 32];
+#pragma unroll
+  for (int i = 0; i < D / 32; ++i) vro[i] = (4 * h + tj) * (D * 2) + 64 * (i ^ tj) + 16 * te + 8 * (tq & 1);
+
+  auto qk = [&](int j, f32x16 (&Sc)[2]) {
+    const uint8_t *ks = kring[j % SLOTS];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r2 = 0; r2 < 16; ++r2) Sc[sb][r2] = 0.f;
+#pragma unroll
+    for (int k8 = 0; k8 < D / 16; ++k8)
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb) {
+        const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(ks + sb * 32 * (D * 2) + kro[k8]));
+        Sc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k8], Sc[sb], 0, 0, 0);
+      }
+  };
+
+  float m = -INFINITY, lsum = 0.f;
+  f32x16 O[D / 32];
+#pragma unroll
+  for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) O[i][r] = 0.f;
+  uint32_t an0 = 0, an1 = 0, an2 = 0, an3 = 0;   // this row's ancestor words (after the first barrier)
+  const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
+
+  // Scores of tile j -> bf16 weights (online softmax, lazy rescale) -> O += V^T P^T.
+  // Accumulator entry r of sub-block sb is key kt + 32 sb + 8 (r / 4) + 4 h + r % 4.
+  auto softmax_pv = [&](int j, f32x16 (&Sc)[2]) {
+    const int kt = k0 + j * TK;
+    if (kt + TK > min(k1, L)) {          // tile reaches the tree rows or the chunk end
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r2 = 0; r2 < 16; ++r2) {
+          const int t = kt + 32 * sb + 8 * (r2 >> 2) + 4 * h + (r2 & 3);
+          const uint32_t rel = (uint32_t)(t - L);
+          const uint32_t w = rel < 32 ? an0 : rel < 64 ? an1 : rel < 96 ? an2 : an3;
+          const bool vis = t < k1 && (t < L || ((w >> (rel & 31)) & 1u));
+          Sc[sb][r2] = vis ? Sc[sb][r2] : -INFINITY;
+        }
+    }
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r2 = 0; r2 < 16; ++r2) tmax = fmaxf(tmax, Sc[sb][r2]);
+    tmax = max_with_other_half(tmax) * a.scale_log2;
+    // Lazy rescaling: the reference max m moves only when a score exceeds it by
+    // more than kRescaleSlack (log2 units), so weights stay <= 2^kRescaleSlack;
+    // the branch is taken by the whole wave, rarely after the first tile.
+    const bool need = tmax > m + kRescaleSlack;
+    if (__builtin_amdgcn_ballot_w64(need)) {
+      const float m_new = need ? tmax : m;
+      const float alpha = need ? (m == -INFINITY ? 0.f : fast_exp2(m - m_new)) : 1.f;
+      m = m_new;
+      lsum *= alpha;
+#pragma unroll
+      for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+        for (int r2 = 0; r2 < 16; ++r2) O[i][r2] *= alpha;
+    }
+    const float m_use = m == -INFINITY ? 0.f : m;
+    // B operand of 16-key group mh = 2 sb + half: slot 8 h + s <-> key
+    // 32 sb + 16 half + 8 (s / 4) + 4 h + s % 4 (the V^T reads use the same order).
+    uint32_t pk[4][4];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int half = 0; half < 2; ++half)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float p0 = fast_exp2(fmaf(Sc[sb][8 * half + 2 * q], a.scale_log2, -m_use));
+          const float p1 = fast_exp2(fmaf(Sc[sb][8 * half + 2 * q + 1], a.scale_log2, -m_use));
+          pk[2 * sb + half][q] = pack_bf16x2(p0, p1);
+        }
+    // Row sum of the bf16 weights that enter O (two-term dot products with ones).
+#pragma unroll
+    for (int mh = 0; mh < 4; ++mh)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk[mh][q]), ones, lsum, false);
+    const uint8_t *vs = vring[j % SLOTS];
+#pragma unroll
+    for (int mh = 0; mh < 4; ++mh) {
+      const bf16x8 pf = __builtin_bit_cast(bf16x8, uint4{pk[mh][0], pk[mh][1], pk[mh][2], pk[mh][3]});
+#pragma unroll
+      for (int i = 0; i < D / 32; ++i) {
+        const uint8_t *p = vs + 16 * mh * (D * 2) + vro[i];
+        const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)p);
+        const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)(p + 8 * (D * 2)));
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        O[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, O[i], 0, 0, 0);
       }
     }
   };
 
-  float m[NRB2], lsum[NRB2];
-  f32x16 O[NRB2][D / 32];
+  auto wait_loads = [&](int later) {   // wait until at most `later` x IPW of this wave's loads are pending
+    if (later >= 2)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * IPW) : "memory");
+    else if (later == 1)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(IPW) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  };
+  auto read_anc = [&]() {
+    an0 = anc[node][0];
+    an1 = anc[node][1];
+    an2 = anc[node][2];
+    an3 = anc[node][3];
+  };
+
+  // Prologue: tiles 0 .. SLOTS-2 (K then V).  Iteration j needs tile j; after
+  // its barrier every wave is done with tile j-1, whose slots take tile
+  // j+SLOTS-1.
 #pragma unroll
-  for (int b2 = 0; b2 < NRB2; ++b2) {
-    m[b2] = -INFINITY;
-    lsum[b2] = 0.f;
+  for (int t = 0; t < SLOTS - 1; ++t)
+    if (t < ntiles) {
+      issue_k(t);
+      issue_v(t);
+    }
+  for (int j = 0; j < ntiles; ++j) {
+    // loads issued after tile j: tile j+1 (3 slots), two operands
+    wait_loads(SLOTS == 3 && j + 1 < ntiles ? 2 : 0);
+    __syncthreads();
+    if (j == 0) read_anc();
+    if (j + SLOTS - 1 < ntiles) {
+      issue_k(j + SLOTS - 1);
+      issue_v(j + SLOTS - 1);
+    }
+    f32x16 Sc[2];
+    qk(j, Sc);
+    softmax_pv(j, Sc);
+  }
+
+  const float ltot = sum_with_other_half(lsum);
+  if (!row_ok) return;
+  // O^T entry r of d-block i is d = 32 i + 8 (r / 4) + 4 h + r % 4 of this lane's row.
+  if (S.nch == 1) {
+    const float inv = 1.f / ltot;
+    uint16_t *op = static_cast<uint16_t *>(a.out) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D;
 #pragma unroll
     for (int i = 0; i < D / 32; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) O[b2][i][r] = 0.f;
-  }
-
-  // Transposing-load source role of this lane within its 16-lane group:
-  // source lane 4j + q supplies keys row j, head-dim columns 4q..4q+3 of the
-  // group's 16 columns; destination lane o then holds 4 keys of column o.
-  const int tr_j = (lane & 15) >> 2, tr_q = lane & 3;
-  const int tr_d = 16 * ((lane >> 4) & 1) + 4 * tr_q;   // column within a 32-wide d block
-
-  // One tile, one 32-key sub-block at a time: S^T (K rows as the A operand),
-  // online softmax, then O^T += V^T P^T with V^T from the transposing loads.
-  auto compute = [&](int j) {
-    const int kt0 = k0 + j * TK;
-    const uint8_t *ks = ring[j % STAGES][0];
-    const uint8_t *vs = ring[j % STAGES][1];
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      const int kt = kt0 + 32 * sb;
-      const int r = sb * 32 + (lane & 31);
-      bf16x8 kf[D / 16];
-#pragma unroll
-      for (int ks8 = 0; ks8 < D / 16; ++ks8)
-        kf[ks8] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const uint4 *>(ks + r * (D * 2) + 16 * kswz(r, 2 * ks8 + h)));
-      f32x16 sc[NRB2];
-#pragma unroll
-      for (int b2 = 0; b2 < NRB2; ++b2) {
-#pragma unroll
-        for (int r2 = 0; r2 < 16; ++r2) sc[b2][r2] = 0.f;
-#pragma unroll
-        for (int ks8 = 0; ks8 < D / 16; ++ks8)
-          sc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks8], qf[b2][ks8], sc[b2], 0, 0, 0);
+      for (int q4 = 0; q4 < 4; ++q4) {
+        uint2 v = {pack_bf16x2(O[i][4 * q4] * inv, O[i][4 * q4 + 1] * inv),
+                   pack_bf16x2(O[i][4 * q4 + 2] * inv, O[i][4 * q4 + 3] * inv)};
+        *reinterpret_cast<uint2 *>(op + 32 * i + 8 * q4 + 4 * h) = v;
       }
-      // Accumulator entry r of the sub-block is key kt + 8(r/4) + 4h + r%4.
-      // Scores stay unscaled; the running max m is kept in scaled log2 units.
-      const bool full = kt + 32 <= min(k1, L);
-      uint32_t pk[NRB2][2][4];
+  } else {
+    const int local_row = my_row - it.rb * RB;
+    float *slot = a.part + ((int64_t)S.part0 + ((int64_t)it.kvh * S.nrb + it.rb) * S.nch + it.ch) *
+                               (int64_t)attn_partial_floats(RB);
+    uint16_t *po = reinterpret_cast<uint16_t *>(slot) + (int64_t)local_row * D;
 #pragma unroll
-      for (int b2 = 0; b2 < NRB2; ++b2) {
-        float tmax = -INFINITY;
-        if (full) {
+    for (int i = 0; i < D / 32; ++i)
 #pragma unroll
-          for (int r2 = 0; r2 < 16; ++r2) tmax = fmaxf(tmax, sc[b2][r2]);
-        } else {
-          const uint32_t *my_anc = anc[node[b2]];
-#pragma unroll
-          for (int r2 = 0; r2 < 16; ++r2) {
-            float sv = sc[b2][r2];
-            const int t = kt + 8 * (r2 >> 2) + 4 * h + (r2 & 3);
-            const bool vis = t < k1 && (t < L || ((my_anc[(t - L) >> 5] >> ((t - L) & 31)) & 1u));
-            sv = vis ? sv : -INFINITY;
-            sc[b2][r2] = sv;
-            tmax = fmaxf(tmax, sv);
-          }
-        }
-        tmax = max_with_other_half(tmax) * a.scale_log2;
-        // Lazy rescaling: the reference max m moves only when a score exceeds it
-        // by more than kRescaleSlack (log2 units), so p <= 2^kRescaleSlack and
-        // O is rescaled in the rare tiles where that happens.
-        if (tmax > m[b2] + kRescaleSlack) {
-          const float m_new = tmax;
-          const float alpha = m[b2] == -INFINITY ? 0.f : fast_exp2(m[b2] - m_new);
-          m[b2] = m_new;
-          lsum[b2] *= alpha;
-#pragma unroll
-          for (int i = 0; i < D / 32; ++i)
-#pragma unroll
-            for (int r2 = 0; r2 < 16; ++r2) O[b2][i][r2] *= alpha;
-        }
-        const float m_use = m[b2] == -INFINITY ? 0.f : m[b2];
-        float psum = 0.f;
-#pragma unroll
-        for (int mh = 0; mh < 2; ++mh)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float p0 = fast_exp2(fmaf(sc[b2][8 * mh + 2 * q], a.scale_log2, -m_use));
-            const float p1 = fast_exp2(fmaf(sc[b2][8 * mh + 2 * q + 1], a.scale_log2, -m_use));
-            psum += p0 + p1;
-            pk[b2][mh][q] = pack_bf16x2(p0, p1);
-          }
-        lsum[b2] += psum;
-      }
-      // B operand slot 8h + s <-> key 16mh + 8(s/4) + 4h + s%4 of the sub-block;
-      // the transposing loads return V^T in the same key order.
-#pragma unroll
-      for (int mh = 0; mh < 2; ++mh) {
-        const int r0 = 32 * sb + 16 * mh + 4 * h + tr_j;
-        bf16x8 vf[D / 32];
-#pragma unroll
-        for (int i = 0; i < D / 32; ++i) {
-          const int d = 32 * i + tr_d;
-          const int c = d >> 3, cb = (d & 7) * 2;
-          const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_s16x4_t *)(vs + r0 * (D * 2) + 16 * vswz(r0, c) + cb));
-          const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_s16x4_t *)(vs + (r0 + 8) * (D * 2) + 16 * vswz(r0 + 8, c) + cb));
-          vf[i] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        }
-#pragma unroll
-        for (int b2 = 0; b2 < NRB2; ++b2) {
-          const bf16x8 pf = __builtin_bit_cast(bf16x8, uint4{pk[b2][mh][0], pk[b2][mh][1], pk[b2][mh][2], pk[b2][mh][3]});
-#pragma unroll
-          for (int i = 0; i < D / 32; ++i)
-            O[b2][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pf, O[b2][i], 0, 0, 0);
-        }
-      }
-    }
-  };
-
-  // STAGES-deep pipeline: tiles j+1 .. j+STAGES-1 are in flight while tile j is
-  // computed.  Every wave issues 2 * IPW direct loads per tile, so "tile j
-  // landed" is "at most 2 * IPW * (tiles issued after j) loads outstanding".
-#pragma unroll
-  for (int j = 0; j < STAGES - 1; ++j)
-    if (j < ntiles) issue(j);
-  for (int j = 0; j < ntiles; ++j) {
-    const int after = min(ntiles - 1 - j, STAGES - 2);   // tiles issued after j so far
-    if (STAGES == 3 && after == 1)
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * IPW) : "memory");
-    else
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();                    // tile j visible to all waves; all waves are done with tile j-1
-    if (j + STAGES - 1 < ntiles) issue(j + STAGES - 1);
-    compute(j);
-  }
-
-#pragma unroll
-  for (int b2 = 0; b2 < NRB2; ++b2) {
-    const float ltot = sum_with_other_half(lsum[b2]);
-    if (!row_ok[b2]) continue;
-    // O^T entry r of d-block i is d = 32i + 8(r/4) + 4h + r%4 of this lane's row.
-    if (S.nch == 1) {
-      const float inv = 1.f / ltot;
-      uint16_t *op = static_cast<uint16_t *>(a.out) + ((int64_t)(S.node0 + node[b2]) * a.n_q + hq[b2]) * D;
-#pragma unroll
-      for (int i = 0; i < D / 32; ++i)
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          uint2 v = {pack_bf16x2(O[b2][i][4 * q4] * inv, O[b2][i][4 * q4 + 1] * inv),
-                     pack_bf16x2(O[b2][i][4 * q4 + 2] * inv, O[b2][i][4 * q4 + 3] * inv)};
-          *reinterpret_cast<uint2 *>(op + 32 * i + 8 * q4 + 4 * h) = v;
-        }
-    } else {
-      const int local_row = my_row[b2] - it.rb * RB;
-      float *slot = a.part + ((int64_t)S.part0 + ((int64_t)it.kvh * S.nrb + it.rb) * S.nch + it.ch) *
-                                 (int64_t)attn_partial_floats(RB);
-      uint16_t *po = reinterpret_cast<uint16_t *>(slot) + (int64_t)local_row * D;
-#pragma unroll
-      for (int i = 0; i < D / 32; ++i)
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4)
-          *reinterpret_cast<uint2 *>(po + 32 * i + 8 * q4 + 4 * h) =
-              uint2{pack_bf16x2(O[b2][i][4 * q4], O[b2][i][4 * q4 + 1]),
-                    pack_bf16x2(O[b2][i][4 * q4 + 2], O[b2][i][4 * q4 + 3])};
-      if (h == 0) {
-        slot[(int64_t)RB * D / 2 + local_row] = m[b2];
-        slot[(int64_t)RB * D / 2 + RB + local_row] = ltot;
-      }
+      for (int q4 = 0; q4 < 4; ++q4)
+        *reinterpret_cast<uint2 *>(po + 32 * i + 8 * q4 + 4 * h) =
+            uint2{pack_bf16x2(O[i][4 * q4], O[i][4 * q4 + 1]), pack_bf16x2(O[i][4 * q4 + 2], O[i][4 * q4 + 3])};
+    if (h == 0) {
+      slot[(int64_t)RB * D / 2 + local_row] = m;
+      slot[(int64_t)RB * D / 2 + RB + local_row] = ltot;
     }
   }
 }
@@ -417,11 +450,14 @@ __global__ __launch_bounds__(256) void tree_attn_f32(AttnArgs a, int node_begin,
 
 hipError_t launch_tree_attn_bf16(const AttnArgs &a, int rows_per_block, hipStream_t st) {
   if (rows_per_block == 64) {
-    hipLaunchKernelGGL((tree_attn_bf16<2, 1, 2, 2>), dim3(a.items), dim3(128), 0, st, a);
+    hipLaunchKernelGGL((tree_attn_bf16<2, 2, 2>), dim3(a.items), dim3(128), 0, st, a);
     if (a.citems) hipLaunchKernelGGL(tree_attn_combine<64>, dim3(a.citems * (64 / kCombineRows)), dim3(256), 0, st, a);
-  } else {
-    hipLaunchKernelGGL((tree_attn_bf16<4, 1, 2, 2>), dim3(a.items), dim3(256), 0, st, a);
+  } else if (rows_per_block == 128) {
+    hipLaunchKernelGGL((tree_attn_bf16<4, 2, 2>), dim3(a.items), dim3(256), 0, st, a);
     if (a.citems) hipLaunchKernelGGL(tree_attn_combine<128>, dim3(a.citems * (128 / kCombineRows)), dim3(256), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((tree_attn_bf16<8, 3, 1>), dim3(a.items), dim3(512), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<256>, dim3(a.citems * (256 / kCombineRows)), dim3(256), 0, st, a);
   }
   return hipGetLastError();
 }
