@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SPECMEMO_ABI_VERSION 1
+#define SPECMEMO_ABI_VERSION 2
 #define SPECMEMO_MAX_TREE_NODES 128 /* nodes per sequence's tree */
 #define SPECMEMO_MAX_DEPTH 15       /* tree depth (= Medusa heads) */
 #define SPECMEMO_MAX_TOPK 32        /* top-k per head */
@@ -74,6 +74,7 @@ typedef enum {
 typedef enum { SPECMEMO_FP32 = 0, SPECMEMO_BF16 = 1 } specmemo_dtype;
 
 typedef enum { SPECMEMO_ACCEPT_GREEDY = 0, SPECMEMO_ACCEPT_TYPICAL = 1 } specmemo_accept_mode;
+typedef enum { SPECMEMO_HEADS_ROWMAJOR = 0, SPECMEMO_HEADS_PACKED = 1 } specmemo_head_layout;
 
 /* Ragged batch of candidate trees, CSR over nodes.  Device arrays are read by
  * kernels; the host mirrors (same contents) are read for validation and launch
@@ -113,8 +114,11 @@ typedef struct {
  *   node_tok[node_off[b]] = root_tok[b];
  *   node_tok[node_off[b] + n] = topk_ids[b][depth[n]-1][rank[n]]  (n > 0)
  *
- * h: device [B][hidden]; head_w: device [n_heads][vocab][hidden] (row-major,
- * the nn.Linear out x in layout, no bias); both in `dt`.  root_tok: device [B]
+ * h: device [B][hidden] in `dt`.  head_w: device, in `dt`, laid out as
+ * head_layout says: SPECMEMO_HEADS_ROWMAJOR is [n_heads][vocab][hidden] (the
+ * nn.Linear out x in layout, no bias); SPECMEMO_HEADS_PACKED (bf16 only) is
+ * the buffer written by specmemo_pack_heads, which the projection streams
+ * contiguously.  root_tok: device [B]
  * (the base model's own next token from the previous step).  logits_out:
  * device fp32 [B][n_heads][vocab], or NULL.  topk_ids: device int32
  * [B][n_heads][kmax] with kmax = max(topk_h); topk_vals: device fp32, same
@@ -124,9 +128,29 @@ typedef struct {
  * ws: at least specmemo_workspace_bytes(SPECMEMO_WS_TOPK, ...) bytes. */
 int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hidden,
                          int32_t vocab, int32_t n_heads, const int32_t *topk_h, const void *h,
-                         const void *head_w, const int32_t *root_tok, float *logits_out,
-                         int32_t *topk_ids, float *topk_vals, int32_t *node_tok, void *ws,
-                         size_t ws_bytes, void *stream);
+                         const void *head_w, int32_t head_layout, const int32_t *root_tok,
+                         float *logits_out, int32_t *topk_ids, float *topk_vals,
+                         int32_t *node_tok, void *ws, size_t ws_bytes, void *stream);
+
+/* Head weights in the projection's streaming order (bf16).  The heads are
+ * fixed for a model, so they are packed once, at load time:
+ *
+ *   packed element ((((i * nG + G) * nS + s) * 4 + t) * 64 + l) * 8 + e
+ *     = head_w[i][64 G + 16 t + l % 16][32 s + 8 (l / 16) + e]
+ *
+ * for head i, row group G < nG = ceil(vocab / 64), k step s < nS =
+ * ceil(hidden / 32), row tile t < 4, lane l < 64 and e < 8; rows past vocab and
+ * columns past hidden are zero.  Each 1 KB (t, s) block is one matrix-core
+ * operand tile of 16 rows x 32 columns, and a row group's blocks are
+ * contiguous.  src: device [n_heads][vocab][hidden] bf16 (row-major, as
+ * above); dst: device, specmemo_packed_heads_bytes(...) bytes, 16-byte
+ * aligned, not overlapping src.  Requires hidden % 8 == 0.  Asynchronous on
+ * `stream`. */
+int specmemo_pack_heads(specmemo_dtype dt, int32_t n_heads, int32_t vocab, int32_t hidden,
+                        const void *src, void *dst, void *stream);
+/* Bytes of the packed head weights (0 for invalid arguments or fp32). */
+size_t specmemo_packed_heads_bytes(specmemo_dtype dt, int32_t n_heads, int32_t vocab,
+                                   int32_t hidden);
 
 /* (b) Tree-masked attention of one layer (Sec. 3.1: before verification the
  * mask assumes full acceptance of every candidate sequence, so a node attends

@@ -159,38 +159,56 @@ int device_cus() {
   return n;
 }
 
-// Work items of one launch for a chunk length c (INT32_MAX: no split).
-int64_t attn_items(const std::vector<AttnSeq> &grp, int n_kv, int c) {
-  int64_t items = 0;
-  for (const AttnSeq &s : grp) items += (int64_t)n_kv * s.nrb * (s.L <= c ? 1 : (s.L + c - 1) / c);
-  return items;
-}
-
-// Chunk length of one launch.  If every work item fits in one round of
-// resident blocks, the smallest chunk that still fits (largest item smallest);
-// otherwise long sequences are split down to the average work of one block slot.
-int attn_chunk(const std::vector<AttnSeq> &grp, int n_kv, int slots) {
+// Chunks per sequence for one launch (sets s.nch and s.ch_len).  A work item
+// of sequence s covers about (L + N) / nch keys.  When the unsplit items fit
+// in one round of resident blocks, chunks are added greedily to the sequence
+// with the largest items while the round still holds them (this minimises the
+// largest item); otherwise sequences are split down to the average work of one
+// block slot.  Chunks hold at least kMinChunk committed keys, and the last
+// chunk of a sequence also takes its tree rows.
+void attn_chunks(std::vector<AttnSeq> &grp, int n_kv, int slots) {
   static const int fixed_chunk = env_int("SPECMEMO_ATTN_CHUNK", -1);
-  if (fixed_chunk == 0) return INT32_MAX;
-  if (fixed_chunk > 0) return std::max(kAttnKeyTile, fixed_chunk / kAttnKeyTile * kAttnKeyTile);
-  int maxL = 0;
-  int64_t work = 0;
-  for (const AttnSeq &s : grp) {
-    maxL = std::max(maxL, s.L);
-    work += (int64_t)n_kv * s.nrb * (s.L + s.N);
-  }
-  if (attn_items(grp, n_kv, INT32_MAX) <= slots) {
-    int lo = kMinChunk / kAttnKeyTile, hi = (maxL + kAttnKeyTile - 1) / kAttnKeyTile;   // in tiles
-    if (lo >= hi) return INT32_MAX;
-    while (lo < hi) {                  // smallest chunk with items <= slots
-      const int mid = (lo + hi) / 2;
-      if (attn_items(grp, n_kv, mid * kAttnKeyTile) <= slots) hi = mid; else lo = mid + 1;
+  std::vector<int> nch(grp.size(), 1);
+  auto max_nch = [&](const AttnSeq &s) { return std::max(1, s.L / kMinChunk); };
+  if (fixed_chunk > 0) {
+    const int c = std::max(kAttnKeyTile, fixed_chunk / kAttnKeyTile * kAttnKeyTile);
+    for (size_t i = 0; i < grp.size(); ++i) nch[i] = grp[i].L <= c ? 1 : (grp[i].L + c - 1) / c;
+  } else if (fixed_chunk < 0) {
+    int64_t items = 0, work = 0;
+    for (const AttnSeq &s : grp) {
+      items += (int64_t)n_kv * s.nrb;
+      work += (int64_t)n_kv * s.nrb * (s.L + s.N);
     }
-    return lo * kAttnKeyTile >= maxL ? INT32_MAX : lo * kAttnKeyTile;
+    if (items <= slots) {
+      for (;;) {
+        int best = -1;
+        double big = 0;
+        for (size_t i = 0; i < grp.size(); ++i) {
+          const double size = (double)(grp[i].L + grp[i].N) / nch[i];
+          if (size > big) big = size, best = (int)i;
+        }
+        if (best < 0 || nch[best] >= max_nch(grp[best]) || items + (int64_t)n_kv * grp[best].nrb > slots) break;
+        items += (int64_t)n_kv * grp[best].nrb;
+        ++nch[best];
+      }
+    } else {
+      const int64_t target = std::max<int64_t>(kMinChunk, (work + slots - 1) / slots);
+      for (size_t i = 0; i < grp.size(); ++i)
+        nch[i] = (int)std::min<int64_t>(max_nch(grp[i]), (grp[i].L + grp[i].N + target - 1) / target);
+    }
   }
-  const int64_t c = (work + slots - 1) / slots;
-  const int64_t ct = std::max<int64_t>(kMinChunk, (c + kAttnKeyTile - 1) / kAttnKeyTile * kAttnKeyTile);
-  return ct >= maxL ? INT32_MAX : (int)ct;
+  for (size_t i = 0; i < grp.size(); ++i) {
+    AttnSeq &s = grp[i];
+    if (nch[i] <= 1) {
+      s.nch = 1;
+      s.ch_len = s.L + s.N;
+      continue;
+    }
+    // equal chunks of whole key tiles; the count may drop by rounding
+    const int c = ((s.L + nch[i] - 1) / nch[i] + kAttnKeyTile - 1) / kAttnKeyTile * kAttnKeyTile;
+    s.nch = (s.L + c - 1) / c;
+    s.ch_len = s.nch == 1 ? s.L + s.N : c;
+  }
 }
 
 void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *kv, int n_q, AttnPlan *p) {
@@ -198,7 +216,7 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
   const int max_rows = ti.max_nodes * g;
   static const int rows_env = env_int("SPECMEMO_ATTN_ROWS", 0);
   static const int xcd_env = env_int("SPECMEMO_ATTN_XCD", 1);
-  p->rb = max_rows <= 64 ? 64 : max_rows <= 128 ? 128 : 256;
+  p->rb = max_rows <= 64 ? 64 : 128;
   if (rows_env == 64 || rows_env == 128 || rows_env == 256) p->rb = rows_env;
   p->xcd_order = xcd_env != 0;
   const int RB = p->rb;
@@ -219,12 +237,14 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
       s.nrb = (s.N * g + RB - 1) / RB;
       grp.push_back(s);
     }
-    const int ch_len = attn_chunk(grp, kv->n_kv, slots);
+    attn_chunks(grp, kv->n_kv, slots);
+    // largest items first (the dispatch order of the launch)
+    std::stable_sort(grp.begin(), grp.end(), [](const AttnSeq &x, const AttnSeq &y) {
+      return (int64_t)(x.L + x.N) * y.nch > (int64_t)(y.L + y.N) * x.nch;
+    });
     int item = 0, part = 0, citem = 0, unit = 0;
     int per_xcd[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     for (AttnSeq &s : grp) {
-      s.nch = (ch_len == INT32_MAX || s.L <= ch_len) ? 1 : (s.L + ch_len - 1) / ch_len;
-      s.ch_len = s.nch == 1 ? s.L + s.N : ch_len;
       s.item0 = item;
       s.unit0 = unit;
       const int units = kv->n_kv * s.nch;
@@ -296,12 +316,37 @@ size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo
   return 0;
 }
 
-int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hidden, int32_t vocab, int32_t n_heads,
-                         const int32_t *topk_h, const void *h, const void *head_w, const int32_t *root_tok,
-                         float *logits_out, int32_t *topk_ids, float *topk_vals, int32_t *node_tok, void *ws,
-                         size_t ws_bytes, void *stream) {
+size_t specmemo_packed_heads_bytes(specmemo_dtype dt, int32_t n_heads, int32_t vocab, int32_t hidden) {
+  if (dt != SPECMEMO_BF16 || n_heads < 1 || vocab < 1 || hidden < 8 || hidden % 8) return 0;
+  return (size_t)n_heads * packed_row_groups(vocab) * packed_k_steps(hidden) * 4 * 1024;
+}
+
+int specmemo_pack_heads(specmemo_dtype dt, int32_t n_heads, int32_t vocab, int32_t hidden, const void *src, void *dst,
+                        void *stream) {
   int rc;
   if ((rc = check_dtype(dt))) return rc;
+  if (dt != SPECMEMO_BF16) return fail(SPECMEMO_E_DTYPE, "packed heads are bf16 only");
+  if (n_heads < 1 || vocab < 1) return fail(SPECMEMO_E_ARG, "n_heads=%d vocab=%d", n_heads, vocab);
+  if (hidden < 8 || hidden % 8) return fail(SPECMEMO_E_ARG, "hidden=%d must be a positive multiple of 8", hidden);
+  if (!al(src, 16) || !al(dst, 16)) return fail(SPECMEMO_E_ARG, "src / dst must be non-NULL and 16-byte aligned");
+  const size_t nb = specmemo_packed_heads_bytes(dt, n_heads, vocab, hidden);
+  const size_t sb = (size_t)n_heads * vocab * hidden * 2;
+  const uintptr_t s0 = (uintptr_t)src, d0 = (uintptr_t)dst;
+  if (s0 < d0 + nb && d0 < s0 + sb) return fail(SPECMEMO_E_ARG, "dst overlaps src");
+  return hip_status(launch_pack_heads(src, dst, n_heads, vocab, hidden, static_cast<hipStream_t>(stream)),
+                    "head packing launch");
+}
+
+int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hidden, int32_t vocab, int32_t n_heads,
+                         const int32_t *topk_h, const void *h, const void *head_w, int32_t head_layout,
+                         const int32_t *root_tok, float *logits_out, int32_t *topk_ids, float *topk_vals,
+                         int32_t *node_tok, void *ws, size_t ws_bytes, void *stream) {
+  int rc;
+  if ((rc = check_dtype(dt))) return rc;
+  if (head_layout != SPECMEMO_HEADS_ROWMAJOR && head_layout != SPECMEMO_HEADS_PACKED)
+    return fail(SPECMEMO_E_ARG, "unknown head_layout %d", head_layout);
+  if (head_layout == SPECMEMO_HEADS_PACKED && dt != SPECMEMO_BF16)
+    return fail(SPECMEMO_E_DTYPE, "packed heads are bf16 only");
   if (n_heads < 1 || n_heads > SPECMEMO_MAX_DEPTH) return fail(SPECMEMO_E_ARG, "n_heads=%d outside [1, %d]", n_heads, SPECMEMO_MAX_DEPTH);
   if (!topk_h) return fail(SPECMEMO_E_ARG, "topk_h is NULL");
   if (vocab < 1) return fail(SPECMEMO_E_ARG, "vocab=%d", vocab);
@@ -329,7 +374,8 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
   char *cand = static_cast<char *>(ws) + zb;
   const size_t ncand = (size_t)ti.B * n_heads * topk_nsplit(vocab) * kmax;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e = launch_head_logits(dt, h, head_w, z, ti.B, hidden, vocab, n_heads, st);
+  hipError_t e = launch_head_logits(dt, h, head_w, head_layout == SPECMEMO_HEADS_PACKED, z, ti.B, hidden, vocab,
+                                    n_heads, st);
   if (e != hipSuccess) return hip_status(e, "head projection launch");
   TopkArgs a{};
   a.z = z;

@@ -29,8 +29,12 @@ struct TopkArgs {
 constexpr int kTopkSlice = 2048;
 constexpr int kTopkMaxCand = 2048;   // nsplit * kmax, merged by one block
 
-hipError_t launch_head_logits(int dt, const void *h, const void *w, float *z, int B, int hidden,
+hipError_t launch_head_logits(int dt, const void *h, const void *w, bool packed, float *z, int B, int hidden,
                               int vocab, int n_heads, hipStream_t st);
+// Packed head weights: 64-row groups x 32-column k steps of 4 KB each.
+__host__ __device__ constexpr int packed_row_groups(int vocab) { return (vocab + 63) / 64; }
+__host__ __device__ constexpr int packed_k_steps(int hidden) { return (hidden + 31) / 32; }
+hipError_t launch_pack_heads(const void *src, void *dst, int n_heads, int vocab, int hidden, hipStream_t st);
 hipError_t launch_topk(const TopkArgs &a, int B, hipStream_t st);
 
 // ---- tree attention ------------------------------------------------------------

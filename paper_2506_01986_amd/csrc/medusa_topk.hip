@@ -112,6 +112,99 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_bf16(
   }
 }
 
+// Packed heads (see specmemo_pack_heads): wave (head, G) streams its row
+// group's nS * 4 KB contiguously, one 1 KB operand tile per load instruction,
+// and contracts each tile against the 16 hidden states of its batch tile.
+constexpr int kPackedUnroll = 4;   // k steps (4 KB each) issued before their MFMAs
+
+template <int NB>
+__global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
+    const uint16_t *__restrict__ h, const uint4 *__restrict__ Wp, float *__restrict__ z, int B, int hidden,
+    int vocab, int n_heads, int nG, int nS) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int head = blockIdx.y, b0 = blockIdx.z * 16 * NB;
+  const int G = blockIdx.x * kWaves + wave;
+  if (G >= nG) return;
+  const int kq = lane >> 4;
+  const uint4 *wp = Wp + (int64_t)(head * nG + G) * nS * 4 * 64 + lane;
+  bool bvalid[NB];
+  const uint16_t *hp[NB];
+#pragma unroll
+  for (int n = 0; n < NB; ++n) {
+    const int b = b0 + 16 * n + (lane & 15);
+    bvalid[n] = b < B;
+    hp[n] = h + (int64_t)(bvalid[n] ? b : 0) * hidden + kq * 8;
+  }
+  f32x4 acc[NB][4];
+#pragma unroll
+  for (int n = 0; n < NB; ++n)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[n][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto step = [&](const uint4 (&a)[4], int s) {
+    const int k = 32 * s + 8 * kq;
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+      const bf16x8 bv = __builtin_bit_cast(bf16x8, ld16_or_zero(bvalid[n] && k < hidden, hp[n] + 32 * s));
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        acc[n][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[t]), bv, acc[n][t], 0, 0, 0);
+    }
+  };
+  int s = 0;
+  for (; s + kPackedUnroll <= nS; s += kPackedUnroll) {
+    uint4 a[kPackedUnroll][4];
+#pragma unroll
+    for (int u = 0; u < kPackedUnroll; ++u)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) a[u][t] = wp[((s + u) * 4 + t) * 64];
+#pragma unroll
+    for (int u = 0; u < kPackedUnroll; ++u) step(a[u], s + u);
+  }
+  for (; s < nS; ++s) {
+    uint4 a[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) a[t] = wp[(s * 4 + t) * 64];
+    step(a, s);
+  }
+
+  // C layout: lane holds column (batch) lane&15, rows 4*(lane>>4) + 0..3 of each tile.
+#pragma unroll
+  for (int n = 0; n < NB; ++n) {
+    const int b = b0 + 16 * n + (lane & 15);
+    if (b >= B) continue;
+    float *zr = z + ((int64_t)b * n_heads + head) * vocab;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int row = 64 * G + t * 16 + 4 * kq;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (row + j < vocab) zr[row + j] = acc[n][t][j];
+    }
+  }
+}
+
+// One thread per 16-byte chunk of the packed buffer (see specmemo_pack_heads).
+__global__ __launch_bounds__(256) void pack_heads_bf16(const uint16_t *__restrict__ src, uint4 *__restrict__ dst,
+                                                       int vocab, int hidden, int nG, int nS, int64_t chunks) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= chunks) return;
+  const int l = (int)(idx & 63);
+  int64_t rest = idx >> 6;
+  const int t = (int)(rest & 3);
+  rest >>= 2;
+  const int s = (int)(rest % nS);
+  rest /= nS;
+  const int G = (int)(rest % nG);
+  const int head = (int)(rest / nG);
+  const int row = 64 * G + 16 * t + (l & 15);
+  const int col = 32 * s + 8 * (l >> 4);
+  uint4 v = {0u, 0u, 0u, 0u};
+  if (row < vocab && col < hidden)    // hidden % 8 == 0: the 8 columns are all inside or all outside
+    v = *reinterpret_cast<const uint4 *>(src + ((int64_t)head * vocab + row) * hidden + col);
+  dst[idx] = v;
+}
+
 // fp32 heads: one wave per vocabulary row, lanes stride the hidden dimension.
 constexpr int kF32BatchTile = 8;
 
@@ -290,9 +383,16 @@ __global__ __launch_bounds__(kSel) void topk_merge(TopkArgs a) {
 
 }  // namespace
 
-hipError_t launch_head_logits(int dt, const void *h, const void *w, float *z, int B, int hidden,
+hipError_t launch_head_logits(int dt, const void *h, const void *w, bool packed, float *z, int B, int hidden,
                               int vocab, int n_heads, hipStream_t st) {
-  if (dt == 1) {
+  if (dt == 1 && packed) {
+    const int nb = B <= 16 ? 1 : 2;
+    const int nG = packed_row_groups(vocab), nS = packed_k_steps(hidden);
+    dim3 grid((nG + kWaves - 1) / kWaves, n_heads, (B + 16 * nb - 1) / (16 * nb));
+    auto kern = nb == 1 ? head_logits_packed<1> : head_logits_packed<2>;
+    hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0, st, static_cast<const uint16_t *>(h),
+                       static_cast<const uint4 *>(w), z, B, hidden, vocab, n_heads, nG, nS);
+  } else if (dt == 1) {
     const int nb = B <= 16 ? 1 : 2;
     dim3 grid((vocab + kWaves * kRowsPerWave - 1) / (kWaves * kRowsPerWave), n_heads,
               (B + 16 * nb - 1) / (16 * nb));
@@ -304,6 +404,14 @@ hipError_t launch_head_logits(int dt, const void *h, const void *w, float *z, in
     hipLaunchKernelGGL(head_logits_f32, grid, dim3(256), 0, st, static_cast<const float *>(h),
                        static_cast<const float *>(w), z, B, hidden, vocab, n_heads);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_heads(const void *src, void *dst, int n_heads, int vocab, int hidden, hipStream_t st) {
+  const int nG = packed_row_groups(vocab), nS = packed_k_steps(hidden);
+  const int64_t chunks = (int64_t)n_heads * nG * nS * 4 * 64;
+  hipLaunchKernelGGL(pack_heads_bf16, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, st,
+                     static_cast<const uint16_t *>(src), static_cast<uint4 *>(dst), vocab, hidden, nG, nS, chunks);
   return hipGetLastError();
 }
 

@@ -85,6 +85,22 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short s16x4_t __attribute__((__vector_size__(8)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
+// 16-byte direct load of every lane into LDS at lds_base + 16 * lane (one
+// global_load_lds_dwordx4 with M0 = lds_base, which must be wave-uniform).  It
+// is issued from inline assembly so that the compiler does not guard later LDS
+// reads with waits for it: the tile ring orders these loads with explicit
+// vmcnt waits.  M0 must be written one wait state before the load.
+__device__ __forceinline__ void lds_load16(const void *src, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_base)
+               : "memory", "m0");
+}
+
+// Workgroup barrier for the LDS tile ring.  The tile loads into LDS are
+// ordered by explicit vmcnt waits; a __syncthreads() would also wait for the
+// loads still in flight for later tiles (its release fence waits for every
+// outstanding vector memory operation) and so shorten the prefetch distance.
+__device__ __forceinline__ void ring_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // LDS swizzles (16-byte chunk index c of tile row r).  K rows are read 16 rows
 // at a time at one chunk (MFMA A operand): chunk c of row r sits at c ^ (r % 16).
 // V rows are read by the transposing load 4 rows x 4 chunks at a time:
@@ -146,6 +162,11 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
     const uint16_t *qbase = static_cast<const uint16_t *>(a.q) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D + 8 * h;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, ld16_or_zero(row_ok, qbase + 16 * ks));
+    // Land the Q loads here: otherwise the compiler waits for them at their
+    // first use inside the tile loop, on every iteration, and with them for
+    // every tile load in flight.
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) asm volatile("" ::"v"(qf[ks]));
   }
 
   // Key range of this chunk: chunk boundaries lie inside the committed region and
@@ -173,18 +194,17 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   const uint8_t *Vb = reinterpret_cast<const uint8_t *>(Vg);
   auto issue = [&](const uint8_t *src, const int (&off)[IPW], uint8_t *dst, int j) {
     const int kt = k0 + j * TK;
+    const uint32_t lds = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(lds_void_t *)(dst + 1024 * wave * IPW));
     if (kt + TK <= k1) {
       const uint8_t *sb = src + (int64_t)kt * (D * 2);
 #pragma unroll
-      for (int u = 0; u < IPW; ++u)
-        __builtin_amdgcn_global_load_lds((const void *)(sb + off[u]), (lds_void_t *)(dst + 1024 * (wave * IPW + u)), 16, 0, 0);
+      for (int u = 0; u < IPW; ++u) lds_load16(sb + off[u], lds + 1024 * u);
     } else {                             // last tile: rows past the chunk end repeat its last row
 #pragma unroll
       for (int u = 0; u < IPW; ++u) {
         const int64_t t = min(kt + lrow[u], k1 - 1);
-        const int cofs = off[u] - lrow[u] * (D * 2);
-        __builtin_amdgcn_global_load_lds((const void *)(src + t * (D * 2) + cofs),
-                                         (lds_void_t *)(dst + 1024 * (wave * IPW + u)), 16, 0, 0);
+        lds_load16(src + t * (D * 2) + (off[u] - lrow[u] * (D * 2)), lds + 1024 * u);
       }
     }
   };
@@ -327,7 +347,7 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   for (int j = 0; j < ntiles; ++j) {
     // loads issued after tile j: tile j+1 (3 slots), two operands
     wait_loads(SLOTS == 3 && j + 1 < ntiles ? 2 : 0);
-    __syncthreads();
+    ring_barrier();
     if (j == 0) read_anc();
     if (j + SLOTS - 1 < ntiles) {
       issue_k(j + SLOTS - 1);

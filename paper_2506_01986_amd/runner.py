@@ -32,7 +32,7 @@ def to_host_storage(t: torch.Tensor, dtype: str) -> np.ndarray:
 
 class VerifyStep:
     def __init__(self, wl: Workload, device="cuda", mode: int = sm.GREEDY, temperature: float = 0.7,
-                 eps: float = 0.09, delta: float = 0.3, keep_logits: bool = False):
+                 eps: float = 0.09, delta: float = 0.3, keep_logits: bool = False, pack_heads: bool = True):
         cfg = wl.cfg
         self.wl, self.cfg, self.device = wl, cfg, device
         self.dt = sm.FP32 if cfg.dtype == "fp32" else sm.BF16
@@ -41,6 +41,14 @@ class VerifyStep:
         self.trees = sm.Trees(wl.node_off, wl.parent, wl.depth, wl.rank, device=device)
         self.h = to_device(wl.hidden, cfg.dtype, device)
         self.head_w = to_device(wl.head_w, cfg.dtype, device) if wl.head_w is not None else None
+        # bf16 heads are packed once into the projection's streaming order (a
+        # load-time step: the heads are fixed for a model)
+        self.head_layout = sm.HEADS_ROWMAJOR
+        if pack_heads and self.head_w is not None and self.dt == sm.BF16:
+            nb = sm.packed_heads_bytes(self.dt, cfg.n_heads, cfg.vocab, cfg.hidden)
+            packed = torch.empty(nb, dtype=torch.uint8, device=device)
+            sm.pack_heads(self.dt, cfg.n_heads, cfg.vocab, cfg.hidden, self.head_w, packed)
+            self.head_w, self.head_layout = packed, sm.HEADS_PACKED
         self.root_tok = torch.from_numpy(wl.root_tok.copy()).to(device)
         self.q = to_device(wl.q, cfg.dtype, device)
         self.k = to_device(wl.pool_k, cfg.dtype, device)
@@ -72,7 +80,8 @@ class VerifyStep:
         c = self.cfg
         sm.medusa_topk(self.dt, self.trees, c.hidden, c.vocab, c.n_heads, c.topk, self.h, self.head_w,
                        self.root_tok, self.topk_ids, self.node_tok, logits_out=self.logits,
-                       topk_vals=self.topk_vals, ws=self.ws, ws_bytes=self.ws_bytes, stream=stream)
+                       topk_vals=self.topk_vals, ws=self.ws, ws_bytes=self.ws_bytes, stream=stream,
+                       head_layout=self.head_layout)
 
     def tree_attn(self, stream=None):
         sm.tree_attn(self.dt, self.trees, self.kv, self.cfg.n_q, self.q, self.out, ws=self.ws,

@@ -21,6 +21,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "specmemo.h")
 
 FP32, BF16 = 0, 1
 GREEDY, TYPICAL = 0, 1
+HEADS_ROWMAJOR, HEADS_PACKED = 0, 1
 WS_TOPK, WS_ATTN, WS_ACCEPT = 0, 1, 2
 
 STATUS = {0: "OK", -1: "E_ARG", -2: "E_DTYPE", -3: "E_TREE", -4: "E_BUDGET", -5: "E_WORKSPACE", -6: "E_HIP"}
@@ -57,7 +58,11 @@ def load():
         lib = C.CDLL(LIB_PATH)
         vp, i32, sz, f32 = C.c_void_p, C.c_int32, C.c_size_t, C.c_float
         PT, PK = C.POINTER(_Trees), C.POINTER(_KV)
-        lib.specmemo_medusa_topk.argtypes = [i32, PT, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        lib.specmemo_medusa_topk.argtypes = [i32, PT, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, sz, vp]
+        lib.specmemo_pack_heads.argtypes = [i32, i32, i32, i32, vp, vp, vp]
+        lib.specmemo_pack_heads.restype = C.c_int
+        lib.specmemo_packed_heads_bytes.argtypes = [i32, i32, i32, i32]
+        lib.specmemo_packed_heads_bytes.restype = C.c_size_t
         lib.specmemo_tree_attn.argtypes = [i32, PT, PK, i32, f32, vp, vp, vp, sz, vp]
         lib.specmemo_accept.argtypes = [i32, PT, i32, i32, f32, f32, f32, vp, vp, vp, vp, i32, vp, vp, sz, vp]
         lib.specmemo_kv_compact.argtypes = [i32, PT, PK, vp, vp, i32, vp]
@@ -164,12 +169,21 @@ def workspace_bytes(which: int, dt: int, trees: Trees, kv: Optional[KVPool], n_q
 
 def medusa_topk(dt: int, trees: Trees, hidden: int, vocab: int, n_heads: int, topk: Sequence[int], h, head_w,
                 root_tok, topk_ids, node_tok, logits_out=None, topk_vals=None, ws=None, ws_bytes: int = 0,
-                stream=None):
+                stream=None, head_layout: int = HEADS_ROWMAJOR):
     ts = trees.struct()
     tk = _i32(topk)
     _check(load().specmemo_medusa_topk(dt, C.byref(ts), hidden, vocab, n_heads, tk.ctypes.data, _ptr(h),
-                                       _ptr(head_w), _ptr(root_tok), _ptr(logits_out), _ptr(topk_ids),
-                                       _ptr(topk_vals), _ptr(node_tok), _ptr(ws), ws_bytes, _stream(stream)))
+                                       _ptr(head_w), head_layout, _ptr(root_tok), _ptr(logits_out),
+                                       _ptr(topk_ids), _ptr(topk_vals), _ptr(node_tok), _ptr(ws), ws_bytes,
+                                       _stream(stream)))
+
+
+def packed_heads_bytes(dt: int, n_heads: int, vocab: int, hidden: int) -> int:
+    return int(load().specmemo_packed_heads_bytes(dt, n_heads, vocab, hidden))
+
+
+def pack_heads(dt: int, n_heads: int, vocab: int, hidden: int, src, dst, stream=None):
+    _check(load().specmemo_pack_heads(dt, n_heads, vocab, hidden, _ptr(src), _ptr(dst), _stream(stream)))
 
 
 def tree_attn(dt: int, trees: Trees, kv: KVPool, n_q: int, q, out, scale: float = 0.0, ws=None,

@@ -31,7 +31,7 @@ def test_library_loads_and_exports_every_declared_function():
     assert {"specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert sm.abi_version() == 1
+    assert sm.abi_version() == 2
 
 
 class FakeTrees(sm.Trees):
@@ -63,9 +63,10 @@ def attn(trees, kv, n_q=4, dt=sm.BF16):
     sm.tree_attn(dt, trees, kv, n_q, FAKE, FAKE, ws=FAKE, ws_bytes=1 << 30, stream=0)
 
 
-def topk(trees, hidden=256, vocab=1000, n_heads=3, k=(4, 2, 2), dt=sm.BF16, ws_bytes=1 << 30, logits=None):
+def topk(trees, hidden=256, vocab=1000, n_heads=3, k=(4, 2, 2), dt=sm.BF16, ws_bytes=1 << 30, logits=None,
+         layout=sm.HEADS_ROWMAJOR):
     sm.medusa_topk(dt, trees, hidden, vocab, n_heads, k, FAKE, FAKE, FAKE, FAKE, FAKE, logits_out=logits,
-                   ws=FAKE, ws_bytes=ws_bytes, stream=0)
+                   ws=FAKE, ws_bytes=ws_bytes, stream=0, head_layout=layout)
 
 
 @cpu_only
@@ -107,6 +108,26 @@ def test_argument_errors():
     with pytest.raises(sm.SpecmemoError) as e:       # misaligned device pointer
         sm.tree_attn(sm.BF16, t, FakeKV([10], [40], [0]), 4, FAKE + 2, FAKE, stream=0)
     assert e.value.name == "E_ARG"
+
+
+@cpu_only
+def test_packed_head_errors_and_sizes():
+    t = FakeTrees([synth.t16()])
+    expect("E_ARG", topk, t, layout=7)
+    expect("E_DTYPE", topk, t, dt=sm.FP32, layout=sm.HEADS_PACKED)
+    assert sm.packed_heads_bytes(sm.BF16, 4, 32000, 8192) == 4 * 500 * 256 * 4096
+    assert sm.packed_heads_bytes(sm.BF16, 3, 1000, 72) == 3 * 16 * 3 * 4096     # ragged: 16 row groups, 3 k steps
+    assert sm.packed_heads_bytes(sm.FP32, 3, 1000, 256) == 0
+    assert sm.packed_heads_bytes(sm.BF16, 3, 1000, 100) == 0                    # hidden % 8 != 0
+    with pytest.raises(sm.SpecmemoError) as e:
+        sm.pack_heads(sm.FP32, 3, 1000, 256, FAKE, FAKE * 2, stream=0)
+    assert e.value.name == "E_DTYPE"
+    with pytest.raises(sm.SpecmemoError) as e:
+        sm.pack_heads(sm.BF16, 3, 1000, 100, FAKE, FAKE * 2, stream=0)
+    assert e.value.name == "E_ARG"
+    with pytest.raises(sm.SpecmemoError) as e:                                  # dst overlaps src
+        sm.pack_heads(sm.BF16, 3, 1000, 256, FAKE, FAKE + 4096, stream=0)
+    assert e.value.name == "E_ARG" and "overlap" in str(e.value)
 
 
 @cpu_only

@@ -100,12 +100,12 @@ def distinct_sibling_tokens(wl, rng):
     return tok
 
 
-def run_parity(torch, wl, max_attn_rows=None, typical=True, label=""):
+def run_parity(torch, wl, max_attn_rows=None, typical=True, label="", pack_heads=True):
     from paper_2506_01986_amd import runner, specmemo as sm
     cfg = wl.cfg
     say(f"[parity] {label or cfg.name}: B={cfg.B} sumN={wl.total_nodes} L={wl.lens.tolist()[:8]}")
     rng = np.random.default_rng(1234)
-    step = runner.VerifyStep(wl, keep_logits=True)
+    step = runner.VerifyStep(wl, keep_logits=True, pack_heads=pack_heads)
 
     # (a) head projection, top-k, tree tokens
     say("[parity]   stage a")
@@ -233,12 +233,45 @@ EDGES = {
 }
 
 
+# edge cases whose heads stay in the row-major (nn.Linear) layout; the others
+# use the packed layout, as do the five workloads
+ROWMAJOR_HEADS = {"mha_b17", "split_kv"}
+
+
 @pytest.mark.parametrize("name", list(EDGES))
 def test_edge_parity(torch_cuda, name):
     cfg, trees, lens = EDGES[name]
     rng = np.random.default_rng(len(name))
     wl = synth.make(cfg, trees=trees(rng), lens=lens)
-    run_parity(torch_cuda, wl, label=name)
+    run_parity(torch_cuda, wl, label=name, pack_heads=name not in ROWMAJOR_HEADS)
+
+
+def test_pack_heads_layout(torch_cuda):
+    """The packed buffer holds head_w[i][64 G + 16 t + l % 16][32 s + 8 (l / 16) + e]
+    at element ((((i nG + G) nS + s) 4 + t) 64 + l) 8 + e, zero past vocab and hidden."""
+    import torch
+    from paper_2506_01986_amd import specmemo as sm
+    n_heads, vocab, hidden = 2, 150, 72          # ragged in both row groups and k steps
+    rng = np.random.default_rng(9)
+    w = rng.integers(1, 0x7F00, size=(n_heads, vocab, hidden)).astype(np.uint16)   # distinct-ish bit patterns
+    src = torch.from_numpy(w.view(np.int16)).cuda()
+    nbytes = sm.packed_heads_bytes(sm.BF16, n_heads, vocab, hidden)
+    nG, nS = -(-vocab // 64), -(-hidden // 32)
+    assert nbytes == n_heads * nG * nS * 4096
+    dst = torch.full((nbytes // 2,), -1, dtype=torch.int16, device="cuda")
+    sm.pack_heads(sm.BF16, n_heads, vocab, hidden, src, dst)
+    got = dst.cpu().numpy().view(np.uint16)
+    want = np.zeros(nbytes // 2, np.uint16)
+    for i in range(n_heads):
+        for G in range(nG):
+            for s in range(nS):
+                for t in range(4):
+                    for l in range(64):
+                        row, col = 64 * G + 16 * t + l % 16, 32 * s + 8 * (l // 16)
+                        if row < vocab and col < hidden:
+                            o = ((((i * nG + G) * nS + s) * 4 + t) * 64 + l) * 8
+                            want[o:o + 8] = w[i, row, col:col + 8]
+    assert np.array_equal(got, want)
 
 
 def test_acceptance_small_vocab_random(torch_cuda):
