@@ -31,7 +31,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 METRIC = "verified tree tokens/sec per verify step; achieved HBM GB/s vs peak"
 # Kernels each stage launches through the C ABI (for matching rocprofv3 traces).
-STAGE_KERNELS = {"medusa_topk": ["head_logits_packed", "topk_partial", "topk_merge"],
+STAGE_KERNELS = {"medusa_topk": ["head_logits_packed", "topk_rows"],
                  "tree_attn": ["tree_attn_bf16", "tree_attn_combine"],
                  "accept": ["accept_greedy"], "kv_compact": ["kv_compact_kernel"]}
 STAGE_SOURCES = {"medusa_topk": "medusa_topk.hip", "tree_attn": "tree_attn.hip",

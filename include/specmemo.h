@@ -213,8 +213,11 @@ int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specme
 #define SPECMEMO_WS_ATTN 1
 #define SPECMEMO_WS_ACCEPT 2
 
-/* Workspace bytes a call needs for these arguments (host-only; no HIP call).
- *   SPECMEMO_WS_TOPK:   kv ignored; n_q_or_heads = n_heads; vocab used.
+/* Workspace bytes a call needs for these arguments (host-side; the only HIP
+ * calls query the current device's compute-unit count, which the attention
+ * work split depends on; 256 is assumed when no device is visible).
+ *   SPECMEMO_WS_TOPK:   kv ignored; n_q_or_heads = n_heads; vocab used (the
+ *                       fp32 logits; none are needed when logits_out is given).
  *   SPECMEMO_WS_ATTN:   kv required; n_q_or_heads = n_q; vocab ignored.
  *   SPECMEMO_WS_ACCEPT: kv ignored; n_q_or_heads = accept mode; vocab ignored.
  * Returns 0 for invalid arguments as well as when no workspace is needed;

@@ -114,33 +114,42 @@ template <int DT>
 __global__ __launch_bounds__(kNT) void accept_greedy(AcceptArgs a) {
   __shared__ float sv[kWaves];
   __shared__ int si[kWaves];
-  __shared__ int s_next;
-  __shared__ int s_path[kMaxPath];
-  const int b = blockIdx.x, tid = threadIdx.x;
+  __shared__ int s_par[kMaxNodes], s_tok[kMaxNodes];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
+  // The tree's parents and tokens go to LDS once (visible after the first
+  // barrier inside row_argbest); each wave then finds the next node itself.
+  for (int n = tid; n < N; n += kNT) {
+    s_par[n] = n == 0 ? -1 : a.parent[n0 + n];
+    s_tok[n] = a.node_tok[n0 + n];
+  }
   int cur = 0, len = 0, tok = 0;
-  if (tid == 0) s_path[0] = 0;
+  int path[kMaxPath];
+  path[0] = 0;
   for (;;) {
     float v;
     row_argbest<DT>(a.logits, n0 + cur, a.vocab, sv, si, v, tok);
-    if (tid == 0) s_next = -1;
-    __syncthreads();
-    for (int c = 1 + tid; c < N; c += kNT)
-      if (a.parent[n0 + c] == cur && a.node_tok[n0 + c] == tok) s_next = c;   // unique: sibling tokens differ
-    __syncthreads();
-    const int nxt = s_next;
-    __syncthreads();
+    // the child of cur carrying tok (unique: sibling tokens differ), by ballot
+    // over the (at most kMaxNodes = 128) nodes, two per lane
+    const bool m0 = lane < N && s_par[lane] == cur && s_tok[lane] == tok;
+    const bool m1 = lane + 64 < N && s_par[lane + 64] == cur && s_tok[lane + 64] == tok;
+    const uint64_t b0 = __builtin_amdgcn_ballot_w64(m0), b1 = __builtin_amdgcn_ballot_w64(m1);
+    const int nxt = b0 ? (int)__builtin_ctzll(b0) : b1 ? 64 + (int)__builtin_ctzll(b1) : -1;
     if (nxt < 0 || len + 1 >= kMaxPath) break;
     cur = nxt;
-    ++len;
-    if (tid == 0) s_path[len] = cur;
+    path[++len] = cur;
   }
-  __syncthreads();
   if (tid == 0) {
     a.accept_len[b] = len;
     a.next_tok[b] = tok;
   }
-  for (int j = tid; j < a.path_stride; j += kNT) a.path[(int64_t)b * a.path_stride + j] = j <= len ? s_path[j] : -1;
+  for (int j = tid; j < a.path_stride; j += kNT) {
+    int p = -1;
+#pragma unroll
+    for (int i = 0; i < kMaxPath; ++i)
+      if (i == j && i <= len) p = path[i];
+    a.path[(int64_t)b * a.path_stride + j] = p;
+  }
 }
 
 // Typical mode, pass 1: per row u, x = z_u / T: lse_u = log sum exp x and

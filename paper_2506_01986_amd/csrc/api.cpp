@@ -273,10 +273,6 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
 // Top-k workspace: fp32 logits (unless the caller keeps them) then the slice candidates.
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t topk_logit_bytes(int B, int n_heads, int vocab) { return align256((size_t)B * n_heads * vocab * sizeof(float)); }
-int topk_nsplit(int vocab) { return (vocab + kTopkSlice - 1) / kTopkSlice; }
-size_t topk_cand_bytes(int B, int n_heads, int vocab, int kmax) {
-  return align256((size_t)B * n_heads * topk_nsplit(vocab) * kmax * (sizeof(float) + sizeof(int32_t)));
-}
 
 int check_attn_args(int dt, const specmemo_trees *t, const specmemo_kv *kv, int n_q, TreeInfo *ti) {
   int rc;
@@ -301,7 +297,7 @@ size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo
   if (check_dtype(dt) || check_trees(t, &ti)) return 0;
   if (which == SPECMEMO_WS_TOPK) {
     if (n_q_or_heads < 1 || vocab < 1) return 0;
-    return topk_logit_bytes(ti.B, n_q_or_heads, vocab) + topk_cand_bytes(ti.B, n_q_or_heads, vocab, SPECMEMO_MAX_TOPK);
+    return topk_logit_bytes(ti.B, n_q_or_heads, vocab);
   }
   if (which == SPECMEMO_WS_ATTN) {
     if (check_attn_args(dt, t, kv, n_q_or_heads, &ti)) return 0;
@@ -364,15 +360,10 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
     return fail(SPECMEMO_E_ARG, "root_tok / topk_ids / node_tok must be non-NULL and 4-byte aligned");
   if (logits_out && !al(logits_out, 16)) return fail(SPECMEMO_E_ARG, "logits_out must be 16-byte aligned");
   if (topk_vals && !al(topk_vals, 4)) return fail(SPECMEMO_E_ARG, "topk_vals must be 4-byte aligned");
-  if ((int64_t)topk_nsplit(vocab) * kmax > kTopkMaxCand)
-    return fail(SPECMEMO_E_ARG, "vocab=%d with top-%d exceeds the %d-candidate merge", vocab, kmax, kTopkMaxCand);
-  const size_t zb = logits_out ? 0 : topk_logit_bytes(ti.B, n_heads, vocab);
-  const size_t need = zb + topk_cand_bytes(ti.B, n_heads, vocab, kmax);
-  if (!al(ws, 16) || ws_bytes < need)
+  const size_t need = logits_out ? 0 : topk_logit_bytes(ti.B, n_heads, vocab);
+  if (need && (!al(ws, 16) || ws_bytes < need))
     return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
   float *z = logits_out ? logits_out : static_cast<float *>(ws);
-  char *cand = static_cast<char *>(ws) + zb;
-  const size_t ncand = (size_t)ti.B * n_heads * topk_nsplit(vocab) * kmax;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = launch_head_logits(dt, h, head_w, head_layout == SPECMEMO_HEADS_PACKED, z, ti.B, hidden, vocab,
                                     n_heads, st);
@@ -390,9 +381,6 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
   a.ids = topk_ids;
   a.vals = topk_vals;
   a.node_tok = node_tok;
-  a.nsplit = topk_nsplit(vocab);
-  a.cand_v = reinterpret_cast<float *>(cand);
-  a.cand_i = reinterpret_cast<int32_t *>(cand + ncand * sizeof(float));
   return hip_status(launch_topk(a, ti.B, st), "top-k launch");
 }
 

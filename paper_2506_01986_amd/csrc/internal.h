@@ -22,12 +22,7 @@ struct TopkArgs {
   int32_t *ids;            // [B][n_heads][kmax]
   float *vals;             // same or null
   int32_t *node_tok;
-  int32_t nsplit;          // 2048-wide slices per logit row
-  float *cand_v;           // [B][n_heads][nsplit][kmax] slice candidates
-  int32_t *cand_i;
 };
-constexpr int kTopkSlice = 2048;
-constexpr int kTopkMaxCand = 2048;   // nsplit * kmax, merged by one block
 
 hipError_t launch_head_logits(int dt, const void *h, const void *w, bool packed, float *z, int B, int hidden,
                               int vocab, int n_heads, hipStream_t st);

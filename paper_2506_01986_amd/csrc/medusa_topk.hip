@@ -117,6 +117,13 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_bf16(
 // and contracts each tile against the 16 hidden states of its batch tile.
 constexpr int kPackedUnroll = 4;   // k steps (4 KB each) issued before their MFMAs
 
+// Weights are read once per step: nontemporal loads keep them from displacing
+// the hidden states and logits in the caches.
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld16_stream(const uint4 *p) {
+  return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p)));
+}
+
 template <int NB>
 __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
     const uint16_t *__restrict__ h, const uint4 *__restrict__ Wp, float *__restrict__ z, int B, int hidden,
@@ -157,14 +164,14 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
 #pragma unroll
     for (int u = 0; u < kPackedUnroll; ++u)
 #pragma unroll
-      for (int t = 0; t < 4; ++t) a[u][t] = wp[((s + u) * 4 + t) * 64];
+      for (int t = 0; t < 4; ++t) a[u][t] = ld16_stream(wp + ((s + u) * 4 + t) * 64);
 #pragma unroll
     for (int u = 0; u < kPackedUnroll; ++u) step(a[u], s + u);
   }
   for (; s < nS; ++s) {
     uint4 a[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) a[t] = wp[(s * 4 + t) * 64];
+    for (int t = 0; t < 4; ++t) a[t] = ld16_stream(wp + (s * 4 + t) * 64);
     step(a, s);
   }
 
@@ -237,83 +244,21 @@ __global__ __launch_bounds__(256) void head_logits_f32(const float *__restrict__
   }
 }
 
-// Top-k in two levels.  Level 1: each block takes a 2048-wide slice of one
-// (sequence, head) logit row and emits the slice's kmax best (value, id) pairs.
-// Level 2: one block per row merges the slices' candidates into the top-k and
-// writes the tree tokens of that head's level.  Level 1 picks k times the
-// block-wide best remaining pair (larger value, then lower id).
-constexpr int kSel = 256;        // threads per selection block
-constexpr int kPer = 8;          // pairs held per thread
-
-__device__ __forceinline__ void block_best(float &bv, int &bi, float *sv, int *si) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const float ov = __shfl_xor(bv, off);
-    const int oi = __shfl_xor(bi, off);
-    if (better(ov, oi, bv, bi)) {
-      bv = ov;
-      bi = oi;
-    }
-  }
-  if (lane == 0) {
-    sv[wave] = bv;
-    si[wave] = bi;
-  }
-  __syncthreads();
-  bv = sv[0];
-  bi = si[0];
-#pragma unroll
-  for (int w = 1; w < kSel / 64; ++w)
-    if (better(sv[w], si[w], bv, bi)) {
-      bv = sv[w];
-      bi = si[w];
-    }
-  __syncthreads();
-}
-
-// Emit the k best of the thread-held pairs, in order, to (ov, oi) by thread 0.
-__device__ __forceinline__ void select_k(float (&v)[kPer], int (&id)[kPer], int k, float *ov, int *oi) {
-  __shared__ float sv[kSel / 64];
-  __shared__ int si[kSel / 64];
-  for (int j = 0; j < k; ++j) {
-    float bv = -INFINITY;
-    int bi = INT32_MAX;
-#pragma unroll
-    for (int p = 0; p < kPer; ++p)
-      if (better(v[p], id[p], bv, bi)) {
-        bv = v[p];
-        bi = id[p];
-      }
-    block_best(bv, bi, sv, si);
-    if (threadIdx.x == 0) {
-      ov[j] = bv;
-      oi[j] = bi;
-    }
-#pragma unroll
-    for (int p = 0; p < kPer; ++p)       // ids are unique: only the winner's slot is cleared
-      if (id[p] == bi) {
-        v[p] = -INFINITY;
-        id[p] = INT32_MAX;
-      }
-  }
-}
-
-__global__ __launch_bounds__(kSel) void topk_partial(TopkArgs a) {
-  const int row = blockIdx.x / a.nsplit, split = blockIdx.x % a.nsplit;
-  const float *x = a.z + (int64_t)row * a.vocab;
-  float v[kPer];
-  int id[kPer];
-#pragma unroll
-  for (int p = 0; p < kPer; ++p) {
-    const int i = split * kSel * kPer + p * kSel + threadIdx.x;
-    const bool in = i < a.vocab;
-    v[p] = in ? x[i] : -INFINITY;
-    id[p] = in ? i : INT32_MAX;
-  }
-  const int64_t c0 = ((int64_t)row * a.nsplit + split) * a.kmax;
-  select_k(v, id, a.kmax, a.cand_v + c0, a.cand_i + c0);
-}
+// Top-k of one (sequence, head) logit row per block, in the order larger value
+// first, equal values by lower id.
+//  1. Every thread takes the max of its values.
+//  2. Each wave finds the k-th largest of its 64 thread maxima; T = the largest
+//     of these over the waves.  The wave attaining T holds k values >= T, so
+//     the row's k-th best value is >= T and every top-k value is >= T.
+//  3. Values >= T are gathered into LDS (a second pass over the row, which
+//     the first pass left in cache); a gathered value's output slot is the
+//     number of gathered values that beat it (values below T beat none).
+//  4. If ties at T overflow the buffer, the k picks are instead made in k
+//     rounds, each taking the best value worse than the previous pick.
+// The block of head i also writes the tree tokens of level i+1 (head 0: the
+// root token).
+constexpr int kTopkThreads = 1024;
+constexpr int kTopkCand = 2048;
 
 // Number of pairs among (cv, ci)[0..n) that beat (v, id).  The arrays are
 // 16-byte aligned and padded to a multiple of 4 with (-inf, INT32_MAX), which
@@ -333,50 +278,155 @@ __device__ __forceinline__ int count_better(const float *cv, const int *ci, int 
   return rank;
 }
 
-// Level 2 by rank counting: a candidate's output slot is the number of
-// candidates that beat it (ids are unique across slices), so the k winners
-// are placed in one pass without sequential selection rounds.
-__global__ __launch_bounds__(kSel) void topk_merge(TopkArgs a) {
+__global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
+  constexpr int kWavesT = kTopkThreads / 64;
   const int row = blockIdx.x;                 // b * n_heads + head
   const int b = row / a.n_heads, head = row % a.n_heads;
   const int k = a.k[head];
-  const int ncand = a.nsplit * a.kmax;
-  __shared__ __attribute__((aligned(16))) float cv[kTopkMaxCand + 4];
-  __shared__ __attribute__((aligned(16))) int ci[kTopkMaxCand + 4];
+  const int vocab = a.vocab;
+  const float *x = a.z + (int64_t)row * vocab;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ __attribute__((aligned(16))) float cv[kTopkCand + 4];
+  __shared__ __attribute__((aligned(16))) int ci[kTopkCand + 4];
+  __shared__ float wthr[kWavesT];
+  __shared__ float rbv[kWavesT];
+  __shared__ int rbi[kWavesT];
   __shared__ float selv[kMaxTopk];
   __shared__ int sel[kMaxTopk];
-  const int tid = threadIdx.x;
-  for (int i = tid; i < ncand; i += kSel) {
-    cv[i] = a.cand_v[(int64_t)row * ncand + i];
-    ci[i] = a.cand_i[(int64_t)row * ncand + i];
+  __shared__ int ncand;
+  if (tid == 0) ncand = 0;
+
+  // Rows start 16-byte aligned when vocab % 4 == 0: thread tid then reads the
+  // float4 groups tid, tid + 1024, ... (ids 4 g .. 4 g + 3); otherwise single
+  // floats tid, tid + 1024, ...
+  const bool vec = (vocab & 3) == 0;
+  const int ngrp = vec ? vocab >> 2 : vocab;
+  const float4 *x4 = reinterpret_cast<const float4 *>(x);
+
+  // 1. thread max
+  float mx = -INFINITY;
+  if (vec) {
+#pragma unroll 8
+    for (int g = tid; g < ngrp; g += kTopkThreads) {
+      const float4 q = x4[g];
+      mx = fmaxf(mx, fmaxf(fmaxf(q.x, q.y), fmaxf(q.z, q.w)));
+    }
+  } else {
+#pragma unroll 8
+    for (int v = tid; v < vocab; v += kTopkThreads) mx = fmaxf(mx, x[v]);
   }
-  if (tid < 4) {                              // pad to a multiple of 4 with pairs that beat nothing
-    cv[ncand + tid] = -INFINITY;
-    ci[ncand + tid] = INT32_MAX;
+  // 2. k-th largest thread max of the wave: k rounds of wave max, removing one
+  //    holder of the max each round
+  float kth = -INFINITY, cur = mx;
+  for (int j = 0; j < k; ++j) {
+    const float w = wave_max(cur);
+    kth = w;
+    const uint64_t holders = __builtin_amdgcn_ballot_w64(cur == w);
+    if (holders && lane == __builtin_ctzll(holders)) cur = -INFINITY;
+  }
+  if (lane == 0) wthr[wave] = kth;
+  __syncthreads();
+  float T = wthr[0];
+#pragma unroll
+  for (int w = 1; w < kWavesT; ++w) T = fmaxf(T, wthr[w]);
+
+  // 3. gather values >= T
+  auto gather = [&](float xv, int v) {
+    if (xv >= T) {
+      const int slot = atomicAdd(&ncand, 1);
+      if (slot < kTopkCand) {
+        cv[slot] = xv;
+        ci[slot] = v;
+      }
+    }
+  };
+  if (vec) {
+#pragma unroll 8
+    for (int g = tid; g < ngrp; g += kTopkThreads) {
+      const float4 q = x4[g];
+      if (fmaxf(fmaxf(q.x, q.y), fmaxf(q.z, q.w)) >= T) {
+        gather(q.x, 4 * g);
+        gather(q.y, 4 * g + 1);
+        gather(q.z, 4 * g + 2);
+        gather(q.w, 4 * g + 3);
+      }
+    }
+  } else {
+#pragma unroll 8
+    for (int v = tid; v < vocab; v += kTopkThreads) gather(x[v], v);
   }
   __syncthreads();
-  for (int i = tid; i < ncand; i += kSel) {
-    const float v = cv[i];
-    const int id = ci[i];
-    if (id == INT32_MAX) continue;            // empty slot of a short slice
-    const int rank = count_better(cv, ci, ncand, v, id);
-    if (rank < k) {
-      sel[rank] = id;
-      selv[rank] = v;
+  const int n = ncand;
+  if (n <= kTopkCand) {
+    if (tid < 4) {                            // pad to a multiple of 4 with pairs that beat nothing
+      cv[n + tid] = -INFINITY;
+      ci[n + tid] = INT32_MAX;
+    }
+    __syncthreads();
+    for (int i = tid; i < n; i += kTopkThreads) {
+      const int rank = count_better(cv, ci, n, cv[i], ci[i]);
+      if (rank < k) {
+        sel[rank] = ci[i];
+        selv[rank] = cv[i];
+      }
+    }
+  } else {
+    // 4. k rounds over the row: the best value worse than the previous pick
+    float pv = INFINITY;
+    int pi = -1;
+    for (int j = 0; j < k; ++j) {
+      float bv = -INFINITY;
+      int bi = INT32_MAX;
+      for (int v = tid; v < vocab; v += kTopkThreads) {
+        const float xv = x[v];
+        if (better(pv, pi, xv, v) && better(xv, v, bv, bi)) {
+          bv = xv;
+          bi = v;
+        }
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const float ov = __shfl_xor(bv, off);
+        const int oi = __shfl_xor(bi, off);
+        if (better(ov, oi, bv, bi)) {
+          bv = ov;
+          bi = oi;
+        }
+      }
+      if (lane == 0) {
+        rbv[wave] = bv;
+        rbi[wave] = bi;
+      }
+      __syncthreads();
+      bv = rbv[0];
+      bi = rbi[0];
+#pragma unroll
+      for (int w = 1; w < kWavesT; ++w)
+        if (better(rbv[w], rbi[w], bv, bi)) {
+          bv = rbv[w];
+          bi = rbi[w];
+        }
+      if (tid == 0) {
+        sel[j] = bi;
+        selv[j] = bv;
+      }
+      pv = bv;
+      pi = bi;
+      __syncthreads();
     }
   }
   __syncthreads();
   int32_t *ids = a.ids + (int64_t)row * a.kmax;
-  for (int j = tid; j < a.kmax; j += kSel) {
+  for (int j = tid; j < a.kmax; j += kTopkThreads) {
     ids[j] = j < k ? sel[j] : -1;
     if (a.vals) a.vals[(int64_t)row * a.kmax + j] = j < k ? selv[j] : -INFINITY;
   }
   const int n0 = a.node_off[b], n1 = a.node_off[b + 1];
-  for (int n = n0 + tid; n < n1; n += kSel) {
-    if (n == n0) {
-      if (head == 0) a.node_tok[n] = a.root_tok[b];
-    } else if (a.depth[n] == head + 1) {
-      a.node_tok[n] = sel[a.rank[n]];
+  for (int nn = n0 + tid; nn < n1; nn += kTopkThreads) {
+    if (nn == n0) {
+      if (head == 0) a.node_tok[nn] = a.root_tok[b];
+    } else if (a.depth[nn] == head + 1) {
+      a.node_tok[nn] = sel[a.rank[nn]];
     }
   }
 }
@@ -416,8 +466,7 @@ hipError_t launch_pack_heads(const void *src, void *dst, int n_heads, int vocab,
 }
 
 hipError_t launch_topk(const TopkArgs &a, int B, hipStream_t st) {
-  hipLaunchKernelGGL(topk_partial, dim3(B * a.n_heads * a.nsplit), dim3(kSel), 0, st, a);
-  hipLaunchKernelGGL(topk_merge, dim3(B * a.n_heads), dim3(kSel), 0, st, a);
+  hipLaunchKernelGGL(topk_rows, dim3(B * a.n_heads), dim3(kTopkThreads), 0, st, a);
   return hipGetLastError();
 }
 

@@ -246,6 +246,36 @@ def test_edge_parity(torch_cuda, name):
     run_parity(torch_cuda, wl, label=name, pack_heads=name not in ROWMAJOR_HEADS)
 
 
+def test_topk_ties(torch_cuda):
+    """Integer-valued heads and hidden states give exact fp32 logits with many
+    ties: head 0 is all zeros (every logit ties; the candidate buffer
+    overflows), head 1 has entries in {-1, 0, 1}, head 2 is Gaussian, head 3
+    puts a few large values over a flat floor.  Ids must equal the oracle's
+    exactly (equal values by lower id), for both head layouts."""
+    from paper_2506_01986_amd import runner
+    cfg = edge_cfg(B=3, n_q=8, n_kv=1, hidden=64, vocab=5000, topk=(10, 10, 10, 10), seed=5)
+    wl = synth.make(cfg, trees=[synth.t64()] * 3, lens=[10, 20, 30])
+    rng = np.random.default_rng(5)
+    w = np.zeros((4, cfg.vocab, cfg.hidden), np.float32)
+    w[1] = rng.integers(-1, 2, size=(cfg.vocab, cfg.hidden))
+    w[2] = np.round(rng.standard_normal((cfg.vocab, cfg.hidden)) * 4)
+    w[3] = -1.0
+    w[3, rng.choice(cfg.vocab, 40, replace=False)] = 3.0
+    h = rng.integers(-1, 2, size=(cfg.B, cfg.hidden)).astype(np.float32)
+    h[:, 0] = 1.0
+    wl.head_w = synth.to_bf16_bits(w)
+    wl.hidden = synth.to_bf16_bits(h)
+    z64 = oracle.head_logits(wl.hidden, wl.head_w)
+    ids64, _ = oracle.heads_topk(z64, cfg.topk, cfg.kmax)
+    for pack in (True, False):
+        step = runner.VerifyStep(wl, keep_logits=True, pack_heads=pack)
+        step.medusa_topk()
+        torch_cuda.cuda.synchronize()
+        assert np.array_equal(step.logits.cpu().numpy(), z64.astype(np.float32))
+        assert np.array_equal(step.topk_ids.cpu().numpy(), ids64), pack
+        assert np.array_equal(step.topk_ids.cpu().numpy()[:, 0], np.tile(np.arange(10), (3, 1)))
+
+
 def test_pack_heads_layout(torch_cuda):
     """The packed buffer holds head_w[i][64 G + 16 t + l % 16][32 s + 8 (l / 16) + e]
     at element ((((i nG + G) nS + s) 4 + t) 64 + l) 8 + e, zero past vocab and hidden."""
