@@ -33,7 +33,7 @@ METRIC = "verified tree tokens/sec per verify step; achieved HBM GB/s vs peak"
 # Kernels each stage launches through the C ABI (for matching rocprofv3 traces).
 STAGE_KERNELS = {"medusa_topk": ["head_logits_packed", "topk_rows"],
                  "tree_attn": ["tree_attn_bf16", "tree_attn_combine"],
-                 "accept": ["accept_greedy"], "kv_compact": ["kv_compact_kernel"]}
+                 "accept": ["row_argbest_all", "accept_walk"], "kv_compact": ["kv_compact_kernel"]}
 STAGE_SOURCES = {"medusa_topk": "medusa_topk.hip", "tree_attn": "tree_attn.hip",
                  "accept": "accept.hip", "kv_compact": "kv_compact.hip"}
 

@@ -187,7 +187,8 @@ int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmem
  * is always accepted; tau = accept_len + 1); path[B][path_stride] = local
  * node ids root..chosen, -1 padded, path_stride >= max tree depth + 1;
  * next_tok[B] = argmax of the chosen node's row (ties: lower id).
- * ws: SPECMEMO_WS_ACCEPT bytes (0 in greedy mode). */
+ * ws: SPECMEMO_WS_ACCEPT bytes (greedy: one int32 per node; typical: two
+ * floats per node). */
 int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab,
                     specmemo_accept_mode mode, float temperature, float eps, float delta,
                     const void *base_logits, const int32_t *node_tok, int32_t *accept_len,

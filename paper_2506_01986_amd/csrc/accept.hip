@@ -5,12 +5,11 @@
 // accepted; Medusa verifies with typical sampling.  Sec. 3.2: verification of a
 // continuation is cumulative.
 //
-// Greedy mode walks the tree from the root and scans only the logit rows of
-// nodes on the accepted path (at most depth + 1 rows per sequence instead of
-// all N rows), so the per-candidate retrieval buffers of the paper's memory
-// model (Eq. 3, second and third terms) are never materialised.  Typical mode
-// needs every node's softmax statistics: one block per row computes them, then
-// one block per sequence evaluates the edges and picks the path.
+// Greedy mode takes the arg-best token of every node's row in one parallel
+// pass (one block per row) and then walks each tree from the root; the walk
+// has no dependent row loads, only one token per node crosses to it.  Typical
+// mode needs every node's softmax statistics: one block per row computes
+// them, then one block per sequence evaluates the edges and picks the path.
 #include "device.h"
 #include "internal.h"
 
@@ -83,15 +82,7 @@ __device__ void row_argbest(const void *logits, int64_t row, int vocab, float *s
       }
     }
   }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    float ov = __shfl_xor(bv, off);
-    int oi = __shfl_xor(bi, off);
-    if (better(ov, oi, bv, bi)) {
-      bv = ov;
-      bi = oi;
-    }
-  }
+  wave_argbest(bv, bi);
   if (lane == 0) {
     sv[wave] = bv;
     si[wave] = bi;
@@ -110,46 +101,49 @@ __device__ void row_argbest(const void *logits, int64_t row, int vocab, float *s
   out_i = bi;
 }
 
+// Greedy mode, pass 1: the arg-best token of every node's logit row, all rows
+// at once (the walk of pass 2 then has no dependent row loads).
 template <int DT>
-__global__ __launch_bounds__(kNT) void accept_greedy(AcceptArgs a) {
+__global__ __launch_bounds__(kNT) void row_argbest_all(AcceptArgs a) {
   __shared__ float sv[kWaves];
   __shared__ int si[kWaves];
-  __shared__ int s_par[kMaxNodes], s_tok[kMaxNodes];
-  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  float v;
+  int tok;
+  row_argbest<DT>(a.logits, blockIdx.x, a.vocab, sv, si, v, tok);
+  if (threadIdx.x == 0) a.best[blockIdx.x] = tok;
+}
+
+// Greedy mode, pass 2: one wave per sequence walks from the root to the child
+// carrying the current node's arg-best token (unique: sibling tokens differ),
+// with the tree's parents, tokens and arg-best tokens in LDS (at most
+// kMaxNodes = 128 nodes, two per lane).
+__global__ __launch_bounds__(64) void accept_walk(AcceptArgs a) {
+  __shared__ int s_par[kMaxNodes], s_tok[kMaxNodes], s_best[kMaxNodes];
+  const int b = blockIdx.x, lane = threadIdx.x;
   const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
-  // The tree's parents and tokens go to LDS once (visible after the first
-  // barrier inside row_argbest); each wave then finds the next node itself.
-  for (int n = tid; n < N; n += kNT) {
+  for (int n = lane; n < N; n += 64) {
     s_par[n] = n == 0 ? -1 : a.parent[n0 + n];
     s_tok[n] = a.node_tok[n0 + n];
+    s_best[n] = a.best[n0 + n];
   }
-  int cur = 0, len = 0, tok = 0;
-  int path[kMaxPath];
-  path[0] = 0;
+  __syncthreads();
+  int cur = 0, len = 0, p_mine = lane == 0 ? 0 : -1;   // lane j keeps path entry j
   for (;;) {
-    float v;
-    row_argbest<DT>(a.logits, n0 + cur, a.vocab, sv, si, v, tok);
-    // the child of cur carrying tok (unique: sibling tokens differ), by ballot
-    // over the (at most kMaxNodes = 128) nodes, two per lane
+    const int tok = s_best[cur];
     const bool m0 = lane < N && s_par[lane] == cur && s_tok[lane] == tok;
     const bool m1 = lane + 64 < N && s_par[lane + 64] == cur && s_tok[lane + 64] == tok;
     const uint64_t b0 = __builtin_amdgcn_ballot_w64(m0), b1 = __builtin_amdgcn_ballot_w64(m1);
     const int nxt = b0 ? (int)__builtin_ctzll(b0) : b1 ? 64 + (int)__builtin_ctzll(b1) : -1;
     if (nxt < 0 || len + 1 >= kMaxPath) break;
     cur = nxt;
-    path[++len] = cur;
+    ++len;
+    if (lane == len) p_mine = cur;
   }
-  if (tid == 0) {
+  if (lane == 0) {
     a.accept_len[b] = len;
-    a.next_tok[b] = tok;
+    a.next_tok[b] = s_best[cur];
   }
-  for (int j = tid; j < a.path_stride; j += kNT) {
-    int p = -1;
-#pragma unroll
-    for (int i = 0; i < kMaxPath; ++i)
-      if (i == j && i <= len) p = path[i];
-    a.path[(int64_t)b * a.path_stride + j] = p;
-  }
+  for (int j = lane; j < a.path_stride; j += 64) a.path[(int64_t)b * a.path_stride + j] = j < 64 ? p_mine : -1;
 }
 
 // Typical mode, pass 1: per row u, x = z_u / T: lse_u = log sum exp x and
@@ -263,9 +257,10 @@ __global__ __launch_bounds__(kNT) void accept_typical(AcceptArgs a) {
 hipError_t launch_accept(int dt, const AcceptArgs &a, int total_nodes, hipStream_t st) {
   if (a.mode == 0) {
     if (dt == 1)
-      hipLaunchKernelGGL(accept_greedy<1>, dim3(a.B), dim3(kNT), 0, st, a);
+      hipLaunchKernelGGL(row_argbest_all<1>, dim3(total_nodes), dim3(kNT), 0, st, a);
     else
-      hipLaunchKernelGGL(accept_greedy<0>, dim3(a.B), dim3(kNT), 0, st, a);
+      hipLaunchKernelGGL(row_argbest_all<0>, dim3(total_nodes), dim3(kNT), 0, st, a);
+    hipLaunchKernelGGL(accept_walk, dim3(a.B), dim3(64), 0, st, a);
   } else {
     if (dt == 1) {
       hipLaunchKernelGGL(row_softmax_stats<1>, dim3(total_nodes), dim3(256), 0, st, a);

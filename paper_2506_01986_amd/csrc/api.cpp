@@ -307,7 +307,8 @@ size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo
     return p.ws_bytes;
   }
   if (which == SPECMEMO_WS_ACCEPT) {
-    return n_q_or_heads == SPECMEMO_ACCEPT_TYPICAL ? (size_t)ti.total * 2 * sizeof(float) : 0;
+    return n_q_or_heads == SPECMEMO_ACCEPT_TYPICAL ? (size_t)ti.total * 2 * sizeof(float)
+                                                   : (size_t)ti.total * sizeof(int32_t);
   }
   return 0;
 }
@@ -482,6 +483,11 @@ int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, s
     a.inv_temp = 1.0f / temperature;
     a.log_eps = std::log(eps);
     a.log_delta = std::log(delta);
+  } else {
+    const size_t need = (size_t)ti.total * sizeof(int32_t);
+    if (!al(ws, 16) || ws_bytes < need)
+      return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
+    a.best = static_cast<int32_t *>(ws);
   }
   return hip_status(launch_accept(dt, a, ti.total, static_cast<hipStream_t>(stream)), "acceptance launch");
 }

@@ -64,6 +64,43 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 // Larger value first; equal values by lower id.
+__device__ __forceinline__ bool better(float va, int ia, float vb, int ib);
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xF, 0xF, false);
+}
+
+// Best (value, id) pair over the 64 lanes of a wave, in every lane: the same
+// DPP / permlane steps as wave_max, moving both halves of the pair.
+__device__ __forceinline__ void wave_argbest(float &v, int &id) {
+  auto step = [&](float ov, int oi) {
+    if (better(ov, oi, v, id)) {
+      v = ov;
+      id = oi;
+    }
+  };
+  step(dpp_f<0xB1>(v), dpp_i<0xB1>(id));
+  step(dpp_f<0x4E>(v), dpp_i<0x4E>(id));
+  step(dpp_f<0x141>(v), dpp_i<0x141>(id));
+  step(dpp_f<0x140>(v), dpp_i<0x140>(id));
+  {
+    const auto rv = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    const auto ri = __builtin_amdgcn_permlane16_swap((uint32_t)id, (uint32_t)id, false, false);
+    v = __uint_as_float(rv[0]);
+    id = (int)ri[0];
+    step(__uint_as_float(rv[1]), (int)ri[1]);
+  }
+  {
+    const auto rv = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    const auto ri = __builtin_amdgcn_permlane32_swap((uint32_t)id, (uint32_t)id, false, false);
+    v = __uint_as_float(rv[0]);
+    id = (int)ri[0];
+    step(__uint_as_float(rv[1]), (int)ri[1]);
+  }
+}
+
+// Larger value first; equal values by lower id.
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }

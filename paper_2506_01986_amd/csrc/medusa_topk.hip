@@ -247,11 +247,10 @@ __global__ __launch_bounds__(256) void head_logits_f32(const float *__restrict__
 // Top-k of one (sequence, head) logit row per block, in the order larger value
 // first, equal values by lower id.
 //  1. Every thread takes the max of its values.
-//  2. Each wave finds the k-th largest of its 64 thread maxima; T = the largest
-//     of these over the waves.  The wave attaining T holds k values >= T, so
-//     the row's k-th best value is >= T and every top-k value is >= T.
-//  3. Values >= T are gathered into LDS (a second pass over the row, which
-//     the first pass left in cache); a gathered value's output slot is the
+//  2. T = the k-th largest maximum of 64 groups of 16 threads: k groups hold a
+//     value >= T, so the row's k-th best value is >= T and every top-k value
+//     is >= T.
+//  3. Values >= T are gathered into LDS; a gathered value's output slot is the
 //     number of gathered values that beat it (values below T beat none).
 //  4. If ties at T overflow the buffer, the k picks are instead made in k
 //     rounds, each taking the best value worse than the previous pick.
@@ -259,24 +258,8 @@ __global__ __launch_bounds__(256) void head_logits_f32(const float *__restrict__
 // root token).
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkCand = 2048;
-
-// Number of pairs among (cv, ci)[0..n) that beat (v, id).  The arrays are
-// 16-byte aligned and padded to a multiple of 4 with (-inf, INT32_MAX), which
-// beats nothing; reads are 4 pairs wide and unrolled so LDS latency overlaps.
-__device__ __forceinline__ int count_better(const float *cv, const int *ci, int n, float v, int id) {
-  const float4 *cv4 = reinterpret_cast<const float4 *>(cv);
-  const int4 *ci4 = reinterpret_cast<const int4 *>(ci);
-  int rank = 0;
-  const int n4 = (n + 3) >> 2;
-#pragma unroll 8
-  for (int j = 0; j < n4; ++j) {
-    const float4 a4 = cv4[j];
-    const int4 b4 = ci4[j];
-    rank += (better(a4.x, b4.x, v, id) ? 1 : 0) + (better(a4.y, b4.y, v, id) ? 1 : 0) +
-            (better(a4.z, b4.z, v, id) ? 1 : 0) + (better(a4.w, b4.w, v, id) ? 1 : 0);
-  }
-  return rank;
-}
+constexpr int kTopkU = 8;            // float4 groups per thread per batch
+constexpr int kTopkGroups = kTopkThreads / 16;   // 16-thread groups for the threshold
 
 __global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
   constexpr int kWavesT = kTopkThreads / 64;
@@ -288,7 +271,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   __shared__ __attribute__((aligned(16))) float cv[kTopkCand + 4];
   __shared__ __attribute__((aligned(16))) int ci[kTopkCand + 4];
-  __shared__ float wthr[kWavesT];
+  __shared__ float gmax[kTopkGroups];
+  __shared__ float thr;
   __shared__ float rbv[kWavesT];
   __shared__ int rbi[kWavesT];
   __shared__ float selv[kMaxTopk];
@@ -296,39 +280,63 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
   __shared__ int ncand;
   if (tid == 0) ncand = 0;
 
-  // Rows start 16-byte aligned when vocab % 4 == 0: thread tid then reads the
-  // float4 groups tid, tid + 1024, ... (ids 4 g .. 4 g + 3); otherwise single
-  // floats tid, tid + 1024, ...
+  // This sequence's tree fields for the level this head fills (fetched now so
+  // their latency overlaps the row scan).
+  const int n0 = a.node_off[b], n1 = a.node_off[b + 1];
+  int my_depth = 0, my_rank = 0;
+  if (n0 + tid < n1) {
+    my_depth = a.depth[n0 + tid];
+    my_rank = a.rank[n0 + tid];
+  }
+
+  // The row is read in batches of kTopkU groups per thread, all loads of a
+  // batch in flight together; a group is a float4 (ids 4 g .. 4 g + 3) when
+  // rows start 16-byte aligned (vocab % 4 == 0), else one float.  A row of one
+  // batch (vocab <= 4 * 1024 * kTopkU) stays in registers for the gather.
   const bool vec = (vocab & 3) == 0;
   const int ngrp = vec ? vocab >> 2 : vocab;
   const float4 *x4 = reinterpret_cast<const float4 *>(x);
+  constexpr float NEG = -INFINITY;
+  float4 q[kTopkU];
+  auto load_batch = [&](int g0) {
+#pragma unroll
+    for (int u = 0; u < kTopkU; ++u) {
+      const int g = g0 + u * kTopkThreads + tid;
+      q[u] = g < ngrp ? (vec ? x4[g] : float4{x[g], NEG, NEG, NEG}) : float4{NEG, NEG, NEG, NEG};
+    }
+  };
+  constexpr int kBatch = kTopkU * kTopkThreads;
 
   // 1. thread max
-  float mx = -INFINITY;
-  if (vec) {
-#pragma unroll 8
-    for (int g = tid; g < ngrp; g += kTopkThreads) {
-      const float4 q = x4[g];
-      mx = fmaxf(mx, fmaxf(fmaxf(q.x, q.y), fmaxf(q.z, q.w)));
-    }
-  } else {
-#pragma unroll 8
-    for (int v = tid; v < vocab; v += kTopkThreads) mx = fmaxf(mx, x[v]);
-  }
-  // 2. k-th largest thread max of the wave: k rounds of wave max, removing one
-  //    holder of the max each round
-  float kth = -INFINITY, cur = mx;
-  for (int j = 0; j < k; ++j) {
-    const float w = wave_max(cur);
-    kth = w;
-    const uint64_t holders = __builtin_amdgcn_ballot_w64(cur == w);
-    if (holders && lane == __builtin_ctzll(holders)) cur = -INFINITY;
-  }
-  if (lane == 0) wthr[wave] = kth;
-  __syncthreads();
-  float T = wthr[0];
+  float mx = NEG;
+  for (int g0 = 0; g0 < ngrp; g0 += kBatch) {
+    load_batch(g0);
 #pragma unroll
-  for (int w = 1; w < kWavesT; ++w) T = fmaxf(T, wthr[w]);
+    for (int u = 0; u < kTopkU; ++u) mx = fmaxf(mx, fmaxf(fmaxf(q[u].x, q[u].y), fmaxf(q[u].z, q[u].w)));
+  }
+  // 2. T = the k-th largest of the 64 maxima of 16-thread groups (one DPP row
+  //    each, 512 values per group at 32 values per thread): k groups hold a
+  //    value >= T, so the row's k-th best value is >= T.
+  {
+    float gm = fmaxf(mx, dpp_f<0xB1>(mx));
+    gm = fmaxf(gm, dpp_f<0x4E>(gm));
+    gm = fmaxf(gm, dpp_f<0x141>(gm));
+    gm = fmaxf(gm, dpp_f<0x140>(gm));
+    if ((lane & 15) == 0) gmax[tid >> 4] = gm;
+  }
+  __syncthreads();
+  if (tid < kTopkGroups) {
+    const float g = gmax[tid];
+    int above = 0;                    // groups whose max beats this one (ties by group index)
+#pragma unroll 8
+    for (int j = 0; j < kTopkGroups; ++j) {
+      const float o = gmax[j];
+      above += (o > g || (o == g && j < tid)) ? 1 : 0;
+    }
+    if (above == k - 1) thr = g;
+  }
+  __syncthreads();
+  const float T = thr;
 
   // 3. gather values >= T
   auto gather = [&](float xv, int v) {
@@ -340,34 +348,41 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
       }
     }
   };
-  if (vec) {
-#pragma unroll 8
-    for (int g = tid; g < ngrp; g += kTopkThreads) {
-      const float4 q = x4[g];
-      if (fmaxf(fmaxf(q.x, q.y), fmaxf(q.z, q.w)) >= T) {
-        gather(q.x, 4 * g);
-        gather(q.y, 4 * g + 1);
-        gather(q.z, 4 * g + 2);
-        gather(q.w, 4 * g + 3);
+  for (int g0 = 0; g0 < ngrp; g0 += kBatch) {
+    if (ngrp > kBatch) load_batch(g0);   // one batch: still in registers
+#pragma unroll
+    for (int u = 0; u < kTopkU; ++u) {
+      const int g = g0 + u * kTopkThreads + tid;
+      if (fmaxf(fmaxf(q[u].x, q[u].y), fmaxf(q[u].z, q[u].w)) >= T) {
+        if (vec) {
+          gather(q[u].x, 4 * g);
+          gather(q[u].y, 4 * g + 1);
+          gather(q[u].z, 4 * g + 2);
+          gather(q[u].w, 4 * g + 3);
+        } else {
+          gather(q[u].x, g);
+        }
       }
     }
-  } else {
-#pragma unroll 8
-    for (int v = tid; v < vocab; v += kTopkThreads) gather(x[v], v);
   }
   __syncthreads();
   const int n = ncand;
   if (n <= kTopkCand) {
-    if (tid < 4) {                            // pad to a multiple of 4 with pairs that beat nothing
-      cv[n + tid] = -INFINITY;
-      ci[n + tid] = INT32_MAX;
-    }
-    __syncthreads();
-    for (int i = tid; i < n; i += kTopkThreads) {
-      const int rank = count_better(cv, ci, n, cv[i], ci[i]);
-      if (rank < k) {
-        sel[rank] = ci[i];
-        selv[rank] = cv[i];
+    // rank of candidate c = number of candidates that beat it, counted by one
+    // wave (candidates c = wave, wave + 16, ...) with a ballot per 64
+    for (int c = wave; c < n; c += kWavesT) {
+      const float v = cv[c];
+      const int id = ci[c];
+      int rank = 0;
+      for (int j0 = 0; j0 < n; j0 += 64) {
+        const int j = j0 + lane;
+        const int jr = j < n ? j : 0;
+        const bool beats = j < n && better(cv[jr], ci[jr], v, id);
+        rank += __builtin_popcountll(__builtin_amdgcn_ballot_w64(beats));
+      }
+      if (lane == 0 && rank < k) {
+        sel[rank] = id;
+        selv[rank] = v;
       }
     }
   } else {
@@ -384,15 +399,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
           bi = v;
         }
       }
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) {
-        const float ov = __shfl_xor(bv, off);
-        const int oi = __shfl_xor(bi, off);
-        if (better(ov, oi, bv, bi)) {
-          bv = ov;
-          bi = oi;
-        }
-      }
+      wave_argbest(bv, bi);
       if (lane == 0) {
         rbv[wave] = bv;
         rbi[wave] = bi;
@@ -421,12 +428,11 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
     ids[j] = j < k ? sel[j] : -1;
     if (a.vals) a.vals[(int64_t)row * a.kmax + j] = j < k ? selv[j] : -INFINITY;
   }
-  const int n0 = a.node_off[b], n1 = a.node_off[b + 1];
-  for (int nn = n0 + tid; nn < n1; nn += kTopkThreads) {
-    if (nn == n0) {
-      if (head == 0) a.node_tok[nn] = a.root_tok[b];
-    } else if (a.depth[nn] == head + 1) {
-      a.node_tok[nn] = sel[a.rank[nn]];
+  if (n0 + tid < n1) {                        // trees have at most kMaxNodes <= 1024 nodes
+    if (tid == 0) {
+      if (head == 0) a.node_tok[n0] = a.root_tok[b];
+    } else if (my_depth == head + 1) {
+      a.node_tok[n0 + tid] = sel[my_rank];
     }
   }
 }

@@ -148,7 +148,10 @@ def test_workspace_errors_and_sizes():
     assert need >= 1 * 3 * 1000 * 4                           # the fp32 logits
     expect("E_WORKSPACE", topk, t, ws_bytes=1 * 3 * 1000 * 4 - 4)
     assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.TYPICAL, 0) == 16 * 2 * 4
-    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.GREEDY, 0) == 0
+    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.GREEDY, 0) == 16 * 4
+    with pytest.raises(sm.SpecmemoError) as e:       # greedy keeps one arg-best token per node
+        sm.accept(sm.BF16, t, 1000, sm.GREEDY, FAKE, FAKE, FAKE, FAKE, 4, FAKE, ws=FAKE, ws_bytes=60, stream=0)
+    assert e.value.name == "E_WORKSPACE"
     # a long sequence alone on the device is split along its KV range: partials need workspace
     big = FakeTrees([synth.t64()])
     kv = FakeKV([100000], [100064], [0], n_kv=1, d=128)

@@ -333,7 +333,8 @@ def test_acceptance_small_vocab_random(torch_cuda):
         out = [torch.empty(B, dtype=torch.int32, device="cuda"), torch.empty((B, stride), dtype=torch.int32, device="cuda"),
                torch.empty(B, dtype=torch.int32, device="cuda")]
         dt = sm.FP32 if dtype == "fp32" else sm.BF16
-        sm.accept(dt, tr, vocab, sm.GREEDY, dlg, dtok, out[0], out[1], stride, out[2])
+        wsg = torch.empty(sm.workspace_bytes(sm.WS_ACCEPT, dt, tr, None, sm.GREEDY), dtype=torch.uint8, device="cuda")
+        sm.accept(dt, tr, vocab, sm.GREEDY, dlg, dtok, out[0], out[1], stride, out[2], ws=wsg, ws_bytes=wsg.numel())
         ra, rp, rn = oracle.accept_greedy(lg, tok, node_off, parent, depth, stride)
         assert np.array_equal(out[0].cpu().numpy(), ra)
         assert np.array_equal(out[1].cpu().numpy(), rp)
