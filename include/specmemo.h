@@ -162,7 +162,8 @@ size_t specmemo_packed_heads_bytes(specmemo_dtype dt, int32_t n_heads, int32_t v
  *           path root..n (inclusive)
  *   out[node][hq] = softmax(scale * q[node][hq] . K[kv][key]) . V[kv][key]
  * q, out: device [sum N_b][n_q][head_dim] in `dt`.  scale <= 0 selects
- * 1/sqrt(head_dim).  bf16 requires head_dim == 128; fp32 requires
+ * 1/sqrt(head_dim).  bf16 requires head_dim == 128 and seq_cap[b] <= 2^23
+ * rows (else SPECMEMO_E_BUDGET); fp32 requires
  * head_dim <= 128 and head_dim % 4 == 0.  n_q % n_kv == 0.  Rows of the slab
  * past L_b + N_b are never read.  ws: at least
  * specmemo_workspace_bytes(SPECMEMO_WS_ATTN, ...) bytes (may be 0). */

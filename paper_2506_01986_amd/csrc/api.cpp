@@ -128,6 +128,7 @@ int hip_status(hipError_t e, const char *what) {
 }
 
 // ---- tree attention planning ------------------------------------------------------
+constexpr int kMaxSlabRows = 1 << 23;   // bf16 attention: slab bytes below 2^31
 constexpr int kMinChunk = 256;      // fewest keys per chunk when splitting the KV range
 
 // Tuning overrides (they change the work split, never the result beyond
@@ -144,6 +145,7 @@ struct AttnPlan {
   bool xcd_order = true;
   std::vector<std::vector<AttnSeq>> groups;   // sequences per launch, in launch order
   std::vector<int> items, citems;
+  std::vector<std::vector<int>> xcd_cum;      // per launch: [8][nseq + 1]
   size_t ws_bytes = 0;
 };
 
@@ -244,7 +246,10 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
     });
     int item = 0, part = 0, citem = 0, unit = 0;
     int per_xcd[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (AttnSeq &s : grp) {
+    std::vector<int> cum(8 * (grp.size() + 1), 0);
+    for (size_t si = 0; si < grp.size(); ++si) {
+      AttnSeq &s = grp[si];
+      for (int x = 0; x < 8; ++x) cum[x * (grp.size() + 1) + si] = per_xcd[x];
       s.item0 = item;
       s.unit0 = unit;
       const int units = kv->n_kv * s.nch;
@@ -261,6 +266,8 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
         s.citem0 = -1;
       }
     }
+    for (int x = 0; x < 8; ++x) cum[x * (grp.size() + 1) + grp.size()] = per_xcd[x];
+    p->xcd_cum.push_back(cum);
     p->groups.push_back(grp);
     // XCD order: XCD x runs units x, x + 8, ... (all their row blocks); the grid
     // is padded to 8 x the busiest XCD's blocks, surplus blocks exit at once.
@@ -280,6 +287,10 @@ int check_attn_args(int dt, const specmemo_trees *t, const specmemo_kv *kv, int 
   if ((rc = check_trees(t, ti))) return rc;
   if ((rc = check_kv(dt, kv, *ti, t->node_off_h))) return rc;
   if (n_q < 1 || n_q % kv->n_kv) return fail(SPECMEMO_E_ARG, "n_q=%d must be a positive multiple of n_kv=%d", n_q, kv->n_kv);
+  if (dt == SPECMEMO_BF16)
+    for (int b = 0; b < ti->B; ++b)    // tile loads address a slab with 32-bit byte offsets
+      if (kv->seq_cap_h[b] > kMaxSlabRows)
+        return fail(SPECMEMO_E_BUDGET, "seq_cap[%d]=%d exceeds %d rows", b, kv->seq_cap_h[b], kMaxSlabRows);
   return SPECMEMO_OK;
 }
 
@@ -440,6 +451,8 @@ int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmem
     a.items = p.items[gi];
     a.citems = p.citems[gi];
     a.xcd_order = p.xcd_order ? 1 : 0;
+    for (int x = 0; x < 8; ++x)
+      for (int i = 0; i <= a.nseq; ++i) a.xcd_cum[x][i] = p.xcd_cum[gi][x * (a.nseq + 1) + i];
     hipError_t e = launch_tree_attn_bf16(a, p.rb, st);
     if (e != hipSuccess) return hip_status(e, "tree attention launch");
   }

@@ -59,8 +59,12 @@ struct AttnArgs {
   float scale;
   int32_t nseq, items, citems;   // items: blocks of the launch (XCD order: padded)
   int32_t xcd_order;        // nonzero: consecutive work items share an XCD
+  int32_t xcd_cum[8][kMaxSeqPerLaunch + 1];   // XCD order: blocks of XCD x before sequence s
   AttnSeq seq[kMaxSeqPerLaunch];
 };
+
+static_assert(sizeof(AttnArgs) <= 4096, "kernel arguments are limited to 4 KB");
+static_assert(kMaxSeqPerLaunch <= 64, "one wave searches the sequences of a launch");
 
 constexpr int kAttnKeyTile = 64;
 constexpr int kAttnHeadDim = 128;

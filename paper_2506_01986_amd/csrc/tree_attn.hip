@@ -39,10 +39,19 @@ struct Item {
   int s, kvh, rb, ch;
 };
 
+// The sequence of a block is found by one wave-parallel search: lane l reads
+// sequence l's start (the launch holds at most 64 sequences) and a ballot
+// counts the starts at or below the block's position.
+__device__ __forceinline__ int find_seq(int nseq, int start_of_lane, int pos) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t le = __builtin_amdgcn_ballot_w64(lane < nseq && start_of_lane <= pos);
+  return __builtin_popcountll(le) - 1;
+}
+
 // Work items in launch order: sequence, then KV head, chunk, row block.
 __device__ __forceinline__ Item decode_item(const AttnArgs &a, int idx) {
-  int s = 0;
-  while (s + 1 < a.nseq && a.seq[s + 1].item0 <= idx) ++s;
+  const int lane = threadIdx.x & 63;
+  const int s = find_seq(a.nseq, lane < a.nseq ? a.seq[lane].item0 : 0, idx);
   const AttnSeq &S = a.seq[s];
   int local = idx - S.item0;
   Item it;
@@ -58,27 +67,24 @@ __device__ __forceinline__ Item decode_item(const AttnArgs &a, int idx) {
 // 8 k + x is the k-th block of XCD x.  A unit is one (sequence, KV head,
 // chunk) with all its row blocks, which read the same K/V; unit u (launch
 // order, longest sequences first) runs on XCD u mod 8, so those row blocks
-// share one L2 and every XCD gets long and short units alike.  Returns false
-// for the padding blocks past the busiest XCD's work.
+// share one L2 and every XCD gets long and short units alike.  xcd_cum[x][s]
+// is the number of XCD x's blocks before sequence s.  Returns false for the
+// padding blocks past the busiest XCD's work.
 __device__ __forceinline__ bool decode_item_xcd(const AttnArgs &a, int bid, Item &it) {
-  const int x = bid & 7;
-  int k = bid >> 3;
-  for (int s = 0; s < a.nseq; ++s) {
-    const AttnSeq &S = a.seq[s];
-    const int u0 = S.unit0, nu = a.n_kv * S.nch;
-    const int first = u0 + ((x - (u0 & 7)) & 7);            // first unit >= u0 on XCD x
-    const int cnt = first < u0 + nu ? (u0 + nu - 1 - first) / 8 + 1 : 0;
-    if (k < cnt * S.nrb) {
-      const int u = first + 8 * (k / S.nrb) - u0;
-      it.s = s;
-      it.rb = k % S.nrb;
-      it.ch = u % S.nch;
-      it.kvh = u / S.nch;
-      return true;
-    }
-    k -= cnt * S.nrb;
-  }
-  return false;
+  const int lane = threadIdx.x & 63;
+  const int x = bid & 7, k = bid >> 3;
+  if (k >= a.xcd_cum[x][a.nseq]) return false;
+  const int s = find_seq(a.nseq, lane < a.nseq ? a.xcd_cum[x][lane] : 0, k);
+  const AttnSeq &S = a.seq[s];
+  const int kk = k - a.xcd_cum[x][s];
+  const int u0 = S.unit0;
+  const int first = u0 + ((x - (u0 & 7)) & 7);            // first unit >= u0 on XCD x
+  const int u = first + 8 * (kk / S.nrb) - u0;
+  it.s = s;
+  it.rb = kk % S.nrb;
+  it.ch = u % S.nch;
+  it.kvh = u / S.nch;
+  return true;
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -86,12 +92,13 @@ typedef short s16x4_t __attribute__((__vector_size__(8)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 // 16-byte direct load of every lane into LDS at lds_base + 16 * lane (one
-// global_load_lds_dwordx4 with M0 = lds_base, which must be wave-uniform).  It
-// is issued from inline assembly so that the compiler does not guard later LDS
-// reads with waits for it: the tile ring orders these loads with explicit
-// vmcnt waits.  M0 must be written one wait state before the load.
-__device__ __forceinline__ void lds_load16(const void *src, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_base)
+// global_load_lds_dwordx4 with M0 = lds_base, which must be wave-uniform),
+// from the wave-uniform base `src` (SGPRs) plus this lane's 32-bit byte
+// offset.  It is issued from inline assembly so that the compiler does not
+// guard later LDS reads with waits for it: the tile ring orders these loads
+// with explicit vmcnt waits.  M0 must be written one wait state before the load.
+__device__ __forceinline__ void lds_load16(const void *src, uint32_t off, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(src), "s"(lds_base)
                : "memory", "m0");
 }
 
@@ -121,7 +128,7 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   constexpr int IPW = TILE / 1024 / WAVES;    // 1 KB direct loads per wave per tile and operand
   __shared__ __attribute__((aligned(1024))) uint8_t kring[SLOTS][TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t vring[SLOTS][TILE];
-  __shared__ uint32_t anc[kMaxNodes][4];
+  __shared__ __attribute__((aligned(16))) uint32_t anc[kMaxNodes][4];
 
   Item it;
   if (a.xcd_order) {
@@ -179,37 +186,42 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   const uint16_t *Vg = static_cast<const uint16_t *>(a.v) + ((int64_t)it.kvh * a.cap_total + S.base) * D;
 
   // Direct loads of a tile into its ring slot: lane l of load i writes LDS bytes
-  // [1024 i + 16 l, +16), i.e. tile row r = 4 i + l / 16 at physical chunk l % 16.
-  // Rows past the chunk end repeat its last row (finite values, masked out).
-  int koff[IPW], voff[IPW], lrow[IPW];
-#pragma unroll
-  for (int u = 0; u < IPW; ++u) {
-    const int i = wave * IPW + u;
-    const int r = 4 * i + (lane >> 4), pc = lane & 15;
-    lrow[u] = r;
-    koff[u] = r * (D * 2) + 16 * kswz(r, pc);
-    voff[u] = r * (D * 2) + 16 * vswz(r, pc);
-  }
+  // [1024 i + 16 l, +16), i.e. tile row r = 4 i + l / 16 at physical chunk l % 16,
+  // which holds logical chunk (l % 16) ^ (r % 16) of K or (l % 16) ^ 4 (r % 4)
+  // of V.  For this wave's u-th load, r = 4 (wave IPW + u) + l / 16: the V
+  // offset and the row advance by 1024 and 4 per load; the K chunk is
+  // (l % 16) ^ (l / 16) ^ 4 (u + wave IPW) % 16.  Rows past the chunk end repeat
+  // its last row (finite values, masked out).
+  const int lrow0 = 4 * wave * IPW + (lane >> 4);
+  const int kx = (lane & 15) ^ (lane >> 4);
+  const int voff0 = lrow0 * (D * 2) + 16 * vswz(lrow0, lane & 15);
+  auto load_off = [&](bool is_k, int u) {
+    const int r = lrow0 + 4 * u;
+    return is_k ? r * (D * 2) + 16 * (kx ^ ((4 * (wave * IPW + u)) & 15)) : voff0 + 1024 * u;
+  };
   const uint8_t *Kb = reinterpret_cast<const uint8_t *>(Kg);
   const uint8_t *Vb = reinterpret_cast<const uint8_t *>(Vg);
-  auto issue = [&](const uint8_t *src, const int (&off)[IPW], uint8_t *dst, int j) {
+  // Offsets are relative to the slab base (a slab is at most 2^24 rows, so they
+  // fit 32 bits); the base of a full tile is wave-uniform.
+  auto issue = [&](const uint8_t *src, bool is_k, uint8_t *dst, int j) {
     const int kt = k0 + j * TK;
     const uint32_t lds = __builtin_amdgcn_readfirstlane(
         (uint32_t)(uintptr_t)(lds_void_t *)(dst + 1024 * wave * IPW));
     if (kt + TK <= k1) {
       const uint8_t *sb = src + (int64_t)kt * (D * 2);
 #pragma unroll
-      for (int u = 0; u < IPW; ++u) lds_load16(sb + off[u], lds + 1024 * u);
+      for (int u = 0; u < IPW; ++u) lds_load16(sb, (uint32_t)load_off(is_k, u), lds + 1024 * u);
     } else {                             // last tile: rows past the chunk end repeat its last row
 #pragma unroll
       for (int u = 0; u < IPW; ++u) {
-        const int64_t t = min(kt + lrow[u], k1 - 1);
-        lds_load16(src + t * (D * 2) + (off[u] - lrow[u] * (D * 2)), lds + 1024 * u);
+        const int r = lrow0 + 4 * u;
+        const int t = min(kt + r, k1 - 1);
+        lds_load16(src, (uint32_t)(t * (D * 2) + (load_off(is_k, u) - r * (D * 2))), lds + 1024 * u);
       }
     }
   };
-  auto issue_k = [&](int j) { issue(Kb, koff, kring[j % SLOTS], j); };
-  auto issue_v = [&](int j) { issue(Vb, voff, vring[j % SLOTS], j); };
+  auto issue_k = [&](int j) { issue(Kb, true, kring[j % SLOTS], j); };
+  auto issue_v = [&](int j) { issue(Vb, false, vring[j % SLOTS], j); };
 
   // K operand: row (lane & 31) of a 32-key sub-block, 16-byte chunk 2 ks + h.
   int kro[D / 16];
@@ -238,6 +250,13 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
         const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(ks + sb * 32 * (D * 2) + kro[k8]));
         Sc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k8], Sc[sb], 0, 0, 0);
       }
+    // keep the K fragment reads just ahead of their products (two LDS reads,
+    // two products, eight times) instead of all sixteen reads up front
+#pragma unroll
+    for (int k8 = 0; k8 < D / 16; ++k8) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    }
   };
 
   float m = -INFINITY, lsum = 0.f;
@@ -246,30 +265,37 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   for (int i = 0; i < D / 32; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) O[i][r] = 0.f;
-  uint32_t an0 = 0, an1 = 0, an2 = 0, an3 = 0;   // this row's ancestor words (after the first barrier)
   const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
 
   // Scores of tile j -> bf16 weights (online softmax, lazy rescale) -> O += V^T P^T.
   // Accumulator entry r of sub-block sb is key kt + 32 sb + 8 (r / 4) + 4 h + r % 4.
+  // The tree mask, for tiles that reach the tree rows or the chunk end, is
+  // branch-free (bitwise tests, one select per score) so that the scores keep
+  // their registers on both paths.
   auto softmax_pv = [&](int j, f32x16 (&Sc)[2]) {
     const int kt = k0 + j * TK;
-    if (kt + TK > min(k1, L)) {          // tile reaches the tree rows or the chunk end
+    if (kt + TK > min(k1, L)) {
+      const uint4 an = *reinterpret_cast<const uint4 *>(anc[node]);   // ancestor words of this row's node
+      const uint64_t alo = (uint64_t)an.y << 32 | an.x, ahi = (uint64_t)an.w << 32 | an.z;
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
         for (int r2 = 0; r2 < 16; ++r2) {
           const int t = kt + 32 * sb + 8 * (r2 >> 2) + 4 * h + (r2 & 3);
-          const uint32_t rel = (uint32_t)(t - L);
-          const uint32_t w = rel < 32 ? an0 : rel < 64 ? an1 : rel < 96 ? an2 : an3;
-          const bool vis = t < k1 && (t < L || ((w >> (rel & 31)) & 1u));
+          const uint32_t rel = (uint32_t)(t - L) & 127u;
+          const uint64_t word = rel < 64 ? alo : ahi;
+          const bool anc_bit = (word >> (rel & 63)) & 1u;
+          const bool vis = (t < k1) & ((t < L) | anc_bit);
           Sc[sb][r2] = vis ? Sc[sb][r2] : -INFINITY;
         }
     }
-    float tmax = -INFINITY;
+    // tile max as a tree (three-input maxima), not a dependent chain
+    float t8[8];
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int r2 = 0; r2 < 16; ++r2) tmax = fmaxf(tmax, Sc[sb][r2]);
+    for (int i = 0; i < 8; ++i)
+      t8[i] = fmaxf(fmaxf(Sc[i >> 2][4 * (i & 3)], Sc[i >> 2][4 * (i & 3) + 1]),
+                    fmaxf(Sc[i >> 2][4 * (i & 3) + 2], Sc[i >> 2][4 * (i & 3) + 3]));
+    float tmax = fmaxf(fmaxf(fmaxf(t8[0], t8[1]), fmaxf(t8[2], t8[3])), fmaxf(fmaxf(t8[4], t8[5]), fmaxf(t8[6], t8[7])));
     tmax = max_with_other_half(tmax) * a.scale_log2;
     // Lazy rescaling: the reference max m moves only when a score exceeds it by
     // more than kRescaleSlack (log2 units), so weights stay <= 2^kRescaleSlack;
@@ -328,12 +354,6 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
     else
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   };
-  auto read_anc = [&]() {
-    an0 = anc[node][0];
-    an1 = anc[node][1];
-    an2 = anc[node][2];
-    an3 = anc[node][3];
-  };
 
   // Prologue: tiles 0 .. SLOTS-2 (K then V).  Iteration j needs tile j; after
   // its barrier every wave is done with tile j-1, whose slots take tile
@@ -348,7 +368,6 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
     // loads issued after tile j: tile j+1 (3 slots), two operands
     wait_loads(SLOTS == 3 && j + 1 < ntiles ? 2 : 0);
     ring_barrier();
-    if (j == 0) read_anc();
     if (j + SLOTS - 1 < ntiles) {
       issue_k(j + SLOTS - 1);
       issue_v(j + SLOTS - 1);
@@ -390,44 +409,52 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   }
 }
 
-// Merge the chunk partials of one (sequence, KV head, row block) in chunk order;
-// each block handles kCombineRows rows of the row block.
-constexpr int kCombineRows = 256 / (D / 4);   // 8 rows x 32 float4 columns per block
-
+// Merge the chunk partials of one (sequence, KV head, row block) in chunk
+// order: one block per row block, two threads per query row, each thread 64
+// head-dim columns.
 template <int RB>
-__global__ __launch_bounds__(256) void tree_attn_combine(AttnArgs a) {
-  constexpr int PARTS = RB / kCombineRows;
-  const int idx = blockIdx.x / PARTS, part = blockIdx.x % PARTS;
-  int s = 0;
-  for (int j = 0; j < a.nseq; ++j)
-    if (a.seq[j].nch > 1 && a.seq[j].citem0 <= idx) s = j;
+__global__ __launch_bounds__(2 * RB) void tree_attn_combine(AttnArgs a) {
+  const int idx = blockIdx.x, lane = threadIdx.x & 63;
+  // the split sequence of this block: the last one whose first combine item is <= idx
+  const bool split_le = lane < a.nseq && a.seq[lane].nch > 1 && a.seq[lane].citem0 <= idx;
+  const int s = 63 - __builtin_clzll(__builtin_amdgcn_ballot_w64(split_le));
   const AttnSeq &S = a.seq[s];
   const int local = idx - S.citem0;
   const int kvh = local / S.nrb, rb = local % S.nrb;
-  const int rows = S.N * a.group;
+  const int r = threadIdx.x >> 1, half = threadIdx.x & 1;
+  const int row = rb * RB + r;
+  if (row >= S.N * a.group) return;
   const int64_t pf = attn_partial_floats(RB);
   const float *base = a.part + ((int64_t)S.part0 + ((int64_t)kvh * S.nrb + rb) * S.nch) * pf;
-  const int r = part * kCombineRows + threadIdx.x / (D / 4);
-  const int d4 = (threadIdx.x % (D / 4)) * 4;
-  const int row = rb * RB + r;
-  if (row >= rows) return;
   float M = -INFINITY;
   for (int c = 0; c < S.nch; ++c) M = fmaxf(M, base[c * pf + (int64_t)RB * D / 2 + r]);
-  float l = 0.f, o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
+  float l = 0.f, o[D / 2];
+#pragma unroll
+  for (int e = 0; e < D / 2; ++e) o[e] = 0.f;
   for (int c = 0; c < S.nch; ++c) {
     const float *sl = base + c * pf;
     const float w = fast_exp2(sl[(int64_t)RB * D / 2 + r] - M);
     l += w * sl[(int64_t)RB * D / 2 + RB + r];
-    const uint2 o = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(sl) + (int64_t)r * D + d4);
-    o0 += w * __uint_as_float(o.x << 16);
-    o1 += w * __uint_as_float(o.x & 0xFFFF0000u);
-    o2 += w * __uint_as_float(o.y << 16);
-    o3 += w * __uint_as_float(o.y & 0xFFFF0000u);
+    const uint4 *po = reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(sl) + (int64_t)r * D + half * (D / 2));
+#pragma unroll
+    for (int q = 0; q < D / 16; ++q) {
+      const uint4 v = po[q];
+      const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o[8 * q + 2 * e] += w * __uint_as_float(wv[e] << 16);
+        o[8 * q + 2 * e + 1] += w * __uint_as_float(wv[e] & 0xFFFF0000u);
+      }
+    }
   }
   const float inv = 1.f / l;
   const int node = row / a.group, hq = kvh * a.group + row % a.group;
-  uint16_t *op = static_cast<uint16_t *>(a.out) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D + d4;
-  *reinterpret_cast<uint2 *>(op) = uint2{pack_bf16x2(o0 * inv, o1 * inv), pack_bf16x2(o2 * inv, o3 * inv)};
+  uint4 *op = reinterpret_cast<uint4 *>(static_cast<uint16_t *>(a.out) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D +
+                                        half * (D / 2));
+#pragma unroll
+  for (int q = 0; q < D / 16; ++q)
+    op[q] = uint4{pack_bf16x2(o[8 * q] * inv, o[8 * q + 1] * inv), pack_bf16x2(o[8 * q + 2] * inv, o[8 * q + 3] * inv),
+                  pack_bf16x2(o[8 * q + 4] * inv, o[8 * q + 5] * inv), pack_bf16x2(o[8 * q + 6] * inv, o[8 * q + 7] * inv)};
 }
 
 // fp32 path: one wave per (node, query head); lanes own head-dimension elements
@@ -471,13 +498,13 @@ __global__ __launch_bounds__(256) void tree_attn_f32(AttnArgs a, int node_begin,
 hipError_t launch_tree_attn_bf16(const AttnArgs &a, int rows_per_block, hipStream_t st) {
   if (rows_per_block == 64) {
     hipLaunchKernelGGL((tree_attn_bf16<2, 2, 2>), dim3(a.items), dim3(128), 0, st, a);
-    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<64>, dim3(a.citems * (64 / kCombineRows)), dim3(256), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<64>, dim3(a.citems), dim3(128), 0, st, a);
   } else if (rows_per_block == 128) {
     hipLaunchKernelGGL((tree_attn_bf16<4, 2, 2>), dim3(a.items), dim3(256), 0, st, a);
-    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<128>, dim3(a.citems * (128 / kCombineRows)), dim3(256), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<128>, dim3(a.citems), dim3(256), 0, st, a);
   } else {
     hipLaunchKernelGGL((tree_attn_bf16<8, 3, 1>), dim3(a.items), dim3(512), 0, st, a);
-    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<256>, dim3(a.citems * (256 / kCombineRows)), dim3(256), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<256>, dim3(a.citems), dim3(512), 0, st, a);
   }
   return hipGetLastError();
 }
