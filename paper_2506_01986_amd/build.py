@@ -24,6 +24,11 @@ FLAGS = [
     "-Wall", "-Wno-unused-function",
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
 ]
+# The attention kernels are compiled without NaN semantics: no NaN enters them
+# (scores of finite inputs, -inf for masked keys), and with NaNs honoured every
+# float maximum of a matrix-core result is preceded by a canonicalising
+# instruction (32 extra vector operations per key tile).
+EXTRA = {"tree_attn.hip": ["-fno-honor-nans"]}
 
 
 def hipcc() -> str:
@@ -36,7 +41,7 @@ def build(verbose: bool = False) -> str:
 
     def compile_one(src):
         obj = os.path.join(OUT, os.path.splitext(src)[0] + ".o")
-        cmd = [hipcc(), *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [hipcc(), *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
         if src.endswith(".cpp"):
             cmd.insert(1, "-xhip")
         r = subprocess.run(cmd, capture_output=True, text=True)

@@ -33,58 +33,102 @@ namespace {
 
 constexpr int D = kAttnHeadDim;
 constexpr int TK = kAttnKeyTile;
-constexpr float kRescaleSlack = 8.f;   // log2 units: softmax weights stay <= 256 between rescales
+constexpr float kRescaleSlack = 8.f;
+#ifndef SPECMEMO_PP_SLOTS
+#define SPECMEMO_PP_SLOTS 4
+#endif
+constexpr int kPingPongSlots = SPECMEMO_PP_SLOTS;   // ring depth of the 256-row ping-pong kernel   // log2 units: softmax weights stay <= 256 between rescales
 
 struct Item {
   int s, kvh, rb, ch;
 };
 
-// The sequence of a block is found by one wave-parallel search: lane l reads
-// sequence l's start (the launch holds at most 64 sequences) and a ballot
-// counts the starts at or below the block's position.
+// The sequence of a block is found by one wave-parallel search: lane l holds
+// sequence l's first position (the launch holds at most kMaxSeqPerLaunch
+// sequences) and a ballot counts the starts at or below the block's position.
 __device__ __forceinline__ int find_seq(int nseq, int start_of_lane, int pos) {
   const int lane = threadIdx.x & 63;
   const uint64_t le = __builtin_amdgcn_ballot_w64(lane < nseq && start_of_lane <= pos);
   return __builtin_popcountll(le) - 1;
 }
 
-// Work items in launch order: sequence, then KV head, chunk, row block.
-__device__ __forceinline__ Item decode_item(const AttnArgs &a, int idx) {
-  const int lane = threadIdx.x & 63;
-  const int s = find_seq(a.nseq, lane < a.nseq ? a.seq[lane].item0 : 0, idx);
-  const AttnSeq &S = a.seq[s];
-  int local = idx - S.item0;
-  Item it;
-  it.s = s;
-  it.rb = local % S.nrb;
-  local /= S.nrb;
-  it.ch = local % S.nch;
-  it.kvh = local / S.nch;
-  return it;
+__device__ __forceinline__ int rl(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
+
+// Descriptor of sequence s from the per-lane copies (lane l holds sequence l).
+__device__ __forceinline__ AttnSeq pick_seq(const AttnSeq &d, int s) {
+  AttnSeq r;
+  r.base = (int64_t)((uint64_t)(uint32_t)rl((int)(d.base >> 32), s) << 32 | (uint32_t)rl((int)d.base, s));
+  r.L = rl(d.L, s);
+  r.node0 = rl(d.node0, s);
+  r.N = rl(d.N, s);
+  r.nrb = rl(d.nrb, s);
+  r.nch = rl(d.nch, s);
+  r.ch_len = rl(d.ch_len, s);
+  r.item0 = rl(d.item0, s);
+  r.part0 = rl(d.part0, s);
+  r.citem0 = rl(d.citem0, s);
+  r.unit0 = rl(d.unit0, s);
+  return r;
 }
 
-// XCD order.  Blocks reach the eight XCDs round-robin by block id, so block
+// Work item and sequence descriptor of block `bid`; false for a padding block.
+// Every load is issued up front (one memory latency): the per-lane copies of
+// the sequence descriptors and, for the XCD order, of XCD x's block counts.
+//
+// Launch order: sequence, then KV head, chunk, row block.
+//
+// XCD order: blocks reach the eight XCDs round-robin by block id, so block
 // 8 k + x is the k-th block of XCD x.  A unit is one (sequence, KV head,
 // chunk) with all its row blocks, which read the same K/V; unit u (launch
 // order, longest sequences first) runs on XCD u mod 8, so those row blocks
 // share one L2 and every XCD gets long and short units alike.  xcd_cum[x][s]
-// is the number of XCD x's blocks before sequence s.  Returns false for the
-// padding blocks past the busiest XCD's work.
-__device__ __forceinline__ bool decode_item_xcd(const AttnArgs &a, int bid, Item &it) {
+// is the number of XCD x's blocks before sequence s; blocks past the busiest
+// XCD's work are padding.
+__device__ __forceinline__ bool decode_item(const AttnArgs &a, int bid, Item &it, AttnSeq &S) {
   const int lane = threadIdx.x & 63;
   const int x = bid & 7, k = bid >> 3;
-  if (k >= a.xcd_cum[x][a.nseq]) return false;
-  const int s = find_seq(a.nseq, lane < a.nseq ? a.xcd_cum[x][lane] : 0, k);
-  const AttnSeq &S = a.seq[s];
-  const int kk = k - a.xcd_cum[x][s];
-  const int u0 = S.unit0;
-  const int first = u0 + ((x - (u0 & 7)) & 7);            // first unit >= u0 on XCD x
-  const int u = first + 8 * (kk / S.nrb) - u0;
-  it.s = s;
-  it.rb = kk % S.nrb;
-  it.ch = u % S.nch;
-  it.kvh = u / S.nch;
+  AttnSeq mine{};
+  if (lane < kMaxSeqPerLaunch) mine = a.seq[lane];
+  const int cum = lane <= kMaxSeqPerLaunch ? a.xcd_cum[x][lane] : 0;
+  const int nseq = a.nseq;
+  if (a.xcd_order) {
+    if (k >= rl(cum, nseq)) return false;
+    const int s = find_seq(nseq, cum, k);
+    S = pick_seq(mine, s);
+    const int kk = k - rl(cum, s);
+    const int u0 = S.unit0;
+    const int first = u0 + ((x - (u0 & 7)) & 7);            // first unit >= u0 on XCD x
+    const int u = first + 8 * (kk / S.nrb) - u0;
+    it.s = s;
+    it.rb = kk % S.nrb;
+    it.ch = u % S.nch;
+    it.kvh = u / S.nch;
+  } else {
+    const int s = find_seq(nseq, mine.item0, bid);
+    S = pick_seq(mine, s);
+    int local = bid - S.item0;
+    it.s = s;
+    it.rb = local % S.nrb;
+    local /= S.nrb;
+    it.ch = local % S.nch;
+    it.kvh = local / S.nch;
+  }
   return true;
+}
+
+// Maximum of a lane's 32 scores as a tree of three-input maxima (16 operations).
+__device__ __forceinline__ float tile_max32(const f32x16 (&x)[2]) {
+  float t[12];
+#pragma unroll
+  for (int i = 0; i < 10; ++i) {
+    const int e = 3 * i;
+    t[i] = fmaxf(fmaxf(x[e >> 4][e & 15], x[(e + 1) >> 4][(e + 1) & 15]), x[(e + 2) >> 4][(e + 2) & 15]);
+  }
+  t[10] = x[1][14];
+  t[11] = x[1][15];
+  const float u0 = fmaxf(fmaxf(t[0], t[1]), t[2]), u1 = fmaxf(fmaxf(t[3], t[4]), t[5]);
+  const float u2 = fmaxf(fmaxf(t[6], t[7]), t[8]), u3 = fmaxf(fmaxf(t[9], t[10]), t[11]);
+  return fmaxf(fmaxf(u0, u1), fmaxf(u2, u3));
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -129,52 +173,16 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t kring[SLOTS][TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t vring[SLOTS][TILE];
   __shared__ __attribute__((aligned(16))) uint32_t anc[kMaxNodes][4];
+  __shared__ int par[kMaxNodes];
+  static_assert(WAVES * 64 >= kMaxNodes, "one thread per tree node");
 
   Item it;
-  if (a.xcd_order) {
-    if (!decode_item_xcd(a, blockIdx.x, it)) return;   // padding block: no work, no barrier reached
-  } else {
-    it = decode_item(a, blockIdx.x);
-  }
-  const AttnSeq &S = a.seq[it.s];
+  AttnSeq S;
+  if (!decode_item(a, blockIdx.x, it, S)) return;   // padding block: no work, no barrier reached
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5;              // which half of the wave
   const int L = S.L, N = S.N, g = a.group;
   const int rows = N * g;
-
-  // Ancestor-or-self bitmask of every node of this tree (local ids).
-  for (int n = tid; n < N; n += WAVES * 64) {
-    uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
-    for (int u = n; u >= 0; u = a.parent[S.node0 + u]) {
-      const uint32_t bit = 1u << (u & 31);
-      const int w = u >> 5;
-      m0 |= w == 0 ? bit : 0u;
-      m1 |= w == 1 ? bit : 0u;
-      m2 |= w == 2 ? bit : 0u;
-      m3 |= w == 3 ? bit : 0u;
-    }
-    anc[n][0] = m0;
-    anc[n][1] = m1;
-    anc[n][2] = m2;
-    anc[n][3] = m3;
-  }
-
-  // This lane's query row and its Q fragments (B operand of S^T = K Q^T).
-  const int my_row = it.rb * RB + wave * 32 + (lane & 31);
-  const bool row_ok = my_row < rows;
-  const int node = row_ok ? my_row / g : 0;
-  const int hq = it.kvh * g + (row_ok ? my_row % g : 0);
-  bf16x8 qf[D / 16];
-  {
-    const uint16_t *qbase = static_cast<const uint16_t *>(a.q) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D + 8 * h;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, ld16_or_zero(row_ok, qbase + 16 * ks));
-    // Land the Q loads here: otherwise the compiler waits for them at their
-    // first use inside the tile loop, on every iteration, and with them for
-    // every tile load in flight.
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) asm volatile("" ::"v"(qf[ks]));
-  }
 
   // Key range of this chunk: chunk boundaries lie inside the committed region and
   // the last chunk runs to the end of the tree rows, so every chunk holds at
@@ -223,6 +231,52 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   auto issue_k = [&](int j) { issue(Kb, true, kring[j % SLOTS], j); };
   auto issue_v = [&](int j) { issue(Vb, false, vring[j % SLOTS], j); };
 
+  // Prologue: tiles 0 .. SLOTS-2 (K then V) first, then the Q fragments of this
+  // lane's query row (B operand of S^T = K Q^T) and the tree's parent array,
+  // so that the three loads share one memory latency.
+#pragma unroll
+  for (int t = 0; t < SLOTS - 1; ++t)
+    if (t < ntiles) {
+      issue_k(t);
+      issue_v(t);
+    }
+  const int pn = tid < N ? a.parent[S.node0 + tid] : -1;
+  const int my_row = it.rb * RB + wave * 32 + (lane & 31);
+  const bool row_ok = my_row < rows;
+  const int node = row_ok ? my_row / g : 0;
+  const int hq = it.kvh * g + (row_ok ? my_row % g : 0);
+  bf16x8 qf[D / 16];
+  {
+    const uint16_t *qbase = static_cast<const uint16_t *>(a.q) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D + 8 * h;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, ld16_or_zero(row_ok, qbase + 16 * ks));
+  }
+  if (tid < N) par[tid] = pn;
+  // Land the Q loads here: otherwise the compiler waits for them at their
+  // first use inside the tile loop, on every iteration, and with them for
+  // every tile load in flight.
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) asm volatile("" ::"v"(qf[ks]));
+  ring_barrier();
+
+  // Ancestor-or-self bitmask of every node of this tree (local ids), walked in
+  // LDS; the masks are read after the first barrier of the tile loop.
+  if (tid < N) {
+    uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
+    for (int u = tid; u >= 0; u = par[u]) {
+      const uint32_t bit = 1u << (u & 31);
+      const int w = u >> 5;
+      m0 |= w == 0 ? bit : 0u;
+      m1 |= w == 1 ? bit : 0u;
+      m2 |= w == 2 ? bit : 0u;
+      m3 |= w == 3 ? bit : 0u;
+    }
+    anc[tid][0] = m0;
+    anc[tid][1] = m1;
+    anc[tid][2] = m2;
+    anc[tid][3] = m3;
+  }
+
   // K operand: row (lane & 31) of a 32-key sub-block, 16-byte chunk 2 ks + h.
   int kro[D / 16];
 #pragma unroll
@@ -267,12 +321,13 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
     for (int r = 0; r < 16; ++r) O[i][r] = 0.f;
   const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
 
-  // Scores of tile j -> bf16 weights (online softmax, lazy rescale) -> O += V^T P^T.
+  // Scores of tile j -> bf16 weights (online softmax, lazy rescale); O += V^T P^T.
   // Accumulator entry r of sub-block sb is key kt + 32 sb + 8 (r / 4) + 4 h + r % 4.
   // The tree mask, for tiles that reach the tree rows or the chunk end, is
   // branch-free (bitwise tests, one select per score) so that the scores keep
-  // their registers on both paths.
-  auto softmax_pv = [&](int j, f32x16 (&Sc)[2]) {
+  // their registers on both paths.  The weights are returned packed as the B
+  // operands of the four 16-key groups of the PV product.
+  auto softmax_head = [&](int j, f32x16 (&Sc)[2]) {   // mask, tile max, rescaling
     const int kt = k0 + j * TK;
     if (kt + TK > min(k1, L)) {
       const uint4 an = *reinterpret_cast<const uint4 *>(anc[node]);   // ancestor words of this row's node
@@ -289,14 +344,7 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
           Sc[sb][r2] = vis ? Sc[sb][r2] : -INFINITY;
         }
     }
-    // tile max as a tree (three-input maxima), not a dependent chain
-    float t8[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      t8[i] = fmaxf(fmaxf(Sc[i >> 2][4 * (i & 3)], Sc[i >> 2][4 * (i & 3) + 1]),
-                    fmaxf(Sc[i >> 2][4 * (i & 3) + 2], Sc[i >> 2][4 * (i & 3) + 3]));
-    float tmax = fmaxf(fmaxf(fmaxf(t8[0], t8[1]), fmaxf(t8[2], t8[3])), fmaxf(fmaxf(t8[4], t8[5]), fmaxf(t8[6], t8[7])));
-    tmax = max_with_other_half(tmax) * a.scale_log2;
+    const float tmax = max_with_other_half(tile_max32(Sc)) * a.scale_log2;
     // Lazy rescaling: the reference max m moves only when a score exceeds it by
     // more than kRescaleSlack (log2 units), so weights stay <= 2^kRescaleSlack;
     // the branch is taken by the whole wave, rarely after the first tile.
@@ -311,10 +359,11 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
 #pragma unroll
         for (int r2 = 0; r2 < 16; ++r2) O[i][r2] *= alpha;
     }
+  };
+  auto softmax_tail = [&](const f32x16 (&Sc)[2], uint32_t (&pk)[4][4]) {   // weights and row sum
     const float m_use = m == -INFINITY ? 0.f : m;
     // B operand of 16-key group mh = 2 sb + half: slot 8 h + s <-> key
     // 32 sb + 16 half + 8 (s / 4) + 4 h + s % 4 (the V^T reads use the same order).
-    uint32_t pk[4][4];
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -331,7 +380,8 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk[mh][q]), ones, lsum, false);
-    const uint8_t *vs = vring[j % SLOTS];
+  };
+  auto pv = [&](const uint8_t *vs, const uint32_t (&pk)[4][4]) {
 #pragma unroll
     for (int mh = 0; mh < 4; ++mh) {
       const bf16x8 pf = __builtin_bit_cast(bf16x8, uint4{pk[mh][0], pk[mh][1], pk[mh][2], pk[mh][3]});
@@ -355,15 +405,8 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   };
 
-  // Prologue: tiles 0 .. SLOTS-2 (K then V).  Iteration j needs tile j; after
-  // its barrier every wave is done with tile j-1, whose slots take tile
-  // j+SLOTS-1.
-#pragma unroll
-  for (int t = 0; t < SLOTS - 1; ++t)
-    if (t < ntiles) {
-      issue_k(t);
-      issue_v(t);
-    }
+  // Iteration j needs tile j; after its barrier every wave is done with tile
+  // j-1, whose slots take tile j+SLOTS-1.
   for (int j = 0; j < ntiles; ++j) {
     // loads issued after tile j: tile j+1 (3 slots), two operands
     wait_loads(SLOTS == 3 && j + 1 < ntiles ? 2 : 0);
@@ -373,8 +416,11 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
       issue_v(j + SLOTS - 1);
     }
     f32x16 Sc[2];
+    uint32_t pk[4][4];
     qk(j, Sc);
-    softmax_pv(j, Sc);
+    softmax_head(j, Sc);
+    softmax_tail(Sc, pk);
+    pv(vring[j % SLOTS], pk);
   }
 
   const float ltot = sum_with_other_half(lsum);
