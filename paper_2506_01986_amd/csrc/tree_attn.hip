@@ -456,49 +456,59 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
 }
 
 // Merge the chunk partials of one (sequence, KV head, row block) in chunk
-// order: one block per row block, two threads per query row, each thread 64
-// head-dim columns.
+// order (deterministic, no atomics): one block per row block, four threads per
+// query row, each with 32 head-dim columns, and one pass over the chunks with
+// a running max (the partials hold unnormalised O in bf16, the chunk's max m
+// and sum l in fp32).
 template <int RB>
-__global__ __launch_bounds__(2 * RB) void tree_attn_combine(AttnArgs a) {
+__global__ __launch_bounds__(4 * RB) void tree_attn_combine(AttnArgs a) {
+  constexpr int CPT = D / 4;   // columns per thread
   const int idx = blockIdx.x, lane = threadIdx.x & 63;
+  AttnSeq mine{};
+  if (lane < kMaxSeqPerLaunch) mine = a.seq[lane];
   // the split sequence of this block: the last one whose first combine item is <= idx
-  const bool split_le = lane < a.nseq && a.seq[lane].nch > 1 && a.seq[lane].citem0 <= idx;
+  const bool split_le = lane < a.nseq && mine.nch > 1 && mine.citem0 <= idx;
   const int s = 63 - __builtin_clzll(__builtin_amdgcn_ballot_w64(split_le));
-  const AttnSeq &S = a.seq[s];
+  const AttnSeq S = pick_seq(mine, s);
   const int local = idx - S.citem0;
   const int kvh = local / S.nrb, rb = local % S.nrb;
-  const int r = threadIdx.x >> 1, half = threadIdx.x & 1;
+  const int r = threadIdx.x >> 2, quarter = threadIdx.x & 3;
   const int row = rb * RB + r;
   if (row >= S.N * a.group) return;
   const int64_t pf = attn_partial_floats(RB);
   const float *base = a.part + ((int64_t)S.part0 + ((int64_t)kvh * S.nrb + rb) * S.nch) * pf;
-  float M = -INFINITY;
-  for (int c = 0; c < S.nch; ++c) M = fmaxf(M, base[c * pf + (int64_t)RB * D / 2 + r]);
-  float l = 0.f, o[D / 2];
+  float M = -INFINITY, l = 0.f, o[CPT];
 #pragma unroll
-  for (int e = 0; e < D / 2; ++e) o[e] = 0.f;
+  for (int e = 0; e < CPT; ++e) o[e] = 0.f;
+#pragma unroll 2
   for (int c = 0; c < S.nch; ++c) {
     const float *sl = base + c * pf;
-    const float w = fast_exp2(sl[(int64_t)RB * D / 2 + r] - M);
-    l += w * sl[(int64_t)RB * D / 2 + RB + r];
-    const uint4 *po = reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(sl) + (int64_t)r * D + half * (D / 2));
+    const float mc = sl[(int64_t)RB * D / 2 + r], lc = sl[(int64_t)RB * D / 2 + RB + r];
+    const uint4 *po = reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(sl) + (int64_t)r * D + quarter * CPT);
+    uint4 v[CPT / 8];
 #pragma unroll
-    for (int q = 0; q < D / 16; ++q) {
-      const uint4 v = po[q];
-      const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+    for (int q = 0; q < CPT / 8; ++q) v[q] = po[q];
+    // every chunk holds keys visible to every row, so mc is finite
+    const float Mn = fmaxf(M, mc);
+    const float wa = fast_exp2(M - Mn), wb = fast_exp2(mc - Mn);   // wa = 0 for the first chunk
+    l = l * wa + lc * wb;
+#pragma unroll
+    for (int q = 0; q < CPT / 8; ++q) {
+      const uint32_t wv[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        o[8 * q + 2 * e] += w * __uint_as_float(wv[e] << 16);
-        o[8 * q + 2 * e + 1] += w * __uint_as_float(wv[e] & 0xFFFF0000u);
+        o[8 * q + 2 * e] = o[8 * q + 2 * e] * wa + wb * __uint_as_float(wv[e] << 16);
+        o[8 * q + 2 * e + 1] = o[8 * q + 2 * e + 1] * wa + wb * __uint_as_float(wv[e] & 0xFFFF0000u);
       }
     }
+    M = Mn;
   }
   const float inv = 1.f / l;
   const int node = row / a.group, hq = kvh * a.group + row % a.group;
   uint4 *op = reinterpret_cast<uint4 *>(static_cast<uint16_t *>(a.out) + ((int64_t)(S.node0 + node) * a.n_q + hq) * D +
-                                        half * (D / 2));
+                                        quarter * CPT);
 #pragma unroll
-  for (int q = 0; q < D / 16; ++q)
+  for (int q = 0; q < CPT / 8; ++q)
     op[q] = uint4{pack_bf16x2(o[8 * q] * inv, o[8 * q + 1] * inv), pack_bf16x2(o[8 * q + 2] * inv, o[8 * q + 3] * inv),
                   pack_bf16x2(o[8 * q + 4] * inv, o[8 * q + 5] * inv), pack_bf16x2(o[8 * q + 6] * inv, o[8 * q + 7] * inv)};
 }
@@ -544,13 +554,13 @@ __global__ __launch_bounds__(256) void tree_attn_f32(AttnArgs a, int node_begin,
 hipError_t launch_tree_attn_bf16(const AttnArgs &a, int rows_per_block, hipStream_t st) {
   if (rows_per_block == 64) {
     hipLaunchKernelGGL((tree_attn_bf16<2, 2, 2>), dim3(a.items), dim3(128), 0, st, a);
-    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<64>, dim3(a.citems), dim3(128), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<64>, dim3(a.citems), dim3(256), 0, st, a);
   } else if (rows_per_block == 128) {
     hipLaunchKernelGGL((tree_attn_bf16<4, 2, 2>), dim3(a.items), dim3(256), 0, st, a);
-    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<128>, dim3(a.citems), dim3(256), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<128>, dim3(a.citems), dim3(512), 0, st, a);
   } else {
     hipLaunchKernelGGL((tree_attn_bf16<8, 3, 1>), dim3(a.items), dim3(512), 0, st, a);
-    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<256>, dim3(a.citems), dim3(512), 0, st, a);
+    if (a.citems) hipLaunchKernelGGL(tree_attn_combine<256>, dim3(a.citems), dim3(1024), 0, st, a);
   }
   return hipGetLastError();
 }
