@@ -177,7 +177,8 @@ int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmem
  * cumulative).  base_logits: device [sum N_b][vocab] in `dt`, row u = the
  * base model's next-token logits after node u.  node_tok: device int32.
  *
- * GREEDY:  a[u] = argmax_v base_logits[u][v] (ties: lower v).  From the root,
+ * GREEDY:  a[u] = argmax_v base_logits[u][v] (ties: lower v; -0 equals +0;
+ *          NaN logits are not valid input).  From the root,
  *          move to the child c with node_tok[c] == a[cur] while one exists.
  * TYPICAL: pi_u = softmax(base_logits[u] / temperature), H_u its entropy;
  *          edge u->c passes iff pi_u[node_tok[c]] > min(eps, delta*exp(-H_u));

@@ -26,6 +26,81 @@ __device__ __forceinline__ float ld(const void *p, int64_t i) {
   return bf16_to_f32(static_cast<const uint16_t *>(p)[i]);
 }
 
+typedef short s16x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
+
+// Order-preserving keys of the two bf16 values of a word, one per 16-bit half:
+// a non-negative value gets its sign bit set, a negative one has all 16 bits
+// inverted, so a larger value has a larger unsigned key.  The keys of -0 and
+// +0 differ (0x7FFF, 0x8000); the scan below treats them as equal.
+__device__ __forceinline__ uint32_t bf16x2_keys(uint32_t w) {
+  const s16x2_t sign = __builtin_bit_cast(s16x2_t, w) >> (short)15;   // 0 or -1 per half
+  return w ^ (__builtin_bit_cast(uint32_t, sign) | 0x80008000u);
+}
+
+constexpr int kArgU = 8;                          // 16-byte loads per thread
+constexpr int kArgMaxVocab = kNT * kArgU * 8;     // rows the register pass covers
+
+// Arg-best of a bf16 row with vocab % 8 == 0 and vocab <= kArgMaxVocab, in two
+// steps over the same registers: the row's largest key (one packed 16-bit
+// maximum per two values), then the lowest id holding it, searched only by the
+// threads whose own maximum is that key.  NaN rows are not valid input.
+__device__ void row_argbest_bf16(const uint16_t *row, int vocab, uint32_t *sk, float &out_v, int &out_i) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint4 *p = reinterpret_cast<const uint4 *>(row);
+  const int nch = vocab / 8;
+  uint4 w[kArgU];
+#pragma unroll
+  for (int u = 0; u < kArgU; ++u) {
+    const int c = u * kNT + tid;
+    w[u] = c < nch ? p[c] : uint4{0u, 0u, 0u, 0u};
+  }
+  u16x2_t mx = {0, 0};
+#pragma unroll
+  for (int u = 0; u < kArgU; ++u) {
+    const bool live = u * kNT + tid < nch;   // padding keys stay 0, below every value
+    w[u].x = live ? bf16x2_keys(w[u].x) : 0u;
+    w[u].y = live ? bf16x2_keys(w[u].y) : 0u;
+    w[u].z = live ? bf16x2_keys(w[u].z) : 0u;
+    w[u].w = live ? bf16x2_keys(w[u].w) : 0u;
+    mx = __builtin_elementwise_max(mx, __builtin_bit_cast(u16x2_t, w[u].x));
+    mx = __builtin_elementwise_max(mx, __builtin_bit_cast(u16x2_t, w[u].y));
+    mx = __builtin_elementwise_max(mx, __builtin_bit_cast(u16x2_t, w[u].z));
+    mx = __builtin_elementwise_max(mx, __builtin_bit_cast(u16x2_t, w[u].w));
+  }
+  const uint32_t tk = mx.x > mx.y ? mx.x : mx.y;
+  uint32_t k = wave_reduce_u32<true>(tk);
+  if (lane == 0) sk[wave] = k;
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) k = sk[i] > k ? sk[i] : k;
+  const uint32_t alt = k == 0x8000u ? 0x7FFFu : k;   // +0 is the maximum: -0 ties with it
+  uint32_t cand = 0xFFFFFFFFu;
+  if (tk == k || tk == alt) {
+#pragma unroll
+    for (int u = 0; u < kArgU; ++u) {
+      const uint32_t ws[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t key = (ws[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+        const uint32_t id = 8u * (uint32_t)(u * kNT + tid) + (uint32_t)e;
+        if (cand == 0xFFFFFFFFu && (key == k || key == alt) && u * kNT + tid < nch) cand = id;
+      }
+    }
+  }
+  cand = wave_reduce_u32<false>(cand);
+  __syncthreads();   // every wave has read sk
+  if (lane == 0) sk[wave] = cand;
+  __syncthreads();
+  uint32_t best = sk[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) best = sk[i] < best ? sk[i] : best;
+  __syncthreads();
+  const uint32_t bits = (k & 0x8000u) ? (k ^ 0x8000u) : (k ^ 0xFFFFu);
+  out_v = __uint_as_float(bits << 16);
+  out_i = (int)best;
+}
+
 // Arg-best (largest value, lowest id) of one logit row; result in every thread.
 template <int DT>
 __device__ void row_argbest(const void *logits, int64_t row, int vocab, float *sv, int *si,
@@ -34,6 +109,11 @@ __device__ void row_argbest(const void *logits, int64_t row, int vocab, float *s
   float bv = -INFINITY;
   int bi = INT32_MAX;
   const int64_t base = row * vocab;
+  if (DT == 1 && (vocab & 7) == 0 && vocab <= kArgMaxVocab) {
+    row_argbest_bf16(static_cast<const uint16_t *>(logits) + base, vocab, reinterpret_cast<uint32_t *>(si), out_v,
+                     out_i);
+    return;
+  }
   if (DT == 1 && (vocab & 7) == 0) {
     // All of this thread's 16-byte loads of a pass are issued before any compare.
     constexpr int U = 8;

@@ -24,19 +24,17 @@ __global__ __launch_bounds__(64) void kv_compact_kernel(CompactArgs a) {
   const int b = a.b0 + s;
   const int acc = a.accept_len[b];
   const int32_t *path = a.path + (int64_t)b * a.path_stride;
-  // Validate the device-produced path; an invalid one leaves the sequence untouched.
-  bool ok = acc >= 0 && acc < a.path_stride && acc < kMaxPath && acc < S.N && S.L + acc + 1 <= S.cap &&
-            path[0] == 0;
+  // The path entries are loaded together with accept_len (one memory latency),
+  // up to the row's stride.
+  const int np = min(kMaxPath, a.path_stride);
   int src[kMaxPath];
 #pragma unroll
-  for (int j = 0; j < kMaxPath; ++j) {
-    src[j] = 0;
-    if (ok && j <= acc) {
-      const int p = path[j];
-      ok = ok && p >= j && p < S.N && (j == 0 || p > src[j - 1]);
-      src[j] = p;
-    }
-  }
+  for (int j = 0; j < kMaxPath; ++j) src[j] = j < np ? path[j] : -1;
+  // Validate the device-produced path; an invalid one leaves the sequence untouched.
+  bool ok = acc >= 0 && acc < np && acc < S.N && S.L + acc + 1 <= S.cap && src[0] == 0;
+#pragma unroll
+  for (int j = 1; j < kMaxPath; ++j)
+    if (j <= acc) ok = ok && src[j] >= j && src[j] < S.N && src[j] > src[j - 1];
   if (!ok) return;
   uint32_t *slab = static_cast<uint32_t *>(which ? a.v : a.k) +
                    ((int64_t)kvh * a.cap_total + S.base) * a.row_dwords;

@@ -357,6 +357,64 @@ def test_acceptance_small_vocab_random(torch_cuda):
         assert checked > B // 2
 
 
+def _argbest_rows(rng, vocab, n):
+    """Logit rows (float32, exactly representable in bf16) that stress the arg-best order."""
+    rows = []
+    for r in range(n):
+        kind = r % 8
+        x = rng.standard_normal(vocab).astype(np.float32)
+        x = np.float32(synth.storage_to_f64(synth.to_bf16_bits(x), "bf16"))   # bf16 grid: ties at the max are common
+        if kind == 1:
+            x[-1] = 50.0                                   # max at the last id
+        elif kind == 2:
+            x[0] = 50.0                                    # max at the first id
+        elif kind == 3:
+            x[:] = 1.5                                     # all equal: id 0
+        elif kind == 4:
+            x = -np.abs(x) - 1.0
+            i, j = sorted(rng.choice(vocab, 2, replace=False))
+            x[i], x[j] = -0.0, 0.0                         # -0 first, +0 later: equal, lower id wins
+        elif kind == 5:
+            x = -np.abs(x) - 1.0
+            i, j = sorted(rng.choice(vocab, 2, replace=False))
+            x[i], x[j] = 0.0, -0.0
+        elif kind == 6:
+            x[:] = -np.inf                                 # all -inf: id 0
+        elif kind == 7:
+            top = x.max()
+            x[rng.choice(vocab, 5, replace=False)] = top   # several ties at the max
+        rows.append(x)
+    return np.stack(rows)
+
+
+@pytest.mark.parametrize("vocab", [8, 1000, 1004, 32000, 32768, 32776])
+def test_greedy_argbest_rows(torch_cuda, vocab):
+    """Single-node trees: next_tok is each row's arg-best (larger value, then lower id; -0 == +0)."""
+    import torch
+    from paper_2506_01986_amd import specmemo as sm
+    from paper_2506_01986_amd.runner import to_device
+    rng = np.random.default_rng(vocab)
+    B, stride = 48, 5
+    node_off = np.arange(B + 1, dtype=np.int32)
+    zeros = np.zeros(B, np.int32)
+    tr = sm.Trees(node_off, np.full(B, -1, np.int32), zeros, zeros, device="cuda")
+    raw = _argbest_rows(rng, vocab, B)
+    tok = torch.zeros(B, dtype=torch.int32, device="cuda")
+    for dtype in ("bf16", "fp32"):
+        say(f"argbest vocab={vocab} {dtype}")
+        lg = raw if dtype == "fp32" else synth.to_bf16_bits(raw)
+        dt = sm.FP32 if dtype == "fp32" else sm.BF16
+        dlg = to_device(lg, dtype, "cuda")
+        acc = torch.empty(B, dtype=torch.int32, device="cuda")
+        path = torch.empty((B, stride), dtype=torch.int32, device="cuda")
+        nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+        ws = torch.empty(sm.workspace_bytes(sm.WS_ACCEPT, dt, tr, None, sm.GREEDY), dtype=torch.uint8, device="cuda")
+        sm.accept(dt, tr, vocab, sm.GREEDY, dlg, tok, acc, path, stride, nxt, ws=ws, ws_bytes=ws.numel())
+        ra, rp, rn = oracle.accept_greedy(lg, np.zeros(B, np.int32), node_off, np.full(B, -1, np.int32), zeros, stride)
+        assert np.array_equal(nxt.cpu().numpy(), rn)
+        assert np.array_equal(acc.cpu().numpy(), ra) and np.array_equal(path.cpu().numpy(), rp)
+
+
 def test_run_to_run_determinism(torch_cuda):
     import torch
     from paper_2506_01986_amd import runner
