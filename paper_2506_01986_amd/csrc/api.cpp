@@ -146,6 +146,7 @@ struct AttnPlan {
   std::vector<std::vector<AttnSeq>> groups;   // sequences per launch, in launch order
   std::vector<int> items, citems;
   std::vector<std::vector<int>> xcd_cum;      // per launch: [8][nseq + 1]
+  std::vector<std::vector<int>> xcd_ccum;     // per launch: [8][nseq + 1], combine blocks
   size_t ws_bytes = 0;
 };
 
@@ -245,20 +246,27 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
       return (int64_t)(x.L + x.N) * y.nch > (int64_t)(y.L + y.N) * x.nch;
     });
     int item = 0, part = 0, citem = 0, unit = 0;
-    int per_xcd[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    std::vector<int> cum(8 * (grp.size() + 1), 0);
-    for (size_t si = 0; si < grp.size(); ++si) {
+    int per_xcd[8] = {0, 0, 0, 0, 0, 0, 0, 0}, cper_xcd[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    const size_t ns = grp.size();
+    std::vector<int> cum(8 * (ns + 1), 0), ccum(8 * (ns + 1), 0);
+    for (size_t si = 0; si < ns; ++si) {
       AttnSeq &s = grp[si];
-      for (int x = 0; x < 8; ++x) cum[x * (grp.size() + 1) + si] = per_xcd[x];
+      for (int x = 0; x < 8; ++x) {
+        cum[x * (ns + 1) + si] = per_xcd[x];
+        ccum[x * (ns + 1) + si] = cper_xcd[x];
+      }
       s.item0 = item;
       s.unit0 = unit;
-      const int units = kv->n_kv * s.nch;
-      for (int u = 0; u < units; ++u) per_xcd[(unit + u) & 7] += s.nrb;
-      unit += units;
-      item += units * s.nrb;
+      // unit (sequence, KV head) = all its chunks and row blocks, on XCD unit mod 8
+      for (int h = 0; h < kv->n_kv; ++h) {
+        per_xcd[(unit + h) & 7] += s.nch * s.nrb;
+        if (s.nch > 1) cper_xcd[(unit + h) & 7] += s.nrb;
+      }
+      unit += kv->n_kv;
+      item += kv->n_kv * s.nch * s.nrb;
       if (s.nch > 1) {
         s.part0 = part;
-        part += units * s.nrb;
+        part += kv->n_kv * s.nch * s.nrb;
         s.citem0 = citem;
         citem += kv->n_kv * s.nrb;
       } else {
@@ -266,13 +274,18 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
         s.citem0 = -1;
       }
     }
-    for (int x = 0; x < 8; ++x) cum[x * (grp.size() + 1) + grp.size()] = per_xcd[x];
+    for (int x = 0; x < 8; ++x) {
+      cum[x * (ns + 1) + ns] = per_xcd[x];
+      ccum[x * (ns + 1) + ns] = cper_xcd[x];
+    }
     p->xcd_cum.push_back(cum);
+    p->xcd_ccum.push_back(ccum);
     p->groups.push_back(grp);
-    // XCD order: XCD x runs units x, x + 8, ... (all their row blocks); the grid
-    // is padded to 8 x the busiest XCD's blocks, surplus blocks exit at once.
+    // XCD order: XCD x runs the units x, x + 8, ... with all their chunks and
+    // row blocks, and merges their chunks; each grid is padded to 8 x the
+    // busiest XCD's blocks, surplus blocks exit at once.
     p->items.push_back(p->xcd_order ? 8 * *std::max_element(per_xcd, per_xcd + 8) : item);
-    p->citems.push_back(citem);
+    p->citems.push_back(p->xcd_order ? 8 * *std::max_element(cper_xcd, cper_xcd + 8) : citem);
     p->ws_bytes = std::max(p->ws_bytes, (size_t)part * (size_t)pf * sizeof(float));
   }
 }
@@ -452,7 +465,10 @@ int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmem
     a.citems = p.citems[gi];
     a.xcd_order = p.xcd_order ? 1 : 0;
     for (int x = 0; x < 8; ++x)
-      for (int i = 0; i <= a.nseq; ++i) a.xcd_cum[x][i] = p.xcd_cum[gi][x * (a.nseq + 1) + i];
+      for (int i = 0; i <= a.nseq; ++i) {
+        a.xcd_cum[x][i] = p.xcd_cum[gi][x * (a.nseq + 1) + i];
+        a.xcd_ccum[x][i] = p.xcd_ccum[gi][x * (a.nseq + 1) + i];
+      }
     hipError_t e = launch_tree_attn_bf16(a, p.rb, st);
     if (e != hipSuccess) return hip_status(e, "tree attention launch");
   }

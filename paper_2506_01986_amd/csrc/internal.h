@@ -44,7 +44,7 @@ struct AttnSeq {
   int32_t item0;     // first work item of this sequence in the launch
   int32_t part0;     // first partial slot (multi-chunk sequences), -1 if none
   int32_t citem0;    // first combine item (multi-chunk sequences)
-  int32_t unit0;     // first (KV head, chunk) unit of this sequence in the launch
+  int32_t unit0;     // first (sequence, KV head) unit of this sequence in the launch
 };
 
 struct AttnArgs {
@@ -60,6 +60,7 @@ struct AttnArgs {
   int32_t nseq, items, citems;   // items: blocks of the launch (XCD order: padded)
   int32_t xcd_order;        // nonzero: consecutive work items share an XCD
   int32_t xcd_cum[8][kMaxSeqPerLaunch + 1];   // XCD order: blocks of XCD x before sequence s
+  int32_t xcd_ccum[8][kMaxSeqPerLaunch + 1];  // XCD order: combine blocks of XCD x before sequence s
   AttnSeq seq[kMaxSeqPerLaunch];
 };
 

@@ -78,11 +78,13 @@ __device__ __forceinline__ AttnSeq pick_seq(const AttnSeq &d, int s) {
 // Launch order: sequence, then KV head, chunk, row block.
 //
 // XCD order: blocks reach the eight XCDs round-robin by block id, so block
-// 8 k + x is the k-th block of XCD x.  A unit is one (sequence, KV head,
-// chunk) with all its row blocks, which read the same K/V; unit u (launch
-// order, longest sequences first) runs on XCD u mod 8, so those row blocks
-// share one L2 and every XCD gets long and short units alike.  xcd_cum[x][s]
-// is the number of XCD x's blocks before sequence s; blocks past the busiest
+// 8 k + x is the k-th block of XCD x.  A unit is one (sequence, KV head) with
+// all its chunks and row blocks; unit u (launch order, longest sequences
+// first) runs on XCD u mod 8, chunk by chunk with the row blocks of a chunk
+// adjacent, so the row blocks reading the same K/V share one L2, the chunk
+// partials are merged on the XCD that wrote them, and with 8 KV heads (or a
+// multiple) every XCD gets one KV head of every sequence.  xcd_cum[x][s] is
+// the number of XCD x's blocks before sequence s; blocks past the busiest
 // XCD's work are padding.
 __device__ __forceinline__ bool decode_item(const AttnArgs &a, int bid, Item &it, AttnSeq &S) {
   const int lane = threadIdx.x & 63;
@@ -96,13 +98,12 @@ __device__ __forceinline__ bool decode_item(const AttnArgs &a, int bid, Item &it
     const int s = find_seq(nseq, cum, k);
     S = pick_seq(mine, s);
     const int kk = k - rl(cum, s);
-    const int u0 = S.unit0;
-    const int first = u0 + ((x - (u0 & 7)) & 7);            // first unit >= u0 on XCD x
-    const int u = first + 8 * (kk / S.nrb) - u0;
+    const int per_unit = S.nch * S.nrb;
     it.s = s;
-    it.rb = kk % S.nrb;
-    it.ch = u % S.nch;
-    it.kvh = u / S.nch;
+    it.kvh = ((x - (S.unit0 & 7)) & 7) + 8 * (kk / per_unit);   // this sequence's KV heads on XCD x: first, +8, ...
+    const int local = kk % per_unit;
+    it.ch = local / S.nrb;
+    it.rb = local % S.nrb;
   } else {
     const int s = find_seq(nseq, mine.item0, bid);
     S = pick_seq(mine, s);
@@ -141,6 +142,15 @@ typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 // offset.  It is issued from inline assembly so that the compiler does not
 // guard later LDS reads with waits for it: the tile ring orders these loads
 // with explicit vmcnt waits.  M0 must be written one wait state before the load.
+// A wave-uniform pointer, made explicit for the compiler (so that it stays in
+// SGPRs, as the base operand of the direct loads requires).
+template <typename T>
+__device__ __forceinline__ T *uniform_ptr(T *p) {
+  const uint64_t b = reinterpret_cast<uintptr_t>(p);
+  return reinterpret_cast<T *>((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(b >> 32)) << 32 |
+                               (uint32_t)__builtin_amdgcn_readfirstlane((int)b));
+}
+
 __device__ __forceinline__ void lds_load16(const void *src, uint32_t off, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(src), "s"(lds_base)
                : "memory", "m0");
@@ -207,8 +217,8 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
     const int r = lrow0 + 4 * u;
     return is_k ? r * (D * 2) + 16 * (kx ^ ((4 * (wave * IPW + u)) & 15)) : voff0 + 1024 * u;
   };
-  const uint8_t *Kb = reinterpret_cast<const uint8_t *>(Kg);
-  const uint8_t *Vb = reinterpret_cast<const uint8_t *>(Vg);
+  const uint8_t *Kb = uniform_ptr(reinterpret_cast<const uint8_t *>(Kg));
+  const uint8_t *Vb = uniform_ptr(reinterpret_cast<const uint8_t *>(Vg));
   // Offsets are relative to the slab base (a slab is at most 2^24 rows, so they
   // fit 32 bits); the base of a full tile is wave-uniform.
   auto issue = [&](const uint8_t *src, bool is_k, uint8_t *dst, int j) {
@@ -464,14 +474,29 @@ template <int RB>
 __global__ __launch_bounds__(4 * RB) void tree_attn_combine(AttnArgs a) {
   constexpr int CPT = D / 4;   // columns per thread
   const int idx = blockIdx.x, lane = threadIdx.x & 63;
+  const int x = idx & 7, k = idx >> 3;
   AttnSeq mine{};
   if (lane < kMaxSeqPerLaunch) mine = a.seq[lane];
-  // the split sequence of this block: the last one whose first combine item is <= idx
-  const bool split_le = lane < a.nseq && mine.nch > 1 && mine.citem0 <= idx;
-  const int s = 63 - __builtin_clzll(__builtin_amdgcn_ballot_w64(split_le));
-  const AttnSeq S = pick_seq(mine, s);
-  const int local = idx - S.citem0;
-  const int kvh = local / S.nrb, rb = local % S.nrb;
+  const int ccum = lane <= kMaxSeqPerLaunch ? a.xcd_ccum[x][lane] : 0;
+  int kvh, rb;
+  AttnSeq S;
+  if (a.xcd_order) {
+    // the k-th combine item of XCD x, on the XCD that computed its chunks
+    if (k >= rl(ccum, a.nseq)) return;   // padding block
+    const int s = find_seq(a.nseq, ccum, k);
+    S = pick_seq(mine, s);
+    const int kk = k - rl(ccum, s);
+    kvh = ((x - (S.unit0 & 7)) & 7) + 8 * (kk / S.nrb);
+    rb = kk % S.nrb;
+  } else {
+    // the split sequence of this block: the last one whose first combine item is <= idx
+    const bool split_le = lane < a.nseq && mine.nch > 1 && mine.citem0 <= idx;
+    const int s = 63 - __builtin_clzll(__builtin_amdgcn_ballot_w64(split_le));
+    S = pick_seq(mine, s);
+    const int local = idx - S.citem0;
+    kvh = local / S.nrb;
+    rb = local % S.nrb;
+  }
   const int r = threadIdx.x >> 2, quarter = threadIdx.x & 3;
   const int row = rb * RB + r;
   if (row >= S.N * a.group) return;
