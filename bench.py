@@ -29,6 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense matrix bf16 / fp32 vector, published
 METRIC = "verified tree tokens/sec per verify step; achieved HBM GB/s vs peak"
 # Kernels each stage launches through the C ABI (for matching rocprofv3 traces).
 STAGE_KERNELS = {"medusa_topk": ["head_logits_packed", "topk_rows"],
@@ -86,6 +87,17 @@ def algorithmic_bytes(wl, acc):
     c = int(np.sum(acc + 1)) * cfg.vocab * s + sumN * 4
     d = 2 * int(np.sum(acc + 1)) * 2 * cfg.n_kv * cfg.head_dim * s
     return {"medusa_topk": a, "tree_attn": b, "accept": c, "kv_compact": d}
+
+
+def attention_flops(wl):
+    """QK^T and PV products of stage (b): 4 d per (query row, visible key); a
+    node at depth t sees its L_b committed keys and t + 1 tree rows."""
+    cfg = wl.cfg
+    keys = 0
+    for b in range(cfg.B):
+        n0, n1 = int(wl.node_off[b]), int(wl.node_off[b + 1])
+        keys += int(np.sum(int(wl.lens[b]) + wl.depth[n0:n1].astype(np.int64) + 1))
+    return 4 * cfg.head_dim * cfg.n_q * keys
 
 
 def cpu_baseline(wl, min_seconds=10.0, max_reps=20):
@@ -190,6 +202,22 @@ def main():
             ev[k][j + 1].record()
     torch.cuda.synchronize()
     per_stage = np.array([[ev[k][j].elapsed_time(ev[k][j + 1]) for j in range(4)] for k in range(args.steps)])
+    # Attention with cold caches: a 1 GiB write before each call evicts the
+    # pool from the 256 MB MALL (within the step loop it stays there: the head
+    # weights stream past it nontemporally).
+    print("[bench] attention with cold caches", file=sys.stderr, flush=True)
+    scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    cold_ev = []
+    for k in range(args.steps):
+        scratch.fill_(k & 0xFF)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        step.tree_attn()
+        e1.record()
+        cold_ev.append((e0, e1))
+    torch.cuda.synchronize()
+    cold = np.array([a.elapsed_time(b) for a, b in cold_ev])
+    del scratch
     acc = step.accept_len.cpu().numpy()
     byts = algorithmic_bytes(wl, acc)
     st = {}
@@ -199,6 +227,13 @@ def main():
         st[n] = {"ms": round(t, 5), "ms_p10": round(float(np.percentile(per_stage[:, j], 10)), 5),
                  "ms_p90": round(float(np.percentile(per_stage[:, j], 90)), 5),
                  "algorithmic_bytes": int(byts[n]), "GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+    fl = attention_flops(wl)
+    st["tree_attn"]["flops"] = fl
+    st["tree_attn"]["TFLOPs"] = round(fl / (st["tree_attn"]["ms"] * 1e-3) / 1e12, 1)
+    st["tree_attn"]["mfma_frac"] = round(st["tree_attn"]["TFLOPs"] / MFMA_PEAK_TFLOPS[cfg.dtype], 4)
+    tc = float(np.median(cold))
+    st["tree_attn"]["cold_caches"] = {"ms": round(tc, 5), "GBps": round(byts["tree_attn"] / (tc * 1e-3) / 1e9, 1),
+                                      "TFLOPs": round(fl / (tc * 1e-3) / 1e12, 1)}
     ab = byts["tree_attn"] + byts["kv_compact"]
     at = (per_stage[:, 1] + per_stage[:, 3]).mean()
     st["tree_attn+kv_compact"] = {"ms": round(float(at), 5), "GBps": round(ab / (at * 1e-3) / 1e9, 1),
