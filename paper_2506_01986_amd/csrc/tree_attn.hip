@@ -33,11 +33,7 @@ namespace {
 
 constexpr int D = kAttnHeadDim;
 constexpr int TK = kAttnKeyTile;
-constexpr float kRescaleSlack = 8.f;
-#ifndef SPECMEMO_PP_SLOTS
-#define SPECMEMO_PP_SLOTS 4
-#endif
-constexpr int kPingPongSlots = SPECMEMO_PP_SLOTS;   // ring depth of the 256-row ping-pong kernel   // log2 units: softmax weights stay <= 256 between rescales
+constexpr float kRescaleSlack = 8.f;   // log2 units: softmax weights stay <= 256 between rescales
 
 struct Item {
   int s, kvh, rb, ch;
@@ -182,9 +178,10 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   constexpr int IPW = TILE / 1024 / WAVES;    // 1 KB direct loads per wave per tile and operand
   __shared__ __attribute__((aligned(1024))) uint8_t kring[SLOTS][TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t vring[SLOTS][TILE];
-  __shared__ __attribute__((aligned(16))) uint32_t anc[kMaxNodes][4];
-  __shared__ int par[kMaxNodes];
-  static_assert(WAVES * 64 >= kMaxNodes, "one thread per tree node");
+  // The tree's parent array is staged in the last V slot, which the prologue
+  // does not fill and the first loop barrier frees again.
+  int *const par = reinterpret_cast<int *>(vring[SLOTS - 1]);
+  static_assert(WAVES * 64 >= kMaxNodes && kMaxNodes * 4 <= TILE, "one thread per tree node");
 
   Item it;
   AttnSeq S;
@@ -269,22 +266,16 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   for (int ks = 0; ks < D / 16; ++ks) asm volatile("" ::"v"(qf[ks]));
   ring_barrier();
 
-  // Ancestor-or-self bitmask of every node of this tree (local ids), walked in
-  // LDS; the masks are read after the first barrier of the tile loop.
-  if (tid < N) {
-    uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
-    for (int u = tid; u >= 0; u = par[u]) {
-      const uint32_t bit = 1u << (u & 31);
-      const int w = u >> 5;
-      m0 |= w == 0 ? bit : 0u;
-      m1 |= w == 1 ? bit : 0u;
-      m2 |= w == 2 ? bit : 0u;
-      m3 |= w == 3 ? bit : 0u;
-    }
-    anc[tid][0] = m0;
-    anc[tid][1] = m1;
-    anc[tid][2] = m2;
-    anc[tid][3] = m3;
+  // Ancestor-or-self bitmask of this lane's node (local ids), walked in LDS
+  // and kept in registers.
+  uint4 anc = {0u, 0u, 0u, 0u};
+  for (int u = node; u >= 0; u = par[u]) {
+    const uint32_t bit = 1u << (u & 31);
+    const int w = u >> 5;
+    anc.x |= w == 0 ? bit : 0u;
+    anc.y |= w == 1 ? bit : 0u;
+    anc.z |= w == 2 ? bit : 0u;
+    anc.w |= w == 3 ? bit : 0u;
   }
 
   // K operand: row (lane & 31) of a 32-key sub-block, 16-byte chunk 2 ks + h.
@@ -340,8 +331,7 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   auto softmax_head = [&](int j, f32x16 (&Sc)[2]) {   // mask, tile max, rescaling
     const int kt = k0 + j * TK;
     if (kt + TK > min(k1, L)) {
-      const uint4 an = *reinterpret_cast<const uint4 *>(anc[node]);   // ancestor words of this row's node
-      const uint64_t alo = (uint64_t)an.y << 32 | an.x, ahi = (uint64_t)an.w << 32 | an.z;
+      const uint64_t alo = (uint64_t)anc.y << 32 | anc.x, ahi = (uint64_t)anc.w << 32 | anc.z;
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
