@@ -218,6 +218,22 @@ def main():
     torch.cuda.synchronize()
     cold = np.array([a.elapsed_time(b) for a, b in cold_ev])
     del scratch
+    # The same step captured once in a HIP graph and replayed K times (no
+    # per-launch host work; the kernels and their arguments are those above).
+    print("[bench] graph replay", file=sys.stderr, flush=True)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step.run()
+    graph.replay()
+    torch.cuda.synchronize()
+    g_begin, g_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g_begin.record()
+    for _ in range(args.steps):
+        graph.replay()
+    g_end.record()
+    torch.cuda.synchronize()
+    graph_ms = g_begin.elapsed_time(g_end) / args.steps
+    del graph
     acc = step.accept_len.cpu().numpy()
     byts = algorithmic_bytes(wl, acc)
     st = {}
@@ -261,6 +277,7 @@ def main():
         "accepted_tokens_per_s": round(float(np.sum(acc + 1)) / (ms * 1e-3), 1),
         "wall_ms_per_step": round(wall / args.steps * 1e3, 5),
         "ms_per_step_with_stage_events": round(float(per_stage.sum(axis=1).mean()), 5),
+        "graph": {"ms_per_step": round(graph_ms, 5), "value": round(wl.total_nodes / (graph_ms * 1e-3), 1)},
         "stages": st,
     }
     if not args.no_cpu_baseline:

@@ -415,6 +415,52 @@ def test_greedy_argbest_rows(torch_cuda, vocab):
         assert np.array_equal(acc.cpu().numpy(), ra) and np.array_equal(path.cpu().numpy(), rp)
 
 
+def test_graph_replay(torch_cuda):
+    """The four calls of a step captured in one HIP graph.  Every replay, with
+    eager work between replays (the pool restored, every output poisoned),
+    reproduces the eager step bit for bit: no call records a memset, an
+    allocation or a host synchronisation, and the kernels read nothing that
+    capture freezes except their arguments."""
+    import torch
+    from paper_2506_01986_amd import runner
+    rng = np.random.default_rng(21)
+    cfg = edge_cfg(B=5, n_q=8, n_kv=2, hidden=256, vocab=3000, seed=21)
+    trees = [synth.t64(), synth.t16(), synth.random_tree(rng, 40), synth.chain_tree(5), synth.random_tree(rng, 100)]
+    wl = synth.make(cfg, trees=trees, lens=[900, 0, 300, 2500, 64])
+    step = runner.VerifyStep(wl)
+    step.medusa_topk()
+    torch.cuda.synchronize()
+    step.set_base_logits(synth.planted_logits(wl, step.node_tok.cpu().numpy()))
+    k0, v0, len0 = step.k.clone(), step.v.clone(), step.seq_len.clone()
+    outs = [step.topk_ids, step.node_tok, step.out, step.accept_len, step.path, step.next_tok, step.seq_len,
+            step.k, step.v]
+
+    def restore_and_poison():
+        step.k.copy_(k0)
+        step.v.copy_(v0)
+        step.seq_len.copy_(len0)
+        for t in (step.topk_ids, step.node_tok, step.accept_len, step.path, step.next_tok):
+            t.fill_(-7)
+        step.out.zero_()
+
+    restore_and_poison()
+    step.run()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in outs]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step.run()
+    torch.cuda.synchronize()
+    for r in range(3):
+        say(f"graph replay {r}")
+        restore_and_poison()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(ref, outs)):   # bits: the pool's canary rows hold NaN patterns
+            assert torch.equal(a.contiguous().view(torch.uint8), b.contiguous().view(torch.uint8)), (r, i)
+
+
 def test_run_to_run_determinism(torch_cuda):
     import torch
     from paper_2506_01986_amd import runner
