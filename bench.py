@@ -144,6 +144,50 @@ def _oracle_step(wl):
     return float(stages.sum()), stages
 
 
+def budget_report(cfg, wl, device_bytes, reps=2000):
+    """The memory model and Alg. 1's plan for the workload's model on this
+    device (host calls of the library), with their host times and the
+    oracle's time for the same plans."""
+    from oracle import budget as ob
+    from paper_2506_01986_amd import specmemo as sm
+    tree = (wl.trees[0].parent, wl.trees[0].depth, wl.trees[0].rank)
+    model = dict(base_model_bytes=cfg.params * cfg.elem_bytes, head_bytes=cfg.hidden * cfg.vocab * cfg.elem_bytes,
+                 layers=cfg.layers, n_kv=cfg.n_kv, head_dim=cfg.head_dim, vocab=cfg.vocab,
+                 elem_bytes=cfg.elem_bytes, query_count=1, query_length=int(cfg.kv_len[1]),
+                 default_heads=cfg.n_heads)
+    plan = sm.plan_budget(device_bytes, batch=cfg.B, default_tree=tree, **model)
+    # the largest batch of full-length sequences that keeps the default tree and heads
+    lo, hi = 0, 1 << 20
+    while lo < hi:
+        mid = (lo + hi + 1) // 2
+        ok = sm.plan_budget(device_bytes, batch=mid, default_tree=tree, **model)["kind"] == sm.PLAN_DEFAULT
+        lo, hi = (mid, hi) if ok else (lo, mid - 1)
+    # timing: the plan that fits at once and the one that searches every pruning
+    timings = {}
+    for name, mem in (("fits", device_bytes), ("exhaustive", 0)):
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            sm.plan_budget(mem, batch=cfg.B, default_tree=tree, **model)
+        lib_us = (time.perf_counter() - t0) / reps * 1e6
+        t0 = time.perf_counter()
+        n_or = max(1, reps // 100)
+        for _ in range(n_or):
+            ob.plan_budget(mem, batch=cfg.B, default_tree=tuple(map(list, tree)), **model)
+        timings[name] = {"lib_us": round(lib_us, 2), "oracle_us": round((time.perf_counter() - t0) / n_or * 1e6, 1)}
+    sizes = sm.plan_tree_sizes(wl.lens, wl.seq_cap, int(wl.trees[0].n))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        sm.plan_tree_sizes(wl.lens, wl.seq_cap, int(wl.trees[0].n))
+    sizes_us = (time.perf_counter() - t0) / reps * 1e6
+    per_layer_pool = 2 * wl.cap_total * cfg.n_kv * cfg.head_dim * cfg.elem_bytes
+    return {"device_bytes": int(device_bytes), "model_bytes": model["base_model_bytes"],
+            "head_bytes": model["head_bytes"], "plan": plan, "max_batch_default_tree": lo,
+            "plan_time": timings, "tree_sizes": [int(x) for x in sizes], "tree_sizes_us": round(sizes_us, 2),
+            "pool_bytes_all_layers": int(per_layer_pool * cfg.layers),
+            "eq1_bytes_live_tokens": sm.mem_kv_bytes(cfg.layers, 1, cfg.n_kv, cfg.head_dim,
+                                                     int(np.sum(wl.lens) + wl.total_nodes), cfg.elem_bytes)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -280,6 +324,9 @@ def main():
         "graph": {"ms_per_step": round(graph_ms, 5), "value": round(wl.total_nodes / (graph_ms * 1e-3), 1)},
         "stages": st,
     }
+    if cfg.params:
+        print("[bench] memory budget plan (host)", file=sys.stderr, flush=True)
+        result["budget"] = budget_report(cfg, wl, torch.cuda.get_device_properties(0).total_memory)
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(wl)

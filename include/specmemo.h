@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SPECMEMO_ABI_VERSION 2
+#define SPECMEMO_ABI_VERSION 3
 #define SPECMEMO_MAX_TREE_NODES 128 /* nodes per sequence's tree */
 #define SPECMEMO_MAX_DEPTH 15       /* tree depth (= Medusa heads) */
 #define SPECMEMO_MAX_TOPK 32        /* top-k per head */
@@ -211,6 +211,138 @@ int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab,
 int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
                         const int32_t *accept_len, const int32_t *path, int32_t path_stride,
                         void *stream);
+
+/* ---- Memory budget and tree construction (host only) -------------------------
+ *
+ * SpecMemo's memory model (Sec. 3.1, Eq. 1-6) and its tree construction
+ * (Sec. 3.2 and Alg. 1) as plain host functions: they make no HIP call, read
+ * and write host memory only, and may run on any thread.  Byte counts are
+ * int64; a result that would overflow int64 is reported as an error.
+ *
+ * Trees given to or returned by these calls are in breadth-first order: node 0
+ * is the root (parent -1, depth 0, rank 0); for n > 0, 0 <= parent[n] < n,
+ * depth[n] = depth[parent[n]] + 1, and the triples (depth, parent, rank)
+ * strictly increase with n.  Every prefix of such a tree is a tree.  Rank is
+ * the node's index into head depth[n]'s top-k list, so the leftmost nodes of a
+ * level carry the most probable tokens (Sec. 3.2, Fig. 10). */
+
+/* Eq. 1, with the per-head dimension d that the equation's legend defines:
+ * bytes of K and V for `tokens` cached positions of every layer, sequence and
+ * KV head, 2 * layers * batch * n_kv * head_dim * tokens * elem_bytes.
+ * Arguments must be >= 0 (elem_bytes >= 1).  Returns -1 on a negative
+ * argument or overflow (specmemo_last_error says which). */
+int64_t specmemo_mem_kv_bytes(int32_t layers, int32_t batch, int32_t n_kv, int32_t head_dim, int64_t tokens,
+                              int32_t elem_bytes);
+
+/* Eq. 3 times the precision: runtime buffers of the verification step,
+ * elem_bytes * (b*N*w + b*S*l*w + b*S*l*l*w) with b = batch, N = nodes,
+ * S = seqs (leaves: candidate sequences), l = levels (Medusa heads),
+ * w = vocab.  Returns -1 on a negative argument or overflow. */
+int64_t specmemo_mem_buffer_bytes(int32_t batch, int32_t nodes, int32_t seqs, int32_t levels, int32_t vocab,
+                                  int32_t elem_bytes);
+
+/* Eq. 4-6: total device memory, base_model_bytes + heads * head_bytes + kv +
+ * buffers (Eq. 6 applies the precision once, inside each term).  Returns -1
+ * on a negative argument or overflow. */
+int64_t specmemo_mem_total_bytes(int64_t base_model_bytes, int64_t head_bytes, int32_t heads, int64_t kv,
+                                 int64_t buffers);
+
+/* Eq. 2: nodes of the full tree of the given arity with `levels` levels below
+ * the root, sum_{i=0..levels} arity^i.  Returns -1 if arity < 1, levels < 0
+ * or the count overflows. */
+int64_t specmemo_tree_full_nodes(int32_t arity, int32_t levels);
+
+/* Building a tree from its features (Sec. 3.2 and Alg. 1's custom tree): a
+ * breadth-first tree with exactly `nodes` nodes and `leaves` leaves (the
+ * candidate sequences), depth <= max_depth and at most `arity` children per
+ * node.  The paper gives no construction; this one keeps
+ * min(arity, leaves, nodes - 1) nodes at level 1 (all k tokens when the leaf
+ * count allows, Sec. 3.2), then gives children to leaves in breadth-first
+ * order (shallowest, then leftmost), the first of them the most, so the tree
+ * is wide at the top and its leftmost branches are the deepest.  It succeeds
+ * whenever some tree with these features, depth and arity exists.
+ * parent/depth/rank: host int32 [nodes], written on success only.
+ * Returns SPECMEMO_OK; SPECMEMO_E_ARG for nodes outside 1..2^24, leaves < 1,
+ * max_depth < 0, arity < 1 or a NULL output; SPECMEMO_E_TREE when no such
+ * tree exists. */
+int specmemo_tree_build(int32_t nodes, int32_t leaves, int32_t max_depth, int32_t arity, int32_t *parent,
+                        int32_t *depth, int32_t *rank);
+
+/* Leaves of a breadth-first tree (its candidate sequences, Sec. 3.1), or -1
+ * if the arrays break the conventions above (host arrays [n], n >= 1). */
+int32_t specmemo_tree_leaves(int32_t n, const int32_t *parent, const int32_t *depth, const int32_t *rank);
+
+/* Right-to-left pruning of a mask (Sec. 3.2): at depth d >= 1 keep the
+ * keep[d-1] leftmost nodes whose parents are kept (depths past n_keep keep
+ * none); the rightmost nodes of each level go first.  Per-level counts are
+ * what a pruning-rate schedule (Figs. 6/7) produces; the paper's logistic
+ * schedule is given only as a plot, so its counts are the caller's.
+ * Input: a breadth-first tree of n nodes (host).  Output: the kept nodes in
+ * the same order, parents renumbered, depths and ranks unchanged, in host
+ * arrays of n entries; *n_out = kept nodes.  The output arrays may be the
+ * input arrays themselves (pruning in place), but may not overlap them
+ * otherwise.
+ * Returns SPECMEMO_OK, SPECMEMO_E_ARG (n < 1, n_keep < 0, a negative keep
+ * count, NULL pointers) or SPECMEMO_E_TREE (the input breaks the conventions).
+ * Pruning a breadth-first tree to its first m nodes is the same operation with
+ * only the deepest kept level cut, which is why the planners below return a
+ * node count: the planned tree is that prefix. */
+int specmemo_tree_prune(int32_t n, const int32_t *parent, const int32_t *depth, const int32_t *rank,
+                        int32_t n_keep, const int32_t *keep, int32_t *n_out, int32_t *parent_out,
+                        int32_t *depth_out, int32_t *rank_out);
+
+/* The model, device and workload that Alg. 1 plans for. */
+typedef struct {
+  int64_t max_memory;         /* device bytes available */
+  int64_t base_model_bytes;   /* Eq. 5: parameters x precision */
+  int64_t head_bytes;         /* Eq. 4: one Medusa head */
+  int32_t layers;             /* Eq. 1: h */
+  int32_t n_kv;               /* Eq. 1: k, KV heads */
+  int32_t head_dim;           /* Eq. 1: d */
+  int32_t vocab;              /* Eq. 3: w */
+  int32_t elem_bytes;         /* p, bytes per element of KV and buffers */
+  int32_t batch;              /* b */
+  int32_t query_count;        /* Eq. 1: n queries ... */
+  int32_t query_length;       /* ... of m tokens each: the minimum cache */
+  int32_t default_heads;      /* heads of the default configuration */
+} specmemo_budget;
+
+#define SPECMEMO_PLAN_DEFAULT 0     /* default tree and heads fit */
+#define SPECMEMO_PLAN_PRUNED 1      /* default heads, tree pruned */
+#define SPECMEMO_PLAN_FEWER_HEADS 2 /* fewer heads (>= 2), tree cut to them and pruned */
+#define SPECMEMO_PLAN_NONE (-1)     /* nothing fits: Alg. 1 would quantise the base model */
+
+typedef struct {
+  int32_t kind;               /* SPECMEMO_PLAN_* */
+  int32_t heads;              /* Medusa heads = tree levels (0 for NONE) */
+  int32_t nodes;              /* the planned tree is the default tree's first `nodes` nodes */
+  int32_t leaves;             /* its candidate sequences */
+  int64_t kv_bytes;           /* Eq. 1 for query_count x query_length tokens */
+  int64_t total_bytes;        /* Eq. 6 of the plan (0 for NONE) */
+} specmemo_budget_plan;
+
+/* Alg. 1 without its quantisation step.  The minimum cache is Eq. 1 for
+ * query_count x query_length tokens.  If the default tree with default_heads
+ * fits max_memory (Eq. 6), that is the plan.  Otherwise, for heads h from
+ * default_heads down to 2 (every one-head tree has the same shape, appendix), the
+ * default tree cut to depth h is pruned right to left one node at a time
+ * (down to 2 nodes) and the first, largest, tree that fits is the plan.
+ * default tree: breadth-first, host [n], depth <= default_heads.
+ * Returns SPECMEMO_OK with *out filled (kind NONE when nothing fits);
+ * SPECMEMO_E_ARG for NULL pointers, default_heads < 2, non-positive sizes
+ * (max_memory, base and head bytes may be 0) or overflow; SPECMEMO_E_TREE for
+ * a bad default tree. */
+int specmemo_plan_budget(const specmemo_budget *m, int32_t n, const int32_t *parent, const int32_t *depth,
+                         const int32_t *rank, specmemo_budget_plan *out);
+
+/* Per-sequence tree sizes under the KV budget (Sec. 3.1, KV-cache paragraph):
+ * nodes_out[b] = max(0, min(default_nodes, seq_cap[b] - seq_len[b])), the
+ * largest right-to-left pruning of the default tree whose K/V rows fit the
+ * slab's free rows this step; 0 means the slab is full.  Host arrays [B].
+ * Returns SPECMEMO_OK, or SPECMEMO_E_ARG (B < 0, default_nodes outside
+ * 1..SPECMEMO_MAX_TREE_NODES, NULL arrays, seq_len[b] < 0 or seq_cap[b] < 0). */
+int specmemo_plan_tree_sizes(int32_t B, const int32_t *seq_len_h, const int32_t *seq_cap_h, int32_t default_nodes,
+                             int32_t *nodes_out);
 
 #define SPECMEMO_WS_TOPK 0
 #define SPECMEMO_WS_ATTN 1

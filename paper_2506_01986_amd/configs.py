@@ -31,6 +31,8 @@ class Config:
     p_range: Tuple[float, float] = (0.6, 0.6)
     w_std: float = 0.02                 # head-weight std
     seed: int = 0
+    layers: int = 1                     # decoder layers of the model the shapes come from
+    params: int = 0                     # its parameter count (memory model only; 0: not a real model)
 
     @property
     def elem_bytes(self) -> int:
@@ -53,23 +55,24 @@ TINY_FP32 = Config(
 LLAMA2_7B = Config(
     name="llama2_7b_b1", dtype="bf16", B=1, n_q=32, n_kv=32, head_dim=128, hidden=4096,
     vocab=32000, n_heads=4, topk=(10, 10, 10, 10), tree="T64", kv_len=(1024, 1024),
-    kv_len_dist="fixed", pool="exact", p_accept=0.6, seed=1)
+    kv_len_dist="fixed", pool="exact", p_accept=0.6, seed=1, layers=32, params=6_738_415_616)
 
 LLAMA2_13B = Config(
     name="llama2_13b_b4", dtype="bf16", B=4, n_q=40, n_kv=40, head_dim=128, hidden=5120,
     vocab=32000, n_heads=4, topk=(10, 10, 10, 10), tree="T64", kv_len=(512, 2048),
-    kv_len_dist="uniform", pool="exact", p_accept=0.6, seed=2)
+    kv_len_dist="uniform", pool="exact", p_accept=0.6, seed=2, layers=40, params=13_015_864_320)
 
 LLAMA2_70B = Config(
     name="llama2_70b_b10", dtype="bf16", B=10, n_q=64, n_kv=8, head_dim=128, hidden=8192,
     vocab=32000, n_heads=4, topk=(10, 10, 10, 10), tree="T64", kv_len=(512, 4096),
-    kv_len_dist="uniform", pool="cap1.1", p_accept=0.6, seed=3)
+    kv_len_dist="uniform", pool="cap1.1", p_accept=0.6, seed=3, layers=80, params=68_976_648_192)
 
 STRESS = Config(
     name="stress_b32", dtype="bf16", B=32, n_q=64, n_kv=8, head_dim=128, hidden=8192,
     vocab=32000, n_heads=4, topk=(10, 10, 10, 10), tree="random",
     tree_sizes=(8, 16, 32, 64, 128), kv_len=(256, 16384), kv_len_dist="loguniform",
-    pool="fixed1.1", p_accept=None, p_range=(0.3, 0.8), seed=4)
+    pool="fixed1.1", p_accept=None, p_range=(0.3, 0.8), seed=4, layers=80,
+    params=68_976_648_192)
 
 ALL = (TINY_FP32, LLAMA2_7B, LLAMA2_13B, LLAMA2_70B, STRESS)
 BY_NAME = {c.name: c for c in ALL}

@@ -19,11 +19,10 @@
 using namespace specmemo;
 
 namespace {
-
 thread_local std::string g_err;
+}  // namespace
 
-int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
-int fail(int code, const char *fmt, ...) {
+int specmemo::fail(int code, const char *fmt, ...) {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
@@ -33,10 +32,12 @@ int fail(int code, const char *fmt, ...) {
   return code;
 }
 
-int ok() {
+int specmemo::ok() {
   g_err.clear();
   return SPECMEMO_OK;
 }
+
+namespace {
 
 bool al(const void *p, uintptr_t a) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 

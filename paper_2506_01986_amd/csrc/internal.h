@@ -13,6 +13,11 @@ constexpr int kMaxPath = 16;           // max depth + 1
 constexpr int kMaxTopk = 32;
 constexpr int kMaxHeads = 15;
 
+// Error reporting of the C ABI: `fail` records the message that
+// specmemo_last_error returns and passes `code` through; `ok` clears it.
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int ok();
+
 // ---- head projection + top-k -------------------------------------------------
 struct TopkArgs {
   const float *z;          // [B][n_heads][vocab] fp32 logits

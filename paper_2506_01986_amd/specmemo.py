@@ -46,6 +46,20 @@ class _KV(C.Structure):
                 ("seq_cap_h", C.c_void_p), ("seq_len_h", C.c_void_p)]
 
 
+class _Budget(C.Structure):
+    _fields_ = [("max_memory", C.c_int64), ("base_model_bytes", C.c_int64), ("head_bytes", C.c_int64),
+                ("layers", C.c_int32), ("n_kv", C.c_int32), ("head_dim", C.c_int32), ("vocab", C.c_int32),
+                ("elem_bytes", C.c_int32), ("batch", C.c_int32), ("query_count", C.c_int32),
+                ("query_length", C.c_int32), ("default_heads", C.c_int32)]
+
+
+class _BudgetPlan(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("heads", C.c_int32), ("nodes", C.c_int32), ("leaves", C.c_int32),
+                ("kv_bytes", C.c_int64), ("total_bytes", C.c_int64)]
+
+
+PLAN_DEFAULT, PLAN_PRUNED, PLAN_FEWER_HEADS, PLAN_NONE = 0, 1, 2, -1
+
 _lib = None
 
 
@@ -72,6 +86,24 @@ def load():
         lib.specmemo_abi_version.restype = C.c_int32
         for f in ("specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"):
             getattr(lib, f).restype = C.c_int
+        i64 = C.c_int64
+        lib.specmemo_mem_kv_bytes.argtypes = [i32, i32, i32, i32, i64, i32]
+        lib.specmemo_mem_buffer_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
+        lib.specmemo_mem_total_bytes.argtypes = [i64, i64, i32, i64, i64]
+        lib.specmemo_tree_full_nodes.argtypes = [i32, i32]
+        for f in ("specmemo_mem_kv_bytes", "specmemo_mem_buffer_bytes", "specmemo_mem_total_bytes",
+                  "specmemo_tree_full_nodes"):
+            getattr(lib, f).restype = i64
+        lib.specmemo_tree_build.argtypes = [i32, i32, i32, i32, vp, vp, vp]
+        lib.specmemo_tree_build.restype = C.c_int
+        lib.specmemo_tree_leaves.argtypes = [i32, vp, vp, vp]
+        lib.specmemo_tree_leaves.restype = i32
+        lib.specmemo_tree_prune.argtypes = [i32, vp, vp, vp, i32, vp, vp, vp, vp, vp]
+        lib.specmemo_tree_prune.restype = C.c_int
+        lib.specmemo_plan_budget.argtypes = [C.POINTER(_Budget), i32, vp, vp, vp, C.POINTER(_BudgetPlan)]
+        lib.specmemo_plan_budget.restype = C.c_int
+        lib.specmemo_plan_tree_sizes.argtypes = [i32, vp, vp, i32, vp]
+        lib.specmemo_plan_tree_sizes.restype = C.c_int
         _lib = lib
     return _lib
 
@@ -206,3 +238,74 @@ def kv_compact(dt: int, trees: Trees, kv: KVPool, accept_len, path, path_stride:
     ts, ks = trees.struct(), kv.struct()
     _check(load().specmemo_kv_compact(dt, C.byref(ts), C.byref(ks), _ptr(accept_len), _ptr(path), path_stride,
                                       _stream(stream)))
+
+
+# ---- memory budget and tree construction (host) ------------------------------
+
+def _bytes(v: int) -> int:
+    if v < 0:
+        raise SpecmemoError(-1, load().specmemo_last_error().decode())
+    return int(v)
+
+
+def mem_kv_bytes(layers: int, batch: int, n_kv: int, head_dim: int, tokens: int, elem_bytes: int) -> int:
+    return _bytes(load().specmemo_mem_kv_bytes(layers, batch, n_kv, head_dim, tokens, elem_bytes))
+
+
+def mem_buffer_bytes(batch: int, nodes: int, seqs: int, levels: int, vocab: int, elem_bytes: int) -> int:
+    return _bytes(load().specmemo_mem_buffer_bytes(batch, nodes, seqs, levels, vocab, elem_bytes))
+
+
+def mem_total_bytes(base_model_bytes: int, head_bytes: int, heads: int, kv: int, buffers: int) -> int:
+    return _bytes(load().specmemo_mem_total_bytes(base_model_bytes, head_bytes, heads, kv, buffers))
+
+
+def tree_full_nodes(arity: int, levels: int) -> int:
+    return _bytes(load().specmemo_tree_full_nodes(arity, levels))
+
+
+def tree_build(nodes: int, leaves: int, max_depth: int, arity: int):
+    """(parent, depth, rank) int32 arrays of the built tree."""
+    out = [np.zeros(max(nodes, 1), np.int32) for _ in range(3)]
+    _check(load().specmemo_tree_build(nodes, leaves, max_depth, arity, *(a.ctypes.data for a in out)))
+    return tuple(out)
+
+
+def tree_leaves(parent, depth, rank) -> int:
+    p, d, r = _i32(parent), _i32(depth), _i32(rank)
+    s = load().specmemo_tree_leaves(len(p), p.ctypes.data, d.ctypes.data, r.ctypes.data)
+    if s < 0:
+        raise SpecmemoError(-3, load().specmemo_last_error().decode())
+    return int(s)
+
+
+def tree_prune(parent, depth, rank, keep: Sequence[int]):
+    """Right-to-left pruning with per-level keep counts; (parent, depth, rank) of the kept nodes."""
+    p, d, r, k = _i32(parent), _i32(depth), _i32(rank), _i32(keep)
+    n = len(p)
+    out = [np.zeros(max(n, 1), np.int32) for _ in range(3)]
+    m = C.c_int32(0)
+    _check(load().specmemo_tree_prune(n, p.ctypes.data, d.ctypes.data, r.ctypes.data, len(k),
+                                      k.ctypes.data if len(k) else None, C.addressof(m),
+                                      *(a.ctypes.data for a in out)))
+    return tuple(a[:m.value].copy() for a in out)
+
+
+def plan_budget(max_memory: int, base_model_bytes: int, head_bytes: int, layers: int, n_kv: int, head_dim: int,
+                vocab: int, elem_bytes: int, batch: int, query_count: int, query_length: int, default_heads: int,
+                default_tree) -> dict:
+    """Alg. 1 without quantisation: dict(kind, heads, nodes, leaves, kv_bytes, total_bytes)."""
+    parent, depth, rank = (_i32(a) for a in default_tree)
+    m = _Budget(max_memory, base_model_bytes, head_bytes, layers, n_kv, head_dim, vocab, elem_bytes, batch,
+                query_count, query_length, default_heads)
+    out = _BudgetPlan()
+    _check(load().specmemo_plan_budget(C.byref(m), len(parent), parent.ctypes.data, depth.ctypes.data,
+                                       rank.ctypes.data, C.byref(out)))
+    return {f: int(getattr(out, f)) for f, _ in _BudgetPlan._fields_}
+
+
+def plan_tree_sizes(seq_len, seq_cap, default_nodes: int) -> np.ndarray:
+    ln, cp = _i32(seq_len), _i32(seq_cap)
+    out = np.zeros(max(len(ln), 1), np.int32)
+    _check(load().specmemo_plan_tree_sizes(len(ln), ln.ctypes.data, cp.ctypes.data, default_nodes, out.ctypes.data))
+    return out[:len(ln)]

@@ -301,11 +301,13 @@ def plant_walks(trees: List[Tree], p: np.ndarray, rng: np.random.Generator):
 
 
 def make(cfg: Config, seed: int | None = None, with_heads: bool = True,
-         trees: List[Tree] | None = None, lens: Sequence[int] | None = None) -> Workload:
+         trees: List[Tree] | None = None, lens: Sequence[int] | None = None,
+         caps: Sequence[int] | None = None) -> Workload:
     """Build the workload of ``cfg`` from ``seed`` (default: the config's).
 
-    ``trees`` / ``lens`` override the drawn ones (used by special-case tests);
-    ``with_heads=False`` skips the head weights.
+    ``trees`` / ``lens`` / ``caps`` (slab rows) override the drawn or derived
+    ones (used by special-case tests); ``with_heads=False`` skips the head
+    weights.
     """
     seed = cfg.seed if seed is None else seed
     ss = dict(zip(STREAMS, np.random.SeedSequence(seed).spawn(len(STREAMS))))
@@ -330,7 +332,8 @@ def make(cfg: Config, seed: int | None = None, with_heads: bool = True,
     root_tok = rng["root"].integers(0, cfg.vocab, size=B).astype(np.int32)
     q = _store(normals(ss["q"], sumN * cfg.n_q * d), dt).reshape(sumN, cfg.n_q, d)
 
-    caps = _caps(cfg, L, sizes)
+    caps = _caps(cfg, L, sizes) if caps is None else np.asarray(caps, np.int32)
+    assert np.all(caps.astype(np.int64) >= L.astype(np.int64) + sizes), "a slab must hold its tree"
     base = np.zeros(B, dtype=np.int64)
     row = 1                                   # canary row 0
     for b in range(B):

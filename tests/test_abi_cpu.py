@@ -31,7 +31,7 @@ def test_library_loads_and_exports_every_declared_function():
     assert {"specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert sm.abi_version() == 2
+    assert sm.abi_version() == 3
 
 
 class FakeTrees(sm.Trees):
@@ -173,3 +173,23 @@ def test_last_error_cleared_by_success_is_thread_local():
     th.join()
     assert msgs == [b""]
     assert sm.load().specmemo_last_error() != b""
+
+
+@cpu_only
+def test_planned_tree_sizes_pass_the_budget_check():
+    # Trees cut to the planner's sizes fit their slabs exactly: every host
+    # check passes and only the launch fails, as no device is visible; one
+    # node more breaks the budget.
+    lens, caps = [100, 50, 7, 0], [164, 60, 8, 300]
+    sizes = [int(x) for x in sm.plan_tree_sizes(lens, caps, 64)]
+    assert sizes == [64, 10, 1, 64]
+    bases = np.concatenate([[0], np.cumsum(caps)[:-1]])
+    t = synth.t64()
+
+    def cut(n):
+        return synth.Tree(t.parent[:n].copy(), t.depth[:n].copy(), t.rank[:n].copy())
+
+    kv = FakeKV(lens, caps, bases)
+    expect("E_HIP", attn, FakeTrees([cut(n) for n in sizes]), kv)
+    expect("E_BUDGET", attn, FakeTrees([cut(n) for n in sizes[:1]] + [cut(sizes[1] + 1)] + [cut(n) for n in sizes[2:]]),
+           kv)

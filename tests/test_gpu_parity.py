@@ -246,6 +246,30 @@ def test_edge_parity(torch_cuda, name):
     run_parity(torch_cuda, wl, label=name, pack_heads=name not in ROWMAJOR_HEADS)
 
 
+def test_budgeted_tree_sizes(torch_cuda):
+    """Tree sizes chosen from each slab's free rows: a 128-node default tree
+    (depth 4, top-10) pruned right to left to what the slab still holds, full
+    slabs sitting the step out, every other slab filled to the last row.  The
+    library's builder and planner must give the oracle's trees, which then go
+    through the whole step."""
+    from oracle import budget as ob
+    from paper_2506_01986_amd import specmemo as sm
+    rng = np.random.default_rng(21)
+    default = ob.build_tree(128, 45, 4, 10)
+    assert [list(map(int, a)) for a in sm.tree_build(128, 45, 4, 10)] == [list(a) for a in default]
+    free = [0, 1, 2, 3, 7, 16, 33, 64, 100, 127, 128, 129, 500]
+    lens = [int(x) for x in rng.integers(0, 3000, len(free))]
+    caps = [n + f for n, f in zip(lens, free)]
+    sizes = ob.plan_tree_sizes(lens, caps, 128)
+    assert list(map(int, sm.plan_tree_sizes(lens, caps, 128))) == sizes
+    run = [b for b in range(len(free)) if sizes[b] > 0]
+    trees = [synth.Tree(*(np.asarray(a[:sizes[b]], np.int32) for a in default)) for b in run]
+    cfg = edge_cfg(B=len(run), n_q=8, n_kv=2, hidden=64, vocab=700, seed=21)
+    wl = synth.make(cfg, trees=trees, lens=[lens[b] for b in run], caps=[caps[b] for b in run])
+    say(f"[parity] budgeted sizes {[sizes[b] for b in run]}")
+    run_parity(torch_cuda, wl, label="budgeted_tree_sizes")
+
+
 def test_topk_ties(torch_cuda):
     """Integer-valued heads and hidden states give exact fp32 logits with many
     ties: head 0 is all zeros (every logit ties; the candidate buffer

@@ -157,3 +157,15 @@ def test_planted_walk_is_a_root_path():
             assert {c for _, c in los} == set(synth.children(t, path[-1]))
         else:
             assert not synth.children(t, path[-1])
+
+
+def test_model_parameter_counts():
+    # Llama-2 decoder: q/o projections hidden^2, k/v hidden x (n_kv * d), a
+    # gated MLP of three hidden x ffn matrices, two norms per layer, untied
+    # embedding and output matrices and a final norm.
+    ffn = {"llama2_7b_b1": 11008, "llama2_13b_b4": 13824, "llama2_70b_b10": 28672, "stress_b32": 28672}
+    for name, f in ffn.items():
+        c = configs.get(name)
+        h, kv = c.hidden, c.n_kv * c.head_dim
+        layer = 2 * h * h + 2 * h * kv + 3 * h * f + 2 * h
+        assert c.params == c.layers * layer + 2 * c.vocab * h + h, name
