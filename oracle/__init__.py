@@ -109,11 +109,13 @@ def tree_tokens(node_off, depth, rank, root_tok, topk_ids) -> np.ndarray:
 
 
 def tree_attn(q, K, V, node_off, parent, seq_len, seq_base, n_kv: int, scale: float | None = None,
-              sel=None) -> np.ndarray:
+              sel=None, key_valid=None) -> np.ndarray:
     """Tree-masked attention in float64.
 
     q: [sumN, n_q, d]; K, V: pool [n_kv, cap_total, d]; sel: optional array of
-    (global node, q head) pairs.  Returns [sumN, n_q, d] or [len(sel), d].
+    (global node, q head) pairs; key_valid: optional [cap_total] flags, 0 for
+    a cached pad token (padded batching).  Returns [sumN, n_q, d] or
+    [len(sel), d].
     """
     sumN, n_q, d = q.shape
     assert K.shape == V.shape and K.shape[0] == n_kv and K.shape[2] == d
@@ -122,17 +124,22 @@ def tree_attn(q, K, V, node_off, parent, seq_len, seq_base, n_kv: int, scale: fl
     seq_base = np.ascontiguousarray(seq_base, dtype=np.int64)
     scale = 1.0 / np.sqrt(d) if scale is None else float(scale)
     B = len(node_off) - 1
+    kvf = None
+    if key_valid is not None:
+        kvf = np.ascontiguousarray(np.asarray(key_valid) != 0, dtype=np.uint8)
+        assert kvf.shape == (K.shape[1],)
+    kvp = _p(kvf) if kvf is not None else None
     if sel is None:
         out = np.empty((sumN, n_q, d), dtype=np.float64)
         lib().oracle_tree_attn(_dt(q), B, _p(node_off), _p(parent), _p(seq_len), _p(seq_base),
                                n_q, n_kv, d, C.c_int64(K.shape[1]), C.c_double(scale), _p(q),
-                               _p(K), _p(V), 0, None, _p(out))
+                               _p(K), _p(V), 0, None, _p(out), kvp)
     else:
         s = _i32(sel).reshape(-1, 2)
         out = np.empty((len(s), d), dtype=np.float64)
         lib().oracle_tree_attn(_dt(q), B, _p(node_off), _p(parent), _p(seq_len), _p(seq_base),
                                n_q, n_kv, d, C.c_int64(K.shape[1]), C.c_double(scale), _p(q),
-                               _p(K), _p(V), len(s), _p(s), _p(out))
+                               _p(K), _p(V), len(s), _p(s), _p(out), kvp)
     return out
 
 

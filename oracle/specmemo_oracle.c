@@ -17,7 +17,9 @@
  *   tree attention - Sec. 3.1 (before verification the mask assumes every
  *                  candidate sequence is fully accepted: a node sees its
  *                  ancestors and itself) and App. A.1 (one forward over all
- *                  candidates), with scaled dot-product attention,
+ *                  candidates), with scaled dot-product attention; with
+ *                  padded batching (Sec. 3.3) a cached pad token takes -inf
+ *                  in the mask,
  *   acceptance   - App. A.1 (threshold per token, cumulative along the path,
  *                  longest verified candidate wins; typical sampling) and
  *                  Sec. 3.2 (verification of a continuation is cumulative),
@@ -128,7 +130,7 @@ static int seq_of(int B, const int *node_off, int node) {
 void oracle_tree_attn(int dt, int B, const int *node_off, const int *parent, const int *seq_len,
                       const int64_t *seq_base, int n_q, int n_kv, int d, int64_t cap_total,
                       double scale, const void *q, const void *K, const void *V, int nsel,
-                      const int *sel, double *out) {
+                      const int *sel, double *out, const uint8_t *key_valid) {
   int total = node_off[B];
   int64_t nrows = sel ? nsel : (int64_t)total * n_q;
   int group = n_q / n_kv;
@@ -155,6 +157,8 @@ void oracle_tree_attn(int dt, int B, const int *node_off, const int *parent, con
         acc += widen(q, dt, ((int64_t)node * n_q + h) * d + e) *
                widen(K, dt, ((int64_t)kv * cap_total + rows[t]) * d + e);
       s[t] = scale * acc;
+      /* a cached pad token (key_valid 0) is masked with -inf (Sec. 3.3) */
+      if (key_valid && t < L && !key_valid[rows[t]]) s[t] = -INFINITY;
       if (s[t] > m) m = s[t];
     }
     double zsum = 0.0;

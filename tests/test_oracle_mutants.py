@@ -33,6 +33,10 @@ MUTANTS = [
      ["test_typical_acceptance_equals_brute_force"]),
     ("no_move", "slab + (size_t)(L + pb[j]) * rb", "slab + (size_t)(L + j) * rb",
      ["test_compaction_moves_accepted_rows_only"]),
+    ("pad_not_masked", "if (key_valid && t < L && !key_valid[rows[t]])", "if (key_valid && t < 0 && !key_valid[rows[t]])",
+     ["test_padded_attention_equals_attention_without_pad_rows"]),
+    ("pad_mask_on_tree_rows", "if (key_valid && t < L && !key_valid[rows[t]])", "if (key_valid && !key_valid[rows[t]])",
+     ["test_padded_attention_equals_attention_without_pad_rows"]),
     ("seq_len_off_by_one", "seq_len[b] = L + a + 1;", "seq_len[b] = L + a;",
      ["test_compaction_moves_accepted_rows_only"]),
 ]

@@ -6,6 +6,7 @@ a dropped term, a wrong sign or index, or a transposed operand fails a test.
 """
 
 import itertools
+import os
 
 import numpy as np
 import pytest
@@ -390,3 +391,117 @@ def test_compaction_moves_accepted_rows_only(dtype):
             touched[s0 + L + j] = True
     for P, P0 in ((K, K0), (V, V0)):
         assert np.array_equal(P[:, ~touched].view(np.uint8), P0[:, ~touched].view(np.uint8))
+
+
+# ----------------------------------------------------------------------------
+# padded batching (Sec. 3.3): pad tokens in the cache, masked with -inf
+# ----------------------------------------------------------------------------
+
+def _padded_case(dtype, seed=5):
+    rng = np.random.default_rng(seed)
+    trees = [synth.random_tree(rng, 12), synth.t16(), synth.chain_tree(4)]
+    cfg = small_cfg(dtype=dtype, B=3, n_q=4, n_kv=2, topk=(10,) * 4, seed=seed)
+    wl = synth.make(cfg, trees=trees, lens=[40, 0, 23])
+    valid = (rng.random(wl.cap_total) < 0.6).astype(np.uint8)
+    for b in range(3):                    # tree rows are never consulted: make them pads too
+        s0, L = int(wl.seq_base[b]), int(wl.lens[b])
+        valid[s0 + L:s0 + L + wl.trees[b].n] = 0
+    return wl, valid
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_padded_attention_equals_attention_without_pad_rows(dtype):
+    # A key masked with -inf has weight exp(-inf) = 0: attention over a cache
+    # with pad tokens equals attention over the same cache with them deleted.
+    wl, valid = _padded_case(dtype)
+    out = run_attn(wl, key_valid=valid)
+    K, V = wl.pool_k.copy(), wl.pool_v.copy()
+    lens = wl.lens.copy()
+    for b in range(3):
+        s0, L, N = int(wl.seq_base[b]), int(wl.lens[b]), wl.trees[b].n
+        keep = [s0 + t for t in range(L) if valid[s0 + t]] + list(range(s0 + L, s0 + L + N))
+        for P, P0 in ((K, wl.pool_k), (V, wl.pool_v)):
+            P[:, s0:s0 + len(keep)] = P0[:, keep]
+        lens[b] = len(keep) - N
+    assert lens.tolist() != wl.lens.tolist()
+    ref = oracle.tree_attn(wl.q, K, V, wl.node_off, wl.parent, lens, wl.seq_base, wl.cfg.n_kv)
+    assert np.allclose(out, ref, rtol=1e-12, atol=1e-13)
+    # all rows valid: the unpadded result, bit for bit
+    full = run_attn(wl, key_valid=np.ones(wl.cap_total, np.uint8))
+    assert np.array_equal(full, run_attn(wl))
+
+
+def _golden_fig8():
+    rows = [list(map(int, ln.split())) for ln in open(os.path.join(os.path.dirname(__file__), "golden",
+                                                                   "fig8_padded_batch.txt"))
+            if ln.strip() and not ln.startswith("#")]
+    return np.array(rows)
+
+
+def test_fig8_padding_of_accepted_tokens():
+    from oracle import padded
+    g = _golden_fig8()
+    tau = g[:, 1]
+    cfg = small_cfg(B=4, n_q=2, n_kv=2, topk=(10,) * 4)
+    wl = synth.make(cfg, trees=[synth.chain_tree(5)] * 4, lens=[3, 0, 7, 1],
+                    caps=[3 + 9, 9, 7 + 9, 1 + 9])
+    acc = (tau - 1).astype(np.int32)
+    paths = np.full((4, 5), -1, np.int32)
+    for b in range(4):
+        paths[b, :tau[b]] = np.arange(tau[b])
+    valid = np.ones(wl.cap_total, np.uint8)
+    K, V = wl.pool_k.copy(), wl.pool_v.copy()
+    pos0 = np.array([3, 0, 7, 1], np.int32)
+    new_len, new_pos = padded.pad_update(K, V, wl.seq_base, wl.lens, pos0, valid, acc, paths)
+    uniform = int(g[0, 1] + g[0, 2])               # accepted + pads, the same for every sequence
+    assert (g[:, 1] + g[:, 2]).tolist() == [uniform] * 4
+    assert (new_len - wl.lens).tolist() == [uniform] * 4
+    assert (new_pos - pos0).tolist() == tau.tolist()
+    for b in range(4):
+        s0, L = int(wl.seq_base[b]), int(wl.lens[b])
+        assert valid[s0 + L:s0 + L + uniform].tolist() == [1] * tau[b] + [0] * g[b, 2]
+    # the chain paths are identities: no K/V row moves
+    assert np.array_equal(K.view(np.uint8), wl.pool_k.view(np.uint8))
+
+
+def test_padded_steps_keep_the_tokens_of_compaction():
+    # Three decode steps from one state, once compacted and once padded, with
+    # the same accepted paths and the same fresh tree K/V each step: the
+    # non-pad rows of each padded slab, in order, are the compacted slab's
+    # committed rows, and the position equals the compacted length.
+    from oracle import padded
+    rng = np.random.default_rng(9)
+    trees = [synth.t16(), synth.random_tree(rng, 20, max_depth=3), synth.chain_tree(4)]
+    cfg = small_cfg(dtype="bf16", B=3, n_q=4, n_kv=2, topk=(10,) * 4)
+    lens0 = np.array([5, 0, 11], np.int32)
+    caps = lens0 + 80
+    wl = synth.make(cfg, trees=trees, lens=lens0, caps=caps)
+    Kc, Vc = wl.pool_k.copy(), wl.pool_v.copy()
+    Kp, Vp = wl.pool_k.copy(), wl.pool_v.copy()
+    valid = np.ones(wl.cap_total, np.uint8)
+    Lc, Lp, pos = lens0.copy(), lens0.copy(), lens0.copy()
+    for step in range(3):
+        acc = np.zeros(3, np.int32)
+        paths = np.full((3, 5), -1, np.int32)
+        for b, t in enumerate(trees):
+            walk = [0]
+            while True:
+                kids = synth.children(t, walk[-1])
+                if not kids or rng.random() < 0.3:
+                    break
+                walk.append(kids[int(rng.integers(len(kids)))])
+            acc[b] = len(walk) - 1
+            paths[b, :len(walk)] = walk
+            s0, N = int(wl.seq_base[b]), t.n
+            fresh = rng.integers(0, 1 << 16, size=(2, cfg.n_kv, N, cfg.head_dim)).astype(np.uint16)
+            Kc[:, s0 + Lc[b]:s0 + Lc[b] + N], Vc[:, s0 + Lc[b]:s0 + Lc[b] + N] = fresh[0], fresh[1]
+            Kp[:, s0 + Lp[b]:s0 + Lp[b] + N], Vp[:, s0 + Lp[b]:s0 + Lp[b] + N] = fresh[0], fresh[1]
+        Lc = oracle.kv_compact(Kc, Vc, wl.seq_base, Lc, acc, paths)
+        Lp, pos = padded.pad_update(Kp, Vp, wl.seq_base, Lp, pos, valid, acc, paths)
+    assert pos.tolist() == Lc.tolist() and np.all(Lp >= Lc)
+    for b in range(3):
+        s0 = int(wl.seq_base[b])
+        real = [s0 + r for r in range(int(Lp[b])) if valid[s0 + r]]
+        assert len(real) == Lc[b]
+        for Pp, Pc in ((Kp, Kc), (Vp, Vc)):
+            assert np.array_equal(Pp[:, real].view(np.uint8), Pc[:, s0:s0 + Lc[b]].view(np.uint8))
