@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SPECMEMO_ABI_VERSION 3
+#define SPECMEMO_ABI_VERSION 4
 #define SPECMEMO_MAX_TREE_NODES 128 /* nodes per sequence's tree */
 #define SPECMEMO_MAX_DEPTH 15       /* tree depth (= Medusa heads) */
 #define SPECMEMO_MAX_TOPK 32        /* top-k per head */
@@ -212,6 +212,56 @@ int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specme
                         const int32_t *accept_len, const int32_t *path, int32_t path_stride,
                         void *stream);
 
+/* ---- Padded batching (Sec. 3.3, Fig. 8) --------------------------------------
+ *
+ * The paper's own batching keeps a batch's tensors uniform: after
+ * verification every sequence's accepted tokens are padded to the batch's
+ * longest acceptance, the pad tokens stay in the KV cache and take -inf in the
+ * attention mask of later steps, and position IDs skip them.  These two calls
+ * are that variant, for comparison with compaction (specmemo_kv_compact),
+ * which needs no pads.
+ *
+ * key_valid: device uint32 flags over the pool's rows, bit (r % 32) of word
+ * r / 32 for pool row r: 1 = a token, 0 = a pad token.  The array holds
+ * specmemo_key_mask_words(cap_total) words (the kernels read up to three words
+ * past the last row's).  Only committed rows (slab rows below L_b) are
+ * consulted; this step's tree rows are always tokens. */
+
+/* Words of a key_valid array for a pool of cap_total rows (0 if cap_total < 1). */
+int64_t specmemo_key_mask_words(int64_t cap_total);
+
+/* (b') Tree attention over a cache that holds pad tokens: specmemo_tree_attn
+ * with every committed key whose key_valid bit is 0 masked with -inf.  Same
+ * arguments, checks and workspace (SPECMEMO_WS_ATTN) as specmemo_tree_attn;
+ * key_valid must be non-NULL and 16-byte aligned.  A row whose committed keys
+ * are all pads still sees its tree path. */
+int specmemo_tree_attn_padded(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
+                              const uint32_t *key_valid, int32_t n_q, float scale, const void *q, void *out,
+                              void *ws, size_t ws_bytes, void *stream);
+
+/* (d') Padded KV update, in place of specmemo_kv_compact.  With
+ * tau_b = accept_len[b] + 1 and the uniform length T = max_b tau_b over the
+ * sequences whose path is valid:
+ *   slab row L_b + j <- slab row L_b + path[b][j], j = 0..accept_len[b]
+ *   (as in compaction), then
+ *   key_valid of rows L_b .. L_b + tau_b - 1 := 1, of rows
+ *   L_b + tau_b .. L_b + T - 1 := 0 (pad tokens: the rejected tree rows
+ *   that were there, now masked),
+ *   kv->seq_len[b] = L_b + T, pos[b] += tau_b (device int32 [B]: the
+ *   position of the next token, counting no pads).
+ * A path is valid if it is a root path of the tree (path[b][0] = 0, each
+ * entry the parent of the next, accept_len in range); a sequence with an
+ * invalid path is left untouched and does not count toward T.  Every sequence
+ * must have room for the longest possible acceptance:
+ * L_b + (deepest tree of the batch) + 1 <= seq_cap[b], else SPECMEMO_E_BUDGET.
+ * key_valid: 4-byte aligned (flags of neighbouring slabs may share a word;
+ * they are changed atomically).  ws: at least
+ * specmemo_workspace_bytes(SPECMEMO_WS_PAD, ...) bytes, 4-byte aligned
+ * (the uniform length). */
+int specmemo_kv_pad_update(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
+                           const int32_t *accept_len, const int32_t *path, int32_t path_stride,
+                           uint32_t *key_valid, int32_t *pos, void *ws, size_t ws_bytes, void *stream);
+
 /* ---- Memory budget and tree construction (host only) -------------------------
  *
  * SpecMemo's memory model (Sec. 3.1, Eq. 1-6) and its tree construction
@@ -347,6 +397,7 @@ int specmemo_plan_tree_sizes(int32_t B, const int32_t *seq_len_h, const int32_t 
 #define SPECMEMO_WS_TOPK 0
 #define SPECMEMO_WS_ATTN 1
 #define SPECMEMO_WS_ACCEPT 2
+#define SPECMEMO_WS_PAD 3
 
 /* Workspace bytes a call needs for these arguments (host-side; the only HIP
  * calls query the current device's compute-unit count, which the attention
@@ -355,6 +406,8 @@ int specmemo_plan_tree_sizes(int32_t B, const int32_t *seq_len_h, const int32_t 
  *                       fp32 logits; none are needed when logits_out is given).
  *   SPECMEMO_WS_ATTN:   kv required; n_q_or_heads = n_q; vocab ignored.
  *   SPECMEMO_WS_ACCEPT: kv ignored; n_q_or_heads = accept mode; vocab ignored.
+ *   SPECMEMO_WS_PAD:    specmemo_kv_pad_update; kv, n_q_or_heads and vocab
+ *                       ignored.
  * Returns 0 for invalid arguments as well as when no workspace is needed;
  * the call itself reports invalid arguments. */
 size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo_trees *t,

@@ -331,6 +331,7 @@ size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo
     plan_attn(ti, t, kv, n_q_or_heads, &p);
     return p.ws_bytes;
   }
+  if (which == SPECMEMO_WS_PAD) return 256;   // the batch's uniform acceptance length
   if (which == SPECMEMO_WS_ACCEPT) {
     return n_q_or_heads == SPECMEMO_ACCEPT_TYPICAL ? (size_t)ti.total * 2 * sizeof(float)
                                                    : (size_t)ti.total * sizeof(int32_t);
@@ -410,8 +411,13 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
   return hip_status(launch_topk(a, ti.B, st), "top-k launch");
 }
 
-int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, int32_t n_q, float scale,
-                       const void *q, void *out, void *ws, size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Tree attention with an optional pad-token mask (padded batching).
+int tree_attn_impl(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, const uint32_t *key_valid,
+                   int32_t n_q, float scale, const void *q, void *out, void *ws, size_t ws_bytes, void *stream) {
   TreeInfo ti;
   int rc;
   if ((rc = check_attn_args(dt, t, kv, n_q, &ti))) return rc;
@@ -424,6 +430,7 @@ int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmem
   a.k = kv->k;
   a.v = kv->v;
   a.parent = t->parent;
+  a.key_valid = key_valid;
   a.cap_total = kv->cap_total;
   a.n_q = n_q;
   a.n_kv = kv->n_kv;
@@ -476,6 +483,27 @@ int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmem
   return ok();
 }
 
+}  // namespace
+
+extern "C" {
+
+int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, int32_t n_q, float scale,
+                       const void *q, void *out, void *ws, size_t ws_bytes, void *stream) {
+  return tree_attn_impl(dt, t, kv, nullptr, n_q, scale, q, out, ws, ws_bytes, stream);
+}
+
+int64_t specmemo_key_mask_words(int64_t cap_total) {
+  if (cap_total < 1) return 0;
+  return (cap_total + 31) / 32 + 3;
+}
+
+int specmemo_tree_attn_padded(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
+                              const uint32_t *key_valid, int32_t n_q, float scale, const void *q, void *out,
+                              void *ws, size_t ws_bytes, void *stream) {
+  if (!al(key_valid, 16)) return fail(SPECMEMO_E_ARG, "key_valid must be non-NULL and 16-byte aligned");
+  return tree_attn_impl(dt, t, kv, key_valid, n_q, scale, q, out, ws, ws_bytes, stream);
+}
+
 int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, specmemo_accept_mode mode,
                     float temperature, float eps, float delta, const void *base_logits, const int32_t *node_tok,
                     int32_t *accept_len, int32_t *path, int32_t path_stride, int32_t *next_tok, void *ws,
@@ -522,8 +550,15 @@ int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, s
   return hip_status(launch_accept(dt, a, ti.total, static_cast<hipStream_t>(stream)), "acceptance launch");
 }
 
-int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, const int32_t *accept_len,
-                        const int32_t *path, int32_t path_stride, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Compaction (padded = false) or the padded update (Sec. 3.3): the same
+// checks and row moves, launched per group of sequences.
+int compact_impl(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, const int32_t *accept_len,
+                 const int32_t *path, int32_t path_stride, bool padded, uint32_t *key_valid, int32_t *pos, void *ws,
+                 size_t ws_bytes, void *stream) {
   int rc;
   if ((rc = check_dtype(dt))) return rc;
   TreeInfo ti;
@@ -534,6 +569,16 @@ int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specme
   if (path_stride < 1) return fail(SPECMEMO_E_ARG, "path_stride=%d", path_stride);
   const int elem = dt == SPECMEMO_BF16 ? 2 : 4;
   if ((kv->head_dim * elem) % 4) return fail(SPECMEMO_E_ARG, "row bytes must be a multiple of 4");
+  if (padded) {
+    if (!al(key_valid, 4) || !al(pos, 4)) return fail(SPECMEMO_E_ARG, "key_valid / pos must be non-NULL and 4-byte aligned");
+    if (!al(ws, 4) || ws_bytes < 4)
+      return fail(SPECMEMO_E_WORKSPACE, "workspace of 4 bytes needed (4-byte aligned), got %zu", ws ? ws_bytes : 0);
+    // every sequence may grow by the batch's longest acceptance: the deepest tree + 1
+    for (int b = 0; b < ti.B; ++b)
+      if ((int64_t)kv->seq_len_h[b] + ti.max_depth + 1 > kv->seq_cap_h[b])
+        return fail(SPECMEMO_E_BUDGET, "seq_len[%d]=%d + uniform length up to %d exceeds seq_cap=%d", b,
+                    kv->seq_len_h[b], ti.max_depth + 1, kv->seq_cap_h[b]);
+  }
   CompactArgs a{};
   a.k = kv->k;
   a.v = kv->v;
@@ -543,20 +588,41 @@ int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specme
   a.path_stride = path_stride;
   a.accept_len = accept_len;
   a.path = path;
+  a.parent = t->parent;
   a.seq_len = kv->seq_len;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t *uniform = static_cast<int32_t *>(ws);
+  if (padded) {
+    hipError_t e = launch_pad_length(t->node_off, t->parent, accept_len, path, path_stride, ti.B, uniform, st);
+    if (e != hipSuccess) return hip_status(e, "pad length launch");
+  }
   for (int b0 = 0; b0 < ti.B; b0 += kMaxSeqPerLaunch) {
     a.nseq = std::min(kMaxSeqPerLaunch, ti.B - b0);
     a.b0 = b0;
     for (int i = 0; i < a.nseq; ++i) {
       const int b = b0 + i;
       a.seq[i] = CompactSeq{kv->seq_base_h[b], kv->seq_len_h[b], t->node_off_h[b + 1] - t->node_off_h[b],
-                            kv->seq_cap_h[b], 0};
+                            kv->seq_cap_h[b], t->node_off_h[b]};
     }
-    hipError_t e = launch_kv_compact(a, st);
-    if (e != hipSuccess) return hip_status(e, "compaction launch");
+    hipError_t e = padded ? launch_kv_pad_update(a, uniform, key_valid, pos, st) : launch_kv_compact(a, st);
+    if (e != hipSuccess) return hip_status(e, padded ? "padded update launch" : "compaction launch");
   }
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, const int32_t *accept_len,
+                        const int32_t *path, int32_t path_stride, void *stream) {
+  return compact_impl(dt, t, kv, accept_len, path, path_stride, false, nullptr, nullptr, nullptr, 0, stream);
+}
+
+int specmemo_kv_pad_update(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
+                           const int32_t *accept_len, const int32_t *path, int32_t path_stride, uint32_t *key_valid,
+                           int32_t *pos, void *ws, size_t ws_bytes, void *stream) {
+  return compact_impl(dt, t, kv, accept_len, path, path_stride, true, key_valid, pos, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -57,6 +57,7 @@ struct AttnArgs {
   void *out;
   const void *k, *v;
   const int32_t *parent;
+  const uint32_t *key_valid;   // padded batching: bit r of the pool's row r, 0 = pad token; null: no pads
   float *part;             // partial results workspace
   int64_t cap_total;
   int32_t n_q, n_kv, group, head_dim;
@@ -97,16 +98,23 @@ hipError_t launch_accept(int dt, const AcceptArgs &a, int total_nodes, hipStream
 // ---- compaction ------------------------------------------------------------------
 struct CompactSeq {
   int64_t base;
-  int32_t L, N, cap, pad;
+  int32_t L, N, cap, node0;   // node0: global id of the root node
 };
 struct CompactArgs {
   void *k, *v;
   int64_t cap_total;
   int32_t n_kv, row_dwords, path_stride, nseq, b0;
   const int32_t *accept_len, *path;
+  const int32_t *parent;   // padded update: the trees' parents (root paths are checked)
   int32_t *seq_len;
   CompactSeq seq[kMaxSeqPerLaunch];
 };
 hipError_t launch_kv_compact(const CompactArgs &a, hipStream_t st);
+// Padded batching: the batch's uniform acceptance length into *uniform (one
+// block), then the row moves and the per-sequence bookkeeping.
+hipError_t launch_pad_length(const int32_t *node_off, const int32_t *parent, const int32_t *accept_len,
+                             const int32_t *path, int32_t path_stride, int32_t B, int32_t *uniform, hipStream_t st);
+hipError_t launch_kv_pad_update(const CompactArgs &a, const int32_t *uniform, uint32_t *key_valid, int32_t *pos,
+                                hipStream_t st);
 
 }  // namespace specmemo

@@ -131,6 +131,7 @@ __device__ __forceinline__ float tile_max32(const f32x16 (&x)[2]) {
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short s16x4_t __attribute__((__vector_size__(8)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // 16-byte direct load of every lane into LDS at lds_base + 16 * lane (one
 // global_load_lds_dwordx4 with M0 = lds_base, which must be wave-uniform),
@@ -170,7 +171,8 @@ __device__ __forceinline__ int vswz(int r, int c) { return c ^ ((r & 3) << 2); }
 // iteration j computes S, the weights and O for tile j, its two 32-key
 // products S^T = K Q^T being independent accumulation chains.
 // MINB: blocks that must fit on one compute unit (bounds the registers).
-template <int WAVES, int SLOTS, int MINB>
+// PAD: the cache holds pad tokens (padded batching), flagged in a.key_valid.
+template <int WAVES, int SLOTS, int MINB, bool PAD>
 __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   static_assert(SLOTS == 2 || SLOTS == 3, "ring depth");
   constexpr int RB = 32 * WAVES;
@@ -314,6 +316,23 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
     }
   };
 
+  // Padded batching (Sec. 3.3): the pad-token flags of the 64 keys of a tile,
+  // as a wave-uniform 64-bit word; bit i is key kt + i, and keys from the tree
+  // rows on count as valid (the ancestor mask governs them).  Scalar load of
+  // the four words around the tile's first row, waited for in place.
+  const uint32_t *const mask_base = PAD ? uniform_ptr(a.key_valid) : nullptr;
+  auto pad_bits = [&](int kt) -> uint64_t {
+    const int64_t row = S.base + kt;
+    const uint32_t *p = mask_base + (row >> 5);
+    u32x4_t w;
+    asm volatile("s_load_dwordx4 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(w) : "s"(p));
+    const uint32_t sh = (uint32_t)row & 31u;
+    uint64_t bits = ((uint64_t)w[1] << 32 | w[0]) >> sh;
+    bits |= sh ? (uint64_t)w[2] << (64 - sh) : 0ull;
+    const int committed = L - kt;
+    return committed < TK ? bits | (~0ull << committed) : bits;
+  };
+
   float m = -INFINITY, lsum = 0.f;
   f32x16 O[D / 32];
 #pragma unroll
@@ -330,6 +349,16 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   // operands of the four 16-key groups of the PV product.
   auto softmax_head = [&](int j, f32x16 (&Sc)[2]) {   // mask, tile max, rescaling
     const int kt = k0 + j * TK;
+    if constexpr (PAD) {
+      if (kt < L) {                      // committed keys: pad tokens take -inf
+        const uint64_t bits = pad_bits(kt) >> (4 * h);
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int r2 = 0; r2 < 16; ++r2)
+            Sc[sb][r2] = (bits >> (32 * sb + 8 * (r2 >> 2) + (r2 & 3))) & 1u ? Sc[sb][r2] : -INFINITY;
+      }
+    }
     if (kt + TK > min(k1, L)) {
       const uint64_t alo = (uint64_t)anc.y << 32 | anc.x, ahi = (uint64_t)anc.w << 32 | anc.z;
 #pragma unroll
@@ -503,9 +532,11 @@ __global__ __launch_bounds__(4 * RB) void tree_attn_combine(AttnArgs a) {
     uint4 v[CPT / 8];
 #pragma unroll
     for (int q = 0; q < CPT / 8; ++q) v[q] = po[q];
-    // every chunk holds keys visible to every row, so mc is finite
+    // A chunk whose keys a row cannot see (only pad tokens) has mc = -inf and
+    // weight 0; the last chunk holds the row's own tree row, so M ends finite.
     const float Mn = fmaxf(M, mc);
-    const float wa = fast_exp2(M - Mn), wb = fast_exp2(mc - Mn);   // wa = 0 for the first chunk
+    const float wa = M == -INFINITY ? 0.f : fast_exp2(M - Mn);
+    const float wb = mc == -INFINITY ? 0.f : fast_exp2(mc - Mn);
     l = l * wa + lc * wb;
 #pragma unroll
     for (int q = 0; q < CPT / 8; ++q) {
@@ -557,7 +588,10 @@ __global__ __launch_bounds__(256) void tree_attn_f32(AttnArgs a, int node_begin,
     o1 = o1 * alpha + pe * (e1 ? V[row * d + lane + 64] : 0.f);
     m = mn;
   };
-  for (int t = 0; t < S.L; ++t) visit(t);
+  for (int t = 0; t < S.L; ++t) {
+    const int64_t r = S.base + t;          // pad tokens (padded batching) are skipped: weight 0
+    if (!a.key_valid || ((a.key_valid[r >> 5] >> (r & 31)) & 1u)) visit(t);
+  }
   for (int u = n; u >= 0; u = a.parent[S.node0 + u]) visit(S.L + u);
   float *out = static_cast<float *>(a.out) + ((int64_t)gnode * a.n_q + hq) * d;
   if (e0) out[lane] = o0 / l;
@@ -566,17 +600,27 @@ __global__ __launch_bounds__(256) void tree_attn_f32(AttnArgs a, int node_begin,
 
 }  // namespace
 
-hipError_t launch_tree_attn_bf16(const AttnArgs &a, int rows_per_block, hipStream_t st) {
+namespace {
+template <bool PAD>
+void launch_bf16(const AttnArgs &a, int rows_per_block, hipStream_t st) {
   if (rows_per_block == 64) {
-    hipLaunchKernelGGL((tree_attn_bf16<2, 2, 2>), dim3(a.items), dim3(128), 0, st, a);
+    hipLaunchKernelGGL((tree_attn_bf16<2, 2, 2, PAD>), dim3(a.items), dim3(128), 0, st, a);
     if (a.citems) hipLaunchKernelGGL(tree_attn_combine<64>, dim3(a.citems), dim3(256), 0, st, a);
   } else if (rows_per_block == 128) {
-    hipLaunchKernelGGL((tree_attn_bf16<4, 2, 2>), dim3(a.items), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((tree_attn_bf16<4, 2, 2, PAD>), dim3(a.items), dim3(256), 0, st, a);
     if (a.citems) hipLaunchKernelGGL(tree_attn_combine<128>, dim3(a.citems), dim3(512), 0, st, a);
   } else {
-    hipLaunchKernelGGL((tree_attn_bf16<8, 3, 1>), dim3(a.items), dim3(512), 0, st, a);
+    hipLaunchKernelGGL((tree_attn_bf16<8, 3, 1, PAD>), dim3(a.items), dim3(512), 0, st, a);
     if (a.citems) hipLaunchKernelGGL(tree_attn_combine<256>, dim3(a.citems), dim3(1024), 0, st, a);
   }
+}
+}  // namespace
+
+hipError_t launch_tree_attn_bf16(const AttnArgs &a, int rows_per_block, hipStream_t st) {
+  if (a.key_valid)
+    launch_bf16<true>(a, rows_per_block, st);
+  else
+    launch_bf16<false>(a, rows_per_block, st);
   return hipGetLastError();
 }
 

@@ -32,7 +32,10 @@ def to_host_storage(t: torch.Tensor, dtype: str) -> np.ndarray:
 
 class VerifyStep:
     def __init__(self, wl: Workload, device="cuda", mode: int = sm.GREEDY, temperature: float = 0.7,
-                 eps: float = 0.09, delta: float = 0.3, keep_logits: bool = False, pack_heads: bool = True):
+                 eps: float = 0.09, delta: float = 0.3, keep_logits: bool = False, pack_heads: bool = True,
+                 key_valid: np.ndarray | None = None):
+        """key_valid: per pool row flags (0 = pad token) for the padded-batching
+        variant (tree_attn_padded / kv_pad_update); None for the ragged path."""
         cfg = wl.cfg
         self.wl, self.cfg, self.device = wl, cfg, device
         self.dt = sm.FP32 if cfg.dtype == "fp32" else sm.BF16
@@ -66,9 +69,18 @@ class VerifyStep:
         self.path = torch.empty((B, self.path_stride), **i32)
         self.next_tok = torch.empty(B, **i32)
         self.base_logits = None
+        self.key_valid = self.pos = None
+        if key_valid is not None:
+            words = sm.pack_key_valid(key_valid)
+            self.key_valid = torch.from_numpy(words.view(np.int32)).to(device)
+            # position of each sequence's next token: its committed rows minus the pads
+            kv_flags = np.asarray(key_valid) != 0
+            pos = [int(kv_flags[int(wl.seq_base[b]):int(wl.seq_base[b]) + int(wl.lens[b])].sum()) for b in range(B)]
+            self.pos = torch.tensor(pos, dtype=torch.int32, device=device)
         ws = max(sm.workspace_bytes(sm.WS_TOPK, self.dt, self.trees, None, nh, cfg.vocab),
                  sm.workspace_bytes(sm.WS_ATTN, self.dt, self.trees, self.kv, cfg.n_q),
-                 sm.workspace_bytes(sm.WS_ACCEPT, self.dt, self.trees, None, mode))
+                 sm.workspace_bytes(sm.WS_ACCEPT, self.dt, self.trees, None, mode),
+                 sm.workspace_bytes(sm.WS_PAD, self.dt, self.trees, None, 0) if key_valid is not None else 0)
         self.ws_bytes = ws
         self.ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=device)
 
@@ -95,8 +107,24 @@ class VerifyStep:
     def kv_compact(self, stream=None):
         sm.kv_compact(self.dt, self.trees, self.kv, self.accept_len, self.path, self.path_stride, stream=stream)
 
+    def tree_attn_padded(self, stream=None):
+        sm.tree_attn_padded(self.dt, self.trees, self.kv, self.key_valid, self.cfg.n_q, self.q, self.out, ws=self.ws,
+                            ws_bytes=self.ws_bytes, stream=stream)
+
+    def kv_pad_update(self, stream=None):
+        sm.kv_pad_update(self.dt, self.trees, self.kv, self.accept_len, self.path, self.path_stride, self.key_valid,
+                         self.pos, ws=self.ws, ws_bytes=self.ws_bytes, stream=stream)
+
     def run(self, stream=None):
         self.medusa_topk(stream)
         self.tree_attn(stream)
         self.accept(stream)
         self.kv_compact(stream)
+
+    def run_padded(self, stream=None):
+        """The step of the padded-batching variant: pad tokens masked in
+        attention, accepted tokens padded to the batch's longest acceptance."""
+        self.medusa_topk(stream)
+        self.tree_attn_padded(stream)
+        self.accept(stream)
+        self.kv_pad_update(stream)

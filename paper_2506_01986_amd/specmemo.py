@@ -22,7 +22,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "specmemo.h")
 FP32, BF16 = 0, 1
 GREEDY, TYPICAL = 0, 1
 HEADS_ROWMAJOR, HEADS_PACKED = 0, 1
-WS_TOPK, WS_ATTN, WS_ACCEPT = 0, 1, 2
+WS_TOPK, WS_ATTN, WS_ACCEPT, WS_PAD = 0, 1, 2, 3
 
 STATUS = {0: "OK", -1: "E_ARG", -2: "E_DTYPE", -3: "E_TREE", -4: "E_BUDGET", -5: "E_WORKSPACE", -6: "E_HIP"}
 
@@ -87,6 +87,12 @@ def load():
         for f in ("specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"):
             getattr(lib, f).restype = C.c_int
         i64 = C.c_int64
+        lib.specmemo_key_mask_words.argtypes = [i64]
+        lib.specmemo_key_mask_words.restype = i64
+        lib.specmemo_tree_attn_padded.argtypes = [i32, PT, PK, vp, i32, f32, vp, vp, vp, sz, vp]
+        lib.specmemo_tree_attn_padded.restype = C.c_int
+        lib.specmemo_kv_pad_update.argtypes = [i32, PT, PK, vp, vp, i32, vp, vp, vp, sz, vp]
+        lib.specmemo_kv_pad_update.restype = C.c_int
         lib.specmemo_mem_kv_bytes.argtypes = [i32, i32, i32, i32, i64, i32]
         lib.specmemo_mem_buffer_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
         lib.specmemo_mem_total_bytes.argtypes = [i64, i64, i32, i64, i64]
@@ -238,6 +244,43 @@ def kv_compact(dt: int, trees: Trees, kv: KVPool, accept_len, path, path_stride:
     ts, ks = trees.struct(), kv.struct()
     _check(load().specmemo_kv_compact(dt, C.byref(ts), C.byref(ks), _ptr(accept_len), _ptr(path), path_stride,
                                       _stream(stream)))
+
+
+# ---- padded batching -------------------------------------------------------------
+
+def key_mask_words(cap_total: int) -> int:
+    return int(load().specmemo_key_mask_words(cap_total))
+
+
+def pack_key_valid(flags) -> np.ndarray:
+    """Per-row flags (nonzero = token, 0 = pad) -> the library's uint32 words
+    (bit r % 32 of word r / 32), padded to key_mask_words(len(flags))."""
+    f = np.asarray(flags) != 0
+    words = np.zeros(key_mask_words(len(f)), np.uint32)
+    packed = np.packbits(f, bitorder="little")
+    packed = np.concatenate([packed, np.zeros((-len(packed)) % 4, np.uint8)])
+    words[:len(packed) // 4] = packed.view("<u4")
+    return words
+
+
+def unpack_key_valid(words, cap_total: int) -> np.ndarray:
+    """Inverse of pack_key_valid: uint8 flags [cap_total]."""
+    w = np.ascontiguousarray(np.asarray(words, dtype=np.uint32))
+    return np.unpackbits(w.view(np.uint8), bitorder="little")[:cap_total]
+
+
+def tree_attn_padded(dt: int, trees: Trees, kv: KVPool, key_valid, n_q: int, q, out, scale: float = 0.0, ws=None,
+                     ws_bytes: int = 0, stream=None):
+    ts, ks = trees.struct(), kv.struct()
+    _check(load().specmemo_tree_attn_padded(dt, C.byref(ts), C.byref(ks), _ptr(key_valid), n_q, scale, _ptr(q),
+                                            _ptr(out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def kv_pad_update(dt: int, trees: Trees, kv: KVPool, accept_len, path, path_stride: int, key_valid, pos, ws=None,
+                  ws_bytes: int = 0, stream=None):
+    ts, ks = trees.struct(), kv.struct()
+    _check(load().specmemo_kv_pad_update(dt, C.byref(ts), C.byref(ks), _ptr(accept_len), _ptr(path), path_stride,
+                                         _ptr(key_valid), _ptr(pos), _ptr(ws), ws_bytes, _stream(stream)))
 
 
 # ---- memory budget and tree construction (host) ------------------------------

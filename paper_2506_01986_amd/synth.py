@@ -397,3 +397,50 @@ def storage_to_f64(x: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "fp32":
         return x.astype(np.float64)
     return bf16_bits_to_f32(x).astype(np.float64)
+
+
+# ----------------------------------------------------------------------------
+# Padded batching: cache layouts with pad tokens
+# ----------------------------------------------------------------------------
+
+def padded_history(rng: np.random.Generator, real_lens: Sequence[int], steps: int, p_accept: float,
+                   depth: int) -> Tuple[np.ndarray, List[np.ndarray]]:
+    """The committed rows of a batch after `steps` steps of padded batching.
+
+    Each step, sequence b commits tau_b = 1 + (levels accepted in a row, each
+    with probability p_accept, at most `depth`) tokens and every sequence's
+    cache grows by T = max_b tau_b rows, the last T - tau_b of them pad
+    tokens.  Before those steps each cache holds its prompt (no pads), sized so
+    that sequence b ends with real_lens[b] tokens.  Returns the committed rows
+    per sequence and, per sequence, its flags (1 = token, 0 = pad).
+    """
+    B = len(real_lens)
+    # tokens per step: 1 + the run of accepted levels
+    runs = np.ones((steps, B), dtype=np.int64)
+    alive = np.ones((steps, B), dtype=bool)
+    for _ in range(depth):
+        alive &= rng.random((steps, B)) < p_accept
+        runs += alive
+    T = runs.max(axis=1)
+    gen = runs.sum(axis=0)
+    prompt = np.asarray(real_lens, dtype=np.int64) - gen
+    assert np.all(prompt >= 0), "fewer steps: a sequence generated more tokens than it holds"
+    flags = []
+    for b in range(B):
+        f = [np.ones(int(prompt[b]), np.uint8)]
+        for s in range(steps):
+            f.append(np.concatenate([np.ones(int(runs[s, b]), np.uint8), np.zeros(int(T[s] - runs[s, b]), np.uint8)]))
+        flags.append(np.concatenate(f))
+    return np.array([len(f) for f in flags], dtype=np.int32), flags
+
+
+def pool_key_flags(wl: Workload, slab_flags: Sequence[np.ndarray]) -> np.ndarray:
+    """Per pool row flags from per-slab flags of the committed rows; every other
+    row (tree rows, free rows, canaries) is flagged 0: those are never read as
+    committed keys."""
+    f = np.zeros(wl.cap_total, np.uint8)
+    for b, sf in enumerate(slab_flags):
+        assert len(sf) == int(wl.lens[b])
+        s0 = int(wl.seq_base[b])
+        f[s0:s0 + len(sf)] = sf
+    return f

@@ -31,7 +31,7 @@ def test_library_loads_and_exports_every_declared_function():
     assert {"specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert sm.abi_version() == 3
+    assert sm.abi_version() == 4
 
 
 class FakeTrees(sm.Trees):
@@ -193,3 +193,29 @@ def test_planned_tree_sizes_pass_the_budget_check():
     expect("E_HIP", attn, FakeTrees([cut(n) for n in sizes]), kv)
     expect("E_BUDGET", attn, FakeTrees([cut(n) for n in sizes[:1]] + [cut(sizes[1] + 1)] + [cut(n) for n in sizes[2:]]),
            kv)
+
+
+@cpu_only
+def test_padded_batching_errors():
+    one = synth.tree_from_rank_paths([()])
+    t = FakeTrees([synth.t64(), one])                     # the deepest tree has 4 levels
+    assert sm.key_mask_words(1) == 4 and sm.key_mask_words(64) == 5 and sm.key_mask_words(65) == 6
+    assert sm.key_mask_words(0) == 0
+
+    def pad(kv, ws_bytes=256, key_valid=FAKE, pos=FAKE):
+        sm.kv_pad_update(sm.BF16, t, kv, FAKE, FAKE, 5, key_valid, pos, ws=FAKE, ws_bytes=ws_bytes, stream=0)
+
+    roomy = FakeKV([10, 10], [80, 40], [0, 100])
+    expect("E_HIP", pad, roomy)                           # every host check passes
+    # the single-node slab holds its tree (36 + 1 <= 38) but not a uniform
+    # length of up to 5 rows (36 + 5 > 38); compaction accepts the same pool
+    tight = FakeKV([10, 36], [80, 38], [0, 100])
+    expect("E_BUDGET", pad, tight)
+    expect("E_HIP", sm.kv_compact, sm.BF16, t, tight, FAKE, FAKE, 5, stream=0)
+    expect("E_WORKSPACE", pad, roomy, ws_bytes=2)
+    expect("E_ARG", pad, roomy, key_valid=None)
+    expect("E_ARG", pad, roomy, pos=None)
+    with pytest.raises(sm.SpecmemoError) as e:
+        sm.tree_attn_padded(sm.BF16, t, roomy, None, 4, FAKE, FAKE, ws=FAKE, ws_bytes=1 << 30, stream=0)
+    assert e.value.name == "E_ARG"
+    assert sm.workspace_bytes(sm.WS_PAD, sm.BF16, t, None, 0) >= 4
