@@ -144,6 +144,56 @@ def _oracle_step(wl):
     return float(stages.sum()), stages
 
 
+def padded_report(torch, cfg, wl, step, steps, history=150):
+    # at most depth + 1 tokens per step: every sequence keeps a prompt
+    history = min(history, int(np.min(wl.lens)) // (cfg.n_heads + 1))
+    """The paper's padded batching (Sec. 3.3) on the same batch, for
+    comparison with compaction: the same real tokens per sequence after
+    `history` padded decode steps (pad tokens interleaved in each cache), one
+    step = head projection, attention with the pad mask, acceptance, padded
+    update.  Same heads, queries, trees and planted logits as the ragged step."""
+    from paper_2506_01986_amd import runner, synth
+    rng = np.random.default_rng(cfg.seed + 1000)
+    p = cfg.p_accept if cfg.p_accept is not None else float(np.mean(cfg.p_range))
+    rows, slab = synth.padded_history(rng, wl.lens, history, p, cfg.n_heads)
+    wp = synth.make(cfg, lens=rows, with_heads=False)
+    wp.head_w, wp.hidden = wl.head_w, wl.hidden
+    flags = synth.pool_key_flags(wp, slab)
+    sp = runner.VerifyStep(wp, key_valid=flags)
+    sp.base_logits = step.base_logits
+    for _ in range(3):
+        sp.run_padded()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    stages = [sp.medusa_topk, sp.tree_attn_padded, sp.accept, sp.kv_pad_update]
+    for k in range(steps):
+        ev[k][0].record()
+        for j, fn in enumerate(stages):
+            fn()
+            ev[k][j + 1].record()
+    torch.cuda.synchronize()
+    t = np.array([[ev[k][j].elapsed_time(ev[k][j + 1]) for j in range(4)] for k in range(steps)])
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        sp.run_padded()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    pads = int(np.sum(rows) - np.sum(wl.lens))
+    row_bytes = 2 * cfg.n_kv * cfg.head_dim * cfg.elem_bytes          # K and V of one layer
+    attn_bytes = (int(np.sum(rows)) + wp.total_nodes) * row_bytes + 2 * wp.total_nodes * cfg.n_q * cfg.head_dim * cfg.elem_bytes
+    ta = float(t[:, 1].mean())
+    return {"history_steps": history, "kv_rows": int(np.sum(rows)), "pad_rows": pads,
+            "pad_frac": round(pads / float(np.sum(rows)), 4),
+            "kv_bytes_all_layers": int((np.sum(rows) + wp.total_nodes) * row_bytes * cfg.layers),
+            "ms_per_step": round(ms, 5), "value": round(wp.total_nodes / (ms * 1e-3), 1),
+            "stages_ms": {n: round(float(t[:, j].mean()), 5) for j, n in
+                          enumerate(["medusa_topk", "tree_attn_padded", "accept", "kv_pad_update"])},
+            "tree_attn_padded": {"ms": round(ta, 5), "algorithmic_bytes": attn_bytes,
+                                 "GBps": round(attn_bytes / (ta * 1e-3) / 1e9, 1)}}
+
+
 def budget_report(cfg, wl, device_bytes, reps=2000):
     """The memory model and Alg. 1's plan for the workload's model on this
     device (host calls of the library), with their host times and the
@@ -195,6 +245,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="llama2_70b_b10")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-padded", action="store_true", help="skip the padded-batching comparison")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="also run a device-to-device copy of BYTES (counter calibration)")
     args = ap.parse_args()
@@ -324,6 +375,13 @@ def main():
         "graph": {"ms_per_step": round(graph_ms, 5), "value": round(wl.total_nodes / (graph_ms * 1e-3), 1)},
         "stages": st,
     }
+    if not args.no_padded:
+        print("[bench] padded batching variant", file=sys.stderr, flush=True)
+        pr = padded_report(torch, cfg, wl, step, args.steps)
+        pr["kv_bytes_all_layers_compacted"] = int((np.sum(wl.lens) + wl.total_nodes) * 2 * cfg.n_kv * cfg.head_dim
+                                                  * cfg.elem_bytes * cfg.layers)
+        pr["step_time_vs_compaction"] = round(pr["ms_per_step"] / ms, 4)
+        result["padded"] = pr
     if cfg.params:
         print("[bench] memory budget plan (host)", file=sys.stderr, flush=True)
         result["budget"] = budget_report(cfg, wl, torch.cuda.get_device_properties(0).total_memory)

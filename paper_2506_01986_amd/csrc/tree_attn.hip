@@ -351,12 +351,15 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
     const int kt = k0 + j * TK;
     if constexpr (PAD) {
       if (kt < L) {                      // committed keys: pad tokens take -inf
-        const uint64_t bits = pad_bits(kt) >> (4 * h);
+        const uint64_t all = pad_bits(kt);
+        if (all != ~0ull) {              // wave-uniform: tiles without pads skip the selects
+          const uint64_t bits = all >> (4 * h);
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
+          for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-          for (int r2 = 0; r2 < 16; ++r2)
-            Sc[sb][r2] = (bits >> (32 * sb + 8 * (r2 >> 2) + (r2 & 3))) & 1u ? Sc[sb][r2] : -INFINITY;
+            for (int r2 = 0; r2 < 16; ++r2)
+              Sc[sb][r2] = (bits >> (32 * sb + 8 * (r2 >> 2) + (r2 & 3))) & 1u ? Sc[sb][r2] : -INFINITY;
+        }
       }
     }
     if (kt + TK > min(k1, L)) {
