@@ -185,3 +185,51 @@ def kv_compact(K, V, seq_base, seq_len, accept_len, path):
     lib().oracle_kv_compact(K.dtype.itemsize, B, n_kv, d, C.c_int64(cap_total), _p(K), _p(V),
                             _p(seq_base), _p(sl), _p(acc), _p(path), stride)
     return sl
+
+
+def resblock(h, W1, b1) -> np.ndarray:
+    """Medusa residual blocks in float64: [n_heads, B, hidden] of
+    h + SiLU(W1_i h + b1_i) (the blocks' outputs before storage rounding)."""
+    B, hidden = h.shape
+    n_heads = W1.shape[0]
+    assert W1.shape == (n_heads, hidden, hidden) and b1.shape == (n_heads, hidden)
+    assert _dt(h) == _dt(W1) == _dt(b1)
+    out = np.empty((n_heads, B, hidden), dtype=np.float64)
+    lib().oracle_resblock(_dt(h), B, hidden, n_heads, _p(h), _p(W1), _p(b1), _p(out))
+    return out
+
+
+def to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
+    """float64 -> the storage type, as a kernel stores an fp32 result: rounded
+    to float32 (nearest even), then for bf16 to its top 16 bits (nearest even)."""
+    f = np.asarray(x, dtype=np.float64).astype(np.float32)
+    if dtype == "fp32":
+        return f
+    u = f.view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    return r
+
+
+def philox4x64_10(ctr, key) -> np.ndarray:
+    """Philox4x64-10 blocks: ctr [n, 4], key [n, 2] (uint64) -> [n, 4]."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint64).reshape(-1, 4)
+    k = np.ascontiguousarray(key, dtype=np.uint64).reshape(-1, 2)
+    assert len(c) == len(k)
+    out = np.empty_like(c)
+    lib().oracle_philox4x64_10(len(c), _p(c), _p(k), _p(out))
+    return out
+
+
+def sample_next(logits, node_off, accept_len, path, temperature: float, seed: int, offset: int):
+    """Gumbel-max draw from softmax(z / T) of each sequence's last accepted
+    node.  Returns (next_tok, best key, second-best key) of each sequence."""
+    sumN, vocab = logits.shape
+    node_off, acc, path = _i32(node_off), _i32(accept_len), _i32(path)
+    B, stride = path.shape
+    tok = np.empty(B, np.int32)
+    best, second = np.empty(B, np.float32), np.empty(B, np.float32)
+    inv_t = np.float32(1.0) / np.float32(temperature)
+    lib().oracle_sample_next(_dt(logits), B, _p(node_off), vocab, C.c_float(inv_t), C.c_uint64(seed),
+                             C.c_uint64(offset), _p(logits), _p(acc), _p(path), stride, _p(tok), _p(best),
+                             _p(second))
+    return tok, best, second

@@ -310,3 +310,89 @@ void oracle_kv_compact(int elem_bytes, int B, int n_kv, int d, int64_t cap_total
   }
   free(tmp);
 }
+
+/* ---- Medusa residual-block heads ----------------------------------------------
+ * Reading (the paper gives only a size per head): head i first maps the last
+ * hidden state through one residual block, h'_i = h + SiLU(W1_i h + b1_i),
+ * SiLU(x) = x / (1 + exp(-x)), and its vocabulary projection then reads h'_i.
+ * W1: [n_heads][hidden][hidden] (out x in), b1: [n_heads][hidden], both in the
+ * storage type.  out: fp64 [n_heads][B][hidden]. */
+void oracle_resblock(int dt, int B, int hidden, int n_heads, const void *h, const void *W1, const void *b1,
+                     double *out) {
+#pragma omp parallel for schedule(static)
+  for (int64_t ic = 0; ic < (int64_t)n_heads * hidden; ++ic) {
+    int i = (int)(ic / hidden), c = (int)(ic % hidden);
+    for (int b = 0; b < B; ++b) {
+      double acc = widen(b1, dt, ic);
+      for (int k = 0; k < hidden; ++k) acc += widen(W1, dt, ic * hidden + k) * widen(h, dt, (int64_t)b * hidden + k);
+      double x = widen(h, dt, (int64_t)b * hidden + c);
+      out[((int64_t)i * B + b) * hidden + c] = x + acc / (1.0 + exp(-acc));
+    }
+  }
+}
+
+/* ---- Philox4x64-10 ------------------------------------------------------------
+ * The counter-based generator of Salmon, Moraes, Dror and Shaw ("Parallel
+ * random numbers: as easy as 1, 2, 3", SC 2011): ten rounds of two 64 x 64 ->
+ * 128-bit multiplications on a 4 x 64-bit counter, the 2 x 64-bit key bumped by
+ * the Weyl constants between rounds. */
+static void philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]) {
+  uint64_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3], k0 = key[0], k1 = key[1];
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B97F4A7C15ull;
+      k1 += 0xBB67AE8584CAA73Bull;
+    }
+    unsigned __int128 p0 = (unsigned __int128)0xD2E7470EE14C6C93ull * x0;
+    unsigned __int128 p1 = (unsigned __int128)0xCA5A826395121157ull * x2;
+    uint64_t hi0 = (uint64_t)(p0 >> 64), lo0 = (uint64_t)p0, hi1 = (uint64_t)(p1 >> 64), lo1 = (uint64_t)p1;
+    x0 = hi1 ^ x1 ^ k0;
+    x1 = lo1;
+    x2 = hi0 ^ x3 ^ k1;
+    x3 = lo0;
+  }
+  out[0] = x0, out[1] = x1, out[2] = x2, out[3] = x3;
+}
+
+void oracle_philox4x64_10(int n, const uint64_t *ctr, const uint64_t *key, uint64_t *out) {
+  for (int i = 0; i < n; ++i) philox4x64_10(ctr + 4 * i, key + 2 * i, out + 4 * i);
+}
+
+/* ---- sampled next token ---------------------------------------------------------
+ * Instead of the greedy argmax, next_tok is drawn from softmax(z / T) of the
+ * last accepted node's row, by the Gumbel-max rule: the argmax over v of
+ * z_v / T + G_v with G_v = -log(-log(u_v)) standard Gumbel.  u_v comes from
+ * Philox4x64-10 with key (seed, offset) and counter (v / 4, b, 0, 0), output
+ * word v % 4: u = ((x >> 40) + 1/2) / 2^24.  The keys are formed in fp32 as
+ * the kernel forms them (fmaf(z, 1/T, G), 1/T rounded once to fp32), so that
+ * both sides take the argmax decision in the same precision; ties go to the
+ * lower token id. */
+void oracle_sample_next(int dt, int B, const int *node_off, int vocab, float inv_temp, uint64_t seed,
+                        uint64_t offset, const void *logits, const int *accept_len, const int *path, int stride,
+                        int *next_tok, float *best_key, float *second_key) {
+  for (int b = 0; b < B; ++b) {
+    int64_t row = node_off[b] + path[(int64_t)b * stride + accept_len[b]];
+    uint64_t key[2] = {seed, offset};
+    float best = -INFINITY, second = -INFINITY;
+    int arg = -1;
+    for (int v0 = 0; v0 < vocab; v0 += 4) {
+      uint64_t ctr[4] = {(uint64_t)(v0 / 4), (uint64_t)b, 0, 0}, x[4];
+      philox4x64_10(ctr, key, x);
+      for (int j = 0; j < 4 && v0 + j < vocab; ++j) {
+        float u = ((float)(x[j] >> 40) + 0.5f) * 0x1p-24f;
+        float g = -logf(-logf(u));
+        float s = fmaf((float)widen(logits, dt, row * vocab + v0 + j), inv_temp, g);
+        if (s > best) {
+          second = best;
+          best = s;
+          arg = v0 + j;
+        } else if (s > second) {
+          second = s;
+        }
+      }
+    }
+    next_tok[b] = arg;
+    if (best_key) best_key[b] = best;
+    if (second_key) second_key[b] = second;
+  }
+}

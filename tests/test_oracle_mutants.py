@@ -37,6 +37,16 @@ MUTANTS = [
      ["test_padded_attention_equals_attention_without_pad_rows"]),
     ("pad_mask_on_tree_rows", "if (key_valid && t < L && !key_valid[rows[t]])", "if (key_valid && !key_valid[rows[t]])",
      ["test_padded_attention_equals_attention_without_pad_rows"]),
+    ("resblock_no_residual", "out[((int64_t)i * B + b) * hidden + c] = x + acc / (1.0 + exp(-acc));",
+     "out[((int64_t)i * B + b) * hidden + c] = acc / (1.0 + exp(-acc));",
+     ["test_resblock_equals_torch_linear_silu"]),
+    ("philox_weyl", "k1 += 0xBB67AE8584CAA73Bull;", "k1 += 0xBB67AE8584CAA73Aull;",
+     ["test_philox_equals_numpy_stream"]),
+    ("gumbel_sign", "float g = -logf(-logf(u));", "float g = logf(-logf(u));",
+     ["test_sampled_token_follows_softmax"]),
+    ("temperature_dropped", "float s = fmaf((float)widen(logits, dt, row * vocab + v0 + j), inv_temp, g);",
+     "float s = (float)widen(logits, dt, row * vocab + v0 + j) + g;",
+     ["test_sampled_token_follows_softmax"]),
     ("seq_len_off_by_one", "seq_len[b] = L + a + 1;", "seq_len[b] = L + a;",
      ["test_compaction_moves_accepted_rows_only"]),
 ]

@@ -505,3 +505,103 @@ def test_padded_steps_keep_the_tokens_of_compaction():
         assert len(real) == Lc[b]
         for Pp, Pc in ((Kp, Kc), (Vp, Vc)):
             assert np.array_equal(Pp[:, real].view(np.uint8), Pc[:, s0:s0 + Lc[b]].view(np.uint8))
+
+
+# ----------------------------------------------------------------------------
+# decode loop pieces: residual-block heads, Philox, sampled next token
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_resblock_equals_torch_linear_silu(dtype):
+    rng = np.random.default_rng(31)
+    B, hidden, n_heads = 3, 24, 2
+    h = synth._store(rng.standard_normal(B * hidden).astype(np.float32), dtype).reshape(B, hidden)
+    W1 = synth._store((0.3 * rng.standard_normal(n_heads * hidden * hidden)).astype(np.float32),
+                      dtype).reshape(n_heads, hidden, hidden)
+    b1 = synth._store(rng.standard_normal(n_heads * hidden).astype(np.float32), dtype).reshape(n_heads, hidden)
+    out = oracle.resblock(h, W1, b1)
+    H, W, bb = (torch.from_numpy(f64(x, dtype)) for x in (h, W1, b1))
+    for i in range(n_heads):
+        ref = H + torch.nn.functional.silu(torch.nn.functional.linear(H, W[i], bb[i]))
+        assert np.allclose(out[i], ref.numpy(), rtol=1e-13, atol=1e-13)
+    # zero weights and bias: the block is the identity
+    z = np.zeros_like(W1), np.zeros_like(b1)
+    assert np.array_equal(oracle.resblock(h, *z), np.broadcast_to(f64(h, dtype), out.shape))
+
+
+def test_storage_rounding_equals_torch():
+    rng = np.random.default_rng(32)
+    x = np.concatenate([rng.standard_normal(10000) * 10.0 ** rng.integers(-8, 8, 10000),
+                        [0.0, -0.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -9, 65504.0, 1e-30]])
+    bf = oracle.to_storage(x, "bf16")
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(bf, ref)
+    assert np.array_equal(oracle.to_storage(x, "fp32"), x.astype(np.float32))
+
+
+def _plus_one(ctr):
+    c = [int(v) for v in ctr]
+    for i in range(4):
+        c[i] = (c[i] + 1) % (1 << 64)
+        if c[i] != 0:
+            break
+    return c
+
+
+@pytest.mark.parametrize("key,ctr", [((0, 0), (0, 0, 0, 0)), ((123456789, 987654321), (5, 6, 7, 8)),
+                                     ((2 ** 64 - 1, 2 ** 63), (2 ** 64 - 1, 2 ** 64 - 1, 3, 4))])
+def test_philox_equals_numpy_stream(key, ctr):
+    # numpy's Philox (4 x 64 bits, 10 rounds) advances its counter before each
+    # block of four outputs
+    bg = np.random.Philox(key=np.array(key, np.uint64), counter=np.array(ctr, np.uint64))
+    raw = bg.random_raw(12).reshape(3, 4)
+    c = list(ctr)
+    for blk in range(3):
+        c = _plus_one(c)
+        got = oracle.philox4x64_10(np.array([c], np.uint64), np.array([key], np.uint64))[0]
+        assert np.array_equal(got, raw[blk]), blk
+
+
+def _sample_rows(z, n, temperature, seed, offset):
+    """n single-node sequences whose only row is z."""
+    vocab = len(z)
+    logits = np.tile(np.asarray(z, np.float32), (n, 1))
+    node_off = np.arange(n + 1, dtype=np.int32)
+    acc = np.zeros(n, np.int32)
+    path = np.zeros((n, 1), np.int32)
+    return oracle.sample_next(logits, node_off, acc, path, temperature, seed, offset)
+
+
+@pytest.mark.parametrize("temperature", [0.5, 1.0, 2.5])
+def test_sampled_token_follows_softmax(temperature):
+    z = np.array([0.3, -1.2, 2.0, 0.0, 1.1, -0.4], np.float32)
+    n = 40000
+    tok, _, _ = _sample_rows(z, n, temperature, seed=77, offset=3)
+    counts = np.bincount(tok, minlength=len(z))
+    p = scipy.special.softmax(z.astype(np.float64) / temperature)
+    chi = scipy.stats.chisquare(counts, n * p)
+    assert chi.pvalue > 1e-3, (counts, n * p)
+    # another seed or offset draws other tokens
+    assert not np.array_equal(tok, _sample_rows(z, n, temperature, seed=78, offset=3)[0])
+    assert not np.array_equal(tok, _sample_rows(z, n, temperature, seed=77, offset=4)[0])
+
+
+def test_sampling_at_low_temperature_is_argmax():
+    rng = np.random.default_rng(33)
+    z = rng.standard_normal(257).astype(np.float32)
+    tok, _, _ = _sample_rows(z, 50, 1e-4, seed=1, offset=0)
+    assert np.all(tok == int(np.argmax(z)))
+
+
+def test_sampling_reads_the_last_accepted_row():
+    # three single-path trees of 4 nodes; each node's row puts a dominant logit
+    # on a token of its own, so the draw names the row that was read
+    B, n, vocab = 3, 4, 50
+    logits = np.zeros((B * n, vocab), np.float32)
+    for r in range(B * n):
+        logits[r, r] = 60.0
+    node_off = np.arange(0, B * n + 1, n, dtype=np.int32)
+    acc = np.array([0, 3, 2], np.int32)
+    path = np.tile(np.arange(n, dtype=np.int32), (B, 1))
+    tok, _, _ = oracle.sample_next(logits, node_off, acc, path, 1.0, 5, 0)
+    assert tok.tolist() == [0 * n + 0, 1 * n + 3, 2 * n + 2]
