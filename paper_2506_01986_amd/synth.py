@@ -382,11 +382,19 @@ def planted_logits(wl: Workload, node_tok: np.ndarray) -> np.ndarray:
     ``node_tok`` holds each tree node's token (the tree assembled from the
     heads' top-k); the planted entries sit at those tokens' columns.
     """
-    out = wl.base_logits.copy()
-    hi = np.float32(PLANT_HI) if wl.store_dtype == "fp32" else to_bf16_bits(np.float32([PLANT_HI]))[0]
-    lo = np.float32(PLANT_LO) if wl.store_dtype == "fp32" else to_bf16_bits(np.float32([PLANT_LO]))[0]
-    for b, plan in enumerate(wl.plan):
-        o = int(wl.node_off[b])
+    return plant_logits(wl.base_logits, wl.node_off, wl.plan, node_tok, wl.store_dtype)
+
+
+def plant_value(v: float, dtype: str):
+    return np.float32(v) if dtype == "fp32" else to_bf16_bits(np.float32([v]))[0]
+
+
+def plant_logits(base_logits: np.ndarray, node_off: np.ndarray, plans, node_tok: np.ndarray,
+                 dtype: str) -> np.ndarray:
+    out = base_logits.copy()
+    hi, lo = plant_value(PLANT_HI, dtype), plant_value(PLANT_LO, dtype)
+    for b, plan in enumerate(plans):
+        o = int(node_off[b])
         for u, c, v in plan:
             out[o + u, int(node_tok[o + c])] = hi if v > 0 else lo
     return out
@@ -444,3 +452,111 @@ def pool_key_flags(wl: Workload, slab_flags: Sequence[np.ndarray]) -> np.ndarray
         s0 = int(wl.seq_base[b])
         f[s0:s0 + len(sf)] = sf
     return f
+
+
+
+# ----------------------------------------------------------------------------
+# Multi-step decoding: a pool that lives across steps, per-step model outputs
+# ----------------------------------------------------------------------------
+
+STEP_STREAMS = ("hidden", "q", "k_tree", "v_tree", "base_logits", "plant")
+
+
+@dataclass
+class DecodeSetup:
+    cfg: Config
+    seed: int
+    lens: np.ndarray            # int32 [B] committed rows before the first step
+    seq_base: np.ndarray        # int64 [B]
+    seq_cap: np.ndarray         # int32 [B] slab rows: the budget of the whole run
+    pool_k: np.ndarray          # [n_kv, cap_total, d] stored, committed rows filled
+    pool_v: np.ndarray
+    default: Tree               # default tree, pruned each step to the slab's free rows
+    head_w: np.ndarray          # [n_heads, vocab, hidden]
+    w1: np.ndarray | None       # [n_heads, hidden, hidden] residual blocks, or None
+    b1: np.ndarray | None       # [n_heads, hidden]
+    root_tok: np.ndarray        # int32 [B] first step's root tokens
+    p_accept: np.ndarray        # float64 [B] planted acceptance per level
+    temperature: float | None   # sampled next token at this temperature, or greedy (None)
+    sample_seed: int
+
+    @property
+    def cap_total(self) -> int:
+        return int(self.pool_k.shape[1])
+
+
+@dataclass
+class StepInputs:
+    hidden: np.ndarray          # [len(seqs), hidden] the base model's last hidden states
+    q: np.ndarray               # [sumN, n_q, d]
+    tree_k: np.ndarray          # [n_kv, sumN, d] K/V rows of the tree nodes, node order
+    tree_v: np.ndarray
+    base_logits: np.ndarray     # [sumN, vocab] before planting
+    plans: list                 # planted walks per active sequence
+
+
+def decode_setup(cfg: Config, seed: int, default: Tree, room: Sequence[int], resblock: bool = True,
+                 temperature: float | None = 0.8, lens: Sequence[int] | None = None) -> DecodeSetup:
+    """Initial state of a multi-step run: each slab holds its committed rows
+    and room[b] free rows for the whole run."""
+    ss = dict(zip(STREAMS, np.random.SeedSequence(seed).spawn(len(STREAMS))))
+    rng = {k: np.random.Generator(np.random.PCG64(v)) for k, v in ss.items()}
+    B, d, dt = cfg.B, cfg.head_dim, cfg.dtype
+    L = _lens(cfg, rng["lens"]) if lens is None else np.asarray(lens, np.int32)
+    caps = (L.astype(np.int64) + np.asarray(room, np.int64)).astype(np.int32)
+    base = np.zeros(B, dtype=np.int64)
+    row = 1
+    for b in range(B):
+        base[b] = row
+        row += int(caps[b]) + 1
+    if dt == "fp32":
+        pk = np.full((cfg.n_kv, row, d), CANARY_FP32, dtype=np.uint32)
+        free = FREE_FP32
+    else:
+        pk = np.full((cfg.n_kv, row, d), CANARY_BF16, dtype=np.uint16)
+        free = FREE_BF16
+    pv = pk.copy()
+    kc, vc = ss["k_comm"].spawn(B), ss["v_comm"].spawn(B)
+    for b in range(B):
+        s0, Lb, cb = int(base[b]), int(L[b]), int(caps[b])
+        for dst, sc in ((pk, kc[b]), (pv, vc[b])):
+            dst[:, s0:s0 + cb, :] = free
+            dst[:, s0:s0 + Lb, :] = _store(normals(sc, cfg.n_kv * Lb * d), dt).reshape(cfg.n_kv, Lb, d).view(dst.dtype)
+    if dt == "fp32":
+        pk, pv = pk.view(np.float32), pv.view(np.float32)
+    hw = ss["head_w"].spawn(3)
+    head_w = _store(normals(hw[0], cfg.n_heads * cfg.vocab * cfg.hidden, cfg.w_std), dt)
+    head_w = head_w.reshape(cfg.n_heads, cfg.vocab, cfg.hidden)
+    w1 = b1 = None
+    if resblock:
+        w1 = _store(normals(hw[1], cfg.n_heads * cfg.hidden * cfg.hidden, cfg.w_std), dt)
+        w1 = w1.reshape(cfg.n_heads, cfg.hidden, cfg.hidden)
+        b1 = _store(normals(hw[2], cfg.n_heads * cfg.hidden, cfg.w_std), dt).reshape(cfg.n_heads, cfg.hidden)
+    root = rng["root"].integers(0, cfg.vocab, size=B).astype(np.int32)
+    pr = rng["plant"]
+    p = pr.uniform(cfg.p_range[0], cfg.p_range[1], size=B) if cfg.p_accept is None else np.full(B, cfg.p_accept)
+    return DecodeSetup(cfg=cfg, seed=seed, lens=L, seq_base=base, seq_cap=caps, pool_k=pk, pool_v=pv,
+                       default=default, head_w=head_w, w1=w1, b1=b1, root_tok=root, p_accept=p,
+                       temperature=temperature, sample_seed=seed * 7919 + 17)
+
+
+def tree_prefix(t: Tree, n: int) -> Tree:
+    """The first n nodes of a breadth-first tree (a tree again)."""
+    return Tree(t.parent[:n].copy(), t.depth[:n].copy(), t.rank[:n].copy())
+
+
+def decode_step_inputs(setup: DecodeSetup, step: int, seqs: Sequence[int], trees: Sequence[Tree]) -> StepInputs:
+    """The base model's outputs for one step of the active sequences `seqs`
+    (Gaussian stand-ins, drawn from (seed, step)), and the planted walks."""
+    cfg, dt, d = setup.cfg, setup.cfg.dtype, setup.cfg.head_dim
+    ss = dict(zip(STEP_STREAMS, np.random.SeedSequence([setup.seed, 1 + step]).spawn(len(STEP_STREAMS))))
+    n = [t.n for t in trees]
+    sumN = int(sum(n))
+    hidden = _store(normals(ss["hidden"], len(seqs) * cfg.hidden), dt).reshape(len(seqs), cfg.hidden)
+    q = _store(normals(ss["q"], sumN * cfg.n_q * d), dt).reshape(sumN, cfg.n_q, d)
+    tk = _store(normals(ss["k_tree"], cfg.n_kv * sumN * d), dt).reshape(cfg.n_kv, sumN, d)
+    tv = _store(normals(ss["v_tree"], cfg.n_kv * sumN * d), dt).reshape(cfg.n_kv, sumN, d)
+    lg = _store(normals(ss["base_logits"], sumN * cfg.vocab), dt).reshape(sumN, cfg.vocab)
+    plans, _ = plant_walks(list(trees), setup.p_accept[list(seqs)],
+                           np.random.Generator(np.random.PCG64(ss["plant"])))
+    return StepInputs(hidden=hidden, q=q, tree_k=tk, tree_v=tv, base_logits=lg, plans=plans)
