@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SPECMEMO_ABI_VERSION 4
+#define SPECMEMO_ABI_VERSION 5
 #define SPECMEMO_MAX_TREE_NODES 128 /* nodes per sequence's tree */
 #define SPECMEMO_MAX_DEPTH 15       /* tree depth (= Medusa heads) */
 #define SPECMEMO_MAX_TOPK 32        /* top-k per head */
@@ -74,7 +74,11 @@ typedef enum {
 typedef enum { SPECMEMO_FP32 = 0, SPECMEMO_BF16 = 1 } specmemo_dtype;
 
 typedef enum { SPECMEMO_ACCEPT_GREEDY = 0, SPECMEMO_ACCEPT_TYPICAL = 1 } specmemo_accept_mode;
-typedef enum { SPECMEMO_HEADS_ROWMAJOR = 0, SPECMEMO_HEADS_PACKED = 1 } specmemo_head_layout;
+typedef enum {
+  SPECMEMO_HEADS_ROWMAJOR = 0,
+  SPECMEMO_HEADS_PACKED = 1,
+  SPECMEMO_HEADS_INPUT_PER_HEAD = 2   /* flag, OR-ed with a layout: h is [n_heads][B][hidden] */
+} specmemo_head_layout;
 
 /* Ragged batch of candidate trees, CSR over nodes.  Device arrays are read by
  * kernels; the host mirrors (same contents) are read for validation and launch
@@ -118,7 +122,9 @@ typedef struct {
  * head_layout says: SPECMEMO_HEADS_ROWMAJOR is [n_heads][vocab][hidden] (the
  * nn.Linear out x in layout, no bias); SPECMEMO_HEADS_PACKED (bf16 only) is
  * the buffer written by specmemo_pack_heads, which the projection streams
- * contiguously.  root_tok: device [B]
+ * contiguously.  With SPECMEMO_HEADS_INPUT_PER_HEAD OR-ed in, h is
+ * [n_heads][B][hidden] and head i reads h[i] (e.g. the outputs of
+ * specmemo_medusa_resblock).  root_tok: device [B]
  * (the base model's own next token from the previous step).  logits_out:
  * device fp32 [B][n_heads][vocab], or NULL.  topk_ids: device int32
  * [B][n_heads][kmax] with kmax = max(topk_h); topk_vals: device fp32, same
@@ -131,6 +137,20 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
                          const void *head_w, int32_t head_layout, const int32_t *root_tok,
                          float *logits_out, int32_t *topk_ids, float *topk_vals,
                          int32_t *node_tok, void *ws, size_t ws_bytes, void *stream);
+
+/* Medusa residual-block heads.  The paper gives only a size per head; this
+ * reading gives each head one residual block before its vocabulary projection:
+ *   out[i][b][c] = h[b][c] + SiLU(sum_k w1[i][c][k] h[b][k] + b1[i][c]),
+ *   SiLU(x) = x / (1 + exp(-x)), fp32 accumulation, stored in `dt`;
+ * out then feeds specmemo_medusa_topk with SPECMEMO_HEADS_INPUT_PER_HEAD.
+ * h: device [B][hidden]; b1: device [n_heads][hidden]; out: device
+ * [n_heads][B][hidden].  w1: bf16 in SPECMEMO_HEADS_PACKED layout, written by
+ * specmemo_pack_heads(dt, n_heads, hidden, hidden, ...) from
+ * [n_heads][hidden][hidden] (out x in); fp32 in SPECMEMO_HEADS_ROWMAJOR.
+ * Requires 1 <= B <= SPECMEMO_MAX_BATCH, 1 <= n_heads <= SPECMEMO_MAX_DEPTH,
+ * hidden % 8 == 0. */
+int specmemo_medusa_resblock(specmemo_dtype dt, int32_t B, int32_t hidden, int32_t n_heads, const void *h,
+                             const void *w1, int32_t w1_layout, const void *b1, void *out, void *stream);
 
 /* Head weights in the projection's streaming order (bf16).  The heads are
  * fixed for a model, so they are packed once, at load time:
@@ -196,6 +216,20 @@ int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab,
                     const void *base_logits, const int32_t *node_tok, int32_t *accept_len,
                     int32_t *path, int32_t path_stride, int32_t *next_tok, void *ws,
                     size_t ws_bytes, void *stream);
+
+/* Sampled next token (in place of the greedy one that specmemo_accept writes):
+ * next_tok[b] is drawn from softmax(z / T) of the last accepted node's row,
+ * z = base_logits[node_off[b] + path[b][accept_len[b]]], by the Gumbel-max
+ * rule: the argmax over v of fmaf(z_v, 1/T, G_v) in fp32, with 1/T rounded
+ * once to fp32, G_v = -log(-log(u_v)) and u_v = ((x >> 40) + 1/2) / 2^24 for
+ * x the 64-bit word v % 4 of Philox4x64-10 (Salmon et al., SC 2011) with key
+ * (seed, offset) and counter (v / 4, b, 0, 0).  Ties go to the lower id.  A
+ * caller draws a fresh sample per step by changing offset.  Sequences whose
+ * accept_len / path entry is out of range keep their next_tok.  temperature
+ * must be positive and finite (and 1/T finite). */
+int specmemo_sample_next(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, float temperature,
+                         uint64_t seed, uint64_t offset, const void *base_logits, const int32_t *accept_len,
+                         const int32_t *path, int32_t path_stride, int32_t *next_tok, void *stream);
 
 /* (d) In-place KV compaction (Sec. 3.1 KV-cache paragraph: the preallocated
  * cache is a scratch space updated during verification; Sec. 3.3: rejected

@@ -332,7 +332,86 @@ __global__ __launch_bounds__(kNT) void accept_typical(AcceptArgs a) {
   }
 }
 
+// ---- sampled next token ---------------------------------------------------------
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds on a 4 x 64-bit
+// counter, each two 64 x 64 -> 128-bit products, the key bumped by the Weyl
+// constants between rounds.
+__device__ __forceinline__ void philox4x64_10(uint64_t (&x)[4], uint64_t k0, uint64_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B97F4A7C15ull;
+      k1 += 0xBB67AE8584CAA73Bull;
+    }
+    const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
+    const uint64_t hi0 = __umul64hi(m0, x[0]), lo0 = m0 * x[0];
+    const uint64_t hi1 = __umul64hi(m1, x[2]), lo1 = m1 * x[2];
+    x[0] = hi1 ^ x[1] ^ k0;
+    x[1] = lo1;
+    x[2] = hi0 ^ x[3] ^ k1;
+    x[3] = lo0;
+  }
+}
+
+// Gumbel-max draw from softmax(z / T) of sequence b's last accepted row: the
+// argmax over v of fmaf(z_v, 1/T, G_v), G_v = -log(-log(u_v)), u_v from
+// Philox with key (seed, offset), counter (v / 4, b, 0, 0), word v % 4, as
+// ((x >> 40) + 1/2) / 2^24.  One block per sequence; ties by lower token id.
+template <int DT>
+__global__ __launch_bounds__(256) void sample_next_kernel(SampleArgs a) {
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
+  const int acc = a.accept_len[b];
+  if (acc < 0 || acc >= a.path_stride) return;             // not an accepted path: next_tok untouched
+  const int node = a.path[(int64_t)b * a.path_stride + acc];
+  if (node < 0 || node >= N) return;
+  const int64_t row = (int64_t)(n0 + node) * a.vocab;
+  float best = -INFINITY;
+  int arg = a.vocab;
+  for (int q = tid; 4 * q < a.vocab; q += 256) {
+    uint64_t x[4] = {(uint64_t)q, (uint64_t)b, 0ull, 0ull};
+    philox4x64_10(x, a.seed, a.offset);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int v = 4 * q + j;
+      if (v < a.vocab) {
+        const float u = ((float)(x[j] >> 40) + 0.5f) * 0x1p-24f;
+        const float g = -logf(-logf(u));
+        const float s = fmaf(ld<DT>(a.logits, row + v), a.inv_temp, g);
+        if (better(s, v, best, arg)) {
+          best = s;
+          arg = v;
+        }
+      }
+    }
+  }
+  wave_argbest(best, arg);
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  if ((tid & 63) == 0) {
+    sv[tid >> 6] = best;
+    si[tid >> 6] = arg;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < 4; ++w)
+      if (better(sv[w], si[w], best, arg)) {
+        best = sv[w];
+        arg = si[w];
+      }
+    a.next_tok[b] = arg;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_sample_next(int dt, const SampleArgs &a, int B, hipStream_t st) {
+  if (dt == 1)
+    hipLaunchKernelGGL(sample_next_kernel<1>, dim3(B), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(sample_next_kernel<0>, dim3(B), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_accept(int dt, const AcceptArgs &a, int total_nodes, hipStream_t st) {
   if (a.mode == 0) {

@@ -366,6 +366,8 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
                          int32_t *node_tok, void *ws, size_t ws_bytes, void *stream) {
   int rc;
   if ((rc = check_dtype(dt))) return rc;
+  const bool per_head_input = head_layout & SPECMEMO_HEADS_INPUT_PER_HEAD;
+  head_layout &= ~SPECMEMO_HEADS_INPUT_PER_HEAD;
   if (head_layout != SPECMEMO_HEADS_ROWMAJOR && head_layout != SPECMEMO_HEADS_PACKED)
     return fail(SPECMEMO_E_ARG, "unknown head_layout %d", head_layout);
   if (head_layout == SPECMEMO_HEADS_PACKED && dt != SPECMEMO_BF16)
@@ -392,8 +394,9 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
     return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
   float *z = logits_out ? logits_out : static_cast<float *>(ws);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e = launch_head_logits(dt, h, head_w, head_layout == SPECMEMO_HEADS_PACKED, z, ti.B, hidden, vocab,
-                                    n_heads, st);
+  const int64_t h_head_stride = per_head_input ? (int64_t)ti.B * hidden : 0;
+  hipError_t e = launch_head_logits(dt, h, h_head_stride, head_w, head_layout == SPECMEMO_HEADS_PACKED, z, ti.B,
+                                    hidden, vocab, n_heads, st);
   if (e != hipSuccess) return hip_status(e, "head projection launch");
   TopkArgs a{};
   a.z = z;
@@ -409,6 +412,23 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
   a.vals = topk_vals;
   a.node_tok = node_tok;
   return hip_status(launch_topk(a, ti.B, st), "top-k launch");
+}
+
+int specmemo_medusa_resblock(specmemo_dtype dt, int32_t B, int32_t hidden, int32_t n_heads, const void *h,
+                             const void *w1, int32_t w1_layout, const void *b1, void *out, void *stream) {
+  int rc;
+  if ((rc = check_dtype(dt))) return rc;
+  if (B < 1 || B > SPECMEMO_MAX_BATCH) return fail(SPECMEMO_E_ARG, "B=%d outside [1, %d]", B, SPECMEMO_MAX_BATCH);
+  if (n_heads < 1 || n_heads > SPECMEMO_MAX_DEPTH) return fail(SPECMEMO_E_ARG, "n_heads=%d outside [1, %d]", n_heads, SPECMEMO_MAX_DEPTH);
+  if (hidden < 8 || hidden % 8) return fail(SPECMEMO_E_ARG, "hidden=%d must be a positive multiple of 8", hidden);
+  if (dt == SPECMEMO_BF16 && w1_layout != SPECMEMO_HEADS_PACKED)
+    return fail(SPECMEMO_E_ARG, "bf16 residual-block weights must be packed (specmemo_pack_heads with vocab = hidden)");
+  if (dt == SPECMEMO_FP32 && w1_layout != SPECMEMO_HEADS_ROWMAJOR)
+    return fail(SPECMEMO_E_DTYPE, "fp32 residual-block weights are row-major");
+  if (!al(h, 16) || !al(w1, 16) || !al(b1, 16) || !al(out, 16))
+    return fail(SPECMEMO_E_ARG, "h / w1 / b1 / out must be non-NULL and 16-byte aligned");
+  return hip_status(launch_resblock(dt, h, w1, b1, out, B, hidden, n_heads, static_cast<hipStream_t>(stream)),
+                    "residual block launch");
 }
 
 }  // extern "C"
@@ -548,6 +568,34 @@ int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, s
     a.best = static_cast<int32_t *>(ws);
   }
   return hip_status(launch_accept(dt, a, ti.total, static_cast<hipStream_t>(stream)), "acceptance launch");
+}
+
+int specmemo_sample_next(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, float temperature, uint64_t seed,
+                         uint64_t offset, const void *base_logits, const int32_t *accept_len, const int32_t *path,
+                         int32_t path_stride, int32_t *next_tok, void *stream) {
+  int rc;
+  if ((rc = check_dtype(dt))) return rc;
+  TreeInfo ti;
+  if ((rc = check_trees(t, &ti))) return rc;
+  if (vocab < 1) return fail(SPECMEMO_E_ARG, "vocab=%d", vocab);
+  if (!(temperature > 0.f) || !std::isfinite(temperature) || !std::isfinite(1.0f / temperature))
+    return fail(SPECMEMO_E_ARG, "temperature must be positive and finite with a finite inverse");
+  if (path_stride < ti.max_depth + 1) return fail(SPECMEMO_E_ARG, "path_stride=%d < max depth + 1 = %d", path_stride, ti.max_depth + 1);
+  if (!al(base_logits, 16)) return fail(SPECMEMO_E_ARG, "base_logits must be non-NULL and 16-byte aligned");
+  if (!al(accept_len, 4) || !al(path, 4) || !al(next_tok, 4))
+    return fail(SPECMEMO_E_ARG, "accept_len / path / next_tok must be non-NULL and 4-byte aligned");
+  SampleArgs a{};
+  a.logits = base_logits;
+  a.node_off = t->node_off;
+  a.accept_len = accept_len;
+  a.path = path;
+  a.vocab = vocab;
+  a.path_stride = path_stride;
+  a.inv_temp = 1.0f / temperature;
+  a.seed = seed;
+  a.offset = offset;
+  a.next_tok = next_tok;
+  return hip_status(launch_sample_next(dt, a, ti.B, static_cast<hipStream_t>(stream)), "sampling launch");
 }
 
 }  // extern "C"

@@ -29,8 +29,12 @@ struct TopkArgs {
   int32_t *node_tok;
 };
 
-hipError_t launch_head_logits(int dt, const void *h, const void *w, bool packed, float *z, int B, int hidden,
-                              int vocab, int n_heads, hipStream_t st);
+// h_head_stride: elements between the heads' inputs (0: every head reads the same h).
+hipError_t launch_head_logits(int dt, const void *h, int64_t h_head_stride, const void *w, bool packed, float *z,
+                              int B, int hidden, int vocab, int n_heads, hipStream_t st);
+// Medusa residual blocks: out[i][b] = h[b] + SiLU(W1_i h[b] + b1_i); bf16 W1 packed like the heads.
+hipError_t launch_resblock(int dt, const void *h, const void *w1, const void *b1, void *out, int B, int hidden,
+                           int n_heads, hipStream_t st);
 // Packed head weights: 64-row groups x 32-column k steps of 4 KB each.
 __host__ __device__ constexpr int packed_row_groups(int vocab) { return (vocab + 63) / 64; }
 __host__ __device__ constexpr int packed_k_steps(int hidden) { return (hidden + 31) / 32; }
@@ -94,6 +98,15 @@ struct AcceptArgs {
   int32_t *accept_len, *path, *next_tok;
 };
 hipError_t launch_accept(int dt, const AcceptArgs &a, int total_nodes, hipStream_t st);
+struct SampleArgs {
+  const void *logits;
+  const int32_t *node_off, *accept_len, *path;
+  int32_t vocab, path_stride;
+  float inv_temp;          // 1 / T, rounded once to fp32 on the host
+  uint64_t seed, offset;   // Philox key
+  int32_t *next_tok;
+};
+hipError_t launch_sample_next(int dt, const SampleArgs &a, int B, hipStream_t st);
 
 // ---- compaction ------------------------------------------------------------------
 struct CompactSeq {

@@ -23,8 +23,8 @@ constexpr int kUnroll = 2;         // k-steps of 32 issued before their MFMAs
 
 template <int NB>   // 16-wide batch tiles contracted per weight load
 __global__ __launch_bounds__(kWaves * 64) void head_logits_bf16(
-    const uint16_t *__restrict__ h, const uint16_t *__restrict__ W, float *__restrict__ z, int B,
-    int hidden, int vocab, int n_heads) {
+    const uint16_t *__restrict__ h, int64_t h_head_stride, const uint16_t *__restrict__ W, float *__restrict__ z,
+    int B, int hidden, int vocab, int n_heads) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int head = blockIdx.y, b0 = blockIdx.z * 16 * NB;
   const int gwave = blockIdx.x * kWaves + wave;
@@ -44,7 +44,7 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_bf16(
   for (int n = 0; n < NB; ++n) {
     int b = b0 + 16 * n + r16;
     bvalid[n] = b < B;
-    hp[n] = h + (int64_t)(bvalid[n] ? b : 0) * hidden + kq * 8;
+    hp[n] = h + head * h_head_stride + (int64_t)(bvalid[n] ? b : 0) * hidden + kq * 8;
   }
 
   f32x4 acc[NB][4];
@@ -124,10 +124,14 @@ __device__ __forceinline__ uint4 ld16_stream(const uint4 *p) {
   return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p)));
 }
 
-template <int NB>
+// EPI 0: fp32 logits z[b][head][row].  EPI 1: a Medusa residual block, the
+// rows being hidden units: out[head][b][row] = h[b][row] + SiLU(acc + bias[head][row])
+// in bf16, with h the block's own input.
+template <int NB, int EPI>
 __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
-    const uint16_t *__restrict__ h, const uint4 *__restrict__ Wp, float *__restrict__ z, int B, int hidden,
-    int vocab, int n_heads, int nG, int nS) {
+    const uint16_t *__restrict__ h, int64_t h_head_stride, const uint4 *__restrict__ Wp, float *__restrict__ z,
+    const uint16_t *__restrict__ bias, uint16_t *__restrict__ hout, int B, int hidden, int vocab, int n_heads,
+    int nG, int nS) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int head = blockIdx.y, b0 = blockIdx.z * 16 * NB;
   const int G = blockIdx.x * kWaves + wave;
@@ -140,7 +144,7 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
   for (int n = 0; n < NB; ++n) {
     const int b = b0 + 16 * n + (lane & 15);
     bvalid[n] = b < B;
-    hp[n] = h + (int64_t)(bvalid[n] ? b : 0) * hidden + kq * 8;
+    hp[n] = h + head * h_head_stride + (int64_t)(bvalid[n] ? b : 0) * hidden + kq * 8;
   }
   f32x4 acc[NB][4];
 #pragma unroll
@@ -180,13 +184,29 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
   for (int n = 0; n < NB; ++n) {
     const int b = b0 + 16 * n + (lane & 15);
     if (b >= B) continue;
-    float *zr = z + ((int64_t)b * n_heads + head) * vocab;
+    if constexpr (EPI == 0) {
+      float *zr = z + ((int64_t)b * n_heads + head) * vocab;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int row = 64 * G + t * 16 + 4 * kq;
+      for (int t = 0; t < 4; ++t) {
+        const int row = 64 * G + t * 16 + 4 * kq;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (row + j < vocab) zr[row + j] = acc[n][t][j];
+        for (int j = 0; j < 4; ++j)
+          if (row + j < vocab) zr[row + j] = acc[n][t][j];
+      }
+    } else {
+      const uint16_t *hin = h + head * h_head_stride + (int64_t)b * hidden;
+      const uint16_t *bh = bias + (int64_t)head * vocab;
+      uint16_t *o = hout + ((int64_t)head * B + b) * vocab;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int row = 64 * G + t * 16 + 4 * kq;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (row + j < vocab) {
+            const float y = acc[n][t][j] + bf16_to_f32(bh[row + j]);
+            o[row + j] = f32_to_bf16(bf16_to_f32(hin[row + j]) + y / (1.f + expf(-y)));
+          }
+      }
     }
   }
 }
@@ -215,15 +235,19 @@ __global__ __launch_bounds__(256) void pack_heads_bf16(const uint16_t *__restric
 // fp32 heads: one wave per vocabulary row, lanes stride the hidden dimension.
 constexpr int kF32BatchTile = 8;
 
-__global__ __launch_bounds__(256) void head_logits_f32(const float *__restrict__ h,
+// EPI as for the packed kernel (fp32 residual-block outputs).
+template <int EPI>
+__global__ __launch_bounds__(256) void head_logits_f32(const float *__restrict__ h, int64_t h_head_stride,
                                                        const float *__restrict__ W,
-                                                       float *__restrict__ z, int B, int hidden,
+                                                       float *__restrict__ z, const float *__restrict__ bias,
+                                                       float *__restrict__ hout, int B, int hidden,
                                                        int vocab, int n_heads) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int head = blockIdx.y;
   const int row = blockIdx.x * 4 + wave;
   if (row >= vocab) return;
   const float *wr = W + ((int64_t)head * vocab + row) * hidden;
+  h += head * h_head_stride;
   for (int b0 = 0; b0 < B; b0 += kF32BatchTile) {
     float acc[kF32BatchTile];
 #pragma unroll
@@ -239,7 +263,14 @@ __global__ __launch_bounds__(256) void head_logits_f32(const float *__restrict__
       float v = acc[j];
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-      if (lane == 0 && b0 + j < B) z[((int64_t)(b0 + j) * n_heads + head) * vocab + row] = v;
+      if (lane == 0 && b0 + j < B) {
+        if constexpr (EPI == 0) {
+          z[((int64_t)(b0 + j) * n_heads + head) * vocab + row] = v;
+        } else {
+          const float y = v + bias[(int64_t)head * vocab + row];
+          hout[((int64_t)head * B + b0 + j) * vocab + row] = h[(int64_t)(b0 + j) * hidden + row] + y / (1.f + expf(-y));
+        }
+      }
     }
   }
 }
@@ -439,26 +470,45 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
 
 }  // namespace
 
-hipError_t launch_head_logits(int dt, const void *h, const void *w, bool packed, float *z, int B, int hidden,
-                              int vocab, int n_heads, hipStream_t st) {
+hipError_t launch_head_logits(int dt, const void *h, int64_t h_head_stride, const void *w, bool packed, float *z,
+                              int B, int hidden, int vocab, int n_heads, hipStream_t st) {
   if (dt == 1 && packed) {
     const int nb = B <= 16 ? 1 : 2;
     const int nG = packed_row_groups(vocab), nS = packed_k_steps(hidden);
     dim3 grid((nG + kWaves - 1) / kWaves, n_heads, (B + 16 * nb - 1) / (16 * nb));
-    auto kern = nb == 1 ? head_logits_packed<1> : head_logits_packed<2>;
-    hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0, st, static_cast<const uint16_t *>(h),
-                       static_cast<const uint4 *>(w), z, B, hidden, vocab, n_heads, nG, nS);
+    auto kern = nb == 1 ? head_logits_packed<1, 0> : head_logits_packed<2, 0>;
+    hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0, st, static_cast<const uint16_t *>(h), h_head_stride,
+                       static_cast<const uint4 *>(w), z, nullptr, nullptr, B, hidden, vocab, n_heads, nG, nS);
   } else if (dt == 1) {
     const int nb = B <= 16 ? 1 : 2;
     dim3 grid((vocab + kWaves * kRowsPerWave - 1) / (kWaves * kRowsPerWave), n_heads,
               (B + 16 * nb - 1) / (16 * nb));
     auto kern = nb == 1 ? head_logits_bf16<1> : head_logits_bf16<2>;
-    hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0, st, static_cast<const uint16_t *>(h),
+    hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0, st, static_cast<const uint16_t *>(h), h_head_stride,
                        static_cast<const uint16_t *>(w), z, B, hidden, vocab, n_heads);
   } else {
     dim3 grid((vocab + 3) / 4, n_heads);
-    hipLaunchKernelGGL(head_logits_f32, grid, dim3(256), 0, st, static_cast<const float *>(h),
-                       static_cast<const float *>(w), z, B, hidden, vocab, n_heads);
+    hipLaunchKernelGGL(head_logits_f32<0>, grid, dim3(256), 0, st, static_cast<const float *>(h), h_head_stride,
+                       static_cast<const float *>(w), z, nullptr, nullptr, B, hidden, vocab, n_heads);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_resblock(int dt, const void *h, const void *w1, const void *b1, void *out, int B, int hidden,
+                           int n_heads, hipStream_t st) {
+  if (dt == 1) {
+    const int nb = B <= 16 ? 1 : 2;
+    const int nG = packed_row_groups(hidden), nS = packed_k_steps(hidden);
+    dim3 grid((nG + kWaves - 1) / kWaves, n_heads, (B + 16 * nb - 1) / (16 * nb));
+    auto kern = nb == 1 ? head_logits_packed<1, 1> : head_logits_packed<2, 1>;
+    hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0, st, static_cast<const uint16_t *>(h), (int64_t)0,
+                       static_cast<const uint4 *>(w1), nullptr, static_cast<const uint16_t *>(b1),
+                       static_cast<uint16_t *>(out), B, hidden, hidden, n_heads, nG, nS);
+  } else {
+    dim3 grid((hidden + 3) / 4, n_heads);
+    hipLaunchKernelGGL(head_logits_f32<1>, grid, dim3(256), 0, st, static_cast<const float *>(h), (int64_t)0,
+                       static_cast<const float *>(w1), nullptr, static_cast<const float *>(b1),
+                       static_cast<float *>(out), B, hidden, hidden, n_heads);
   }
   return hipGetLastError();
 }

@@ -128,3 +128,129 @@ class VerifyStep:
         self.tree_attn_padded(stream)
         self.accept(stream)
         self.kv_pad_update(stream)
+
+
+class DecodeLoop:
+    """Multi-step decoding through the library on one GPU.
+
+    The KV pool lives on the device across steps.  Per step: tree sizes from
+    the library's planner (the default tree pruned to each slab's free rows; a
+    full slab ends its sequence), the step's model outputs uploaded (the tree's
+    K/V rows written at slab rows L_b ..), residual-block heads and the
+    projection with top-k, the planted base-model logits (written on the device
+    at the tokens the heads chose), tree attention, greedy acceptance, the
+    next token (greedy or sampled), compaction.  The host reads back the
+    accepted lengths and next tokens once per step: they size the next step.
+    """
+
+    def __init__(self, setup, device="cuda", keep_logits: bool = True):
+        cfg = setup.cfg
+        self.setup, self.cfg, self.device, self.keep_logits = setup, cfg, device, keep_logits
+        self.dt = sm.FP32 if cfg.dtype == "fp32" else sm.BF16
+        self.k = to_device(setup.pool_k, cfg.dtype, device)
+        self.v = to_device(setup.pool_v, cfg.dtype, device)
+        head_w = to_device(setup.head_w, cfg.dtype, device)
+        self.head_layout = sm.HEADS_ROWMAJOR
+        if self.dt == sm.BF16:
+            packed = torch.empty(sm.packed_heads_bytes(self.dt, cfg.n_heads, cfg.vocab, cfg.hidden),
+                                 dtype=torch.uint8, device=device)
+            sm.pack_heads(self.dt, cfg.n_heads, cfg.vocab, cfg.hidden, head_w, packed)
+            head_w, self.head_layout = packed, sm.HEADS_PACKED
+        self.head_w = head_w
+        self.w1 = self.b1 = None
+        if setup.w1 is not None:
+            w1 = to_device(setup.w1, cfg.dtype, device)
+            self.w1_layout = sm.HEADS_ROWMAJOR
+            if self.dt == sm.BF16:
+                packed = torch.empty(sm.packed_heads_bytes(self.dt, cfg.n_heads, cfg.hidden, cfg.hidden),
+                                     dtype=torch.uint8, device=device)
+                sm.pack_heads(self.dt, cfg.n_heads, cfg.hidden, cfg.hidden, w1, packed)
+                w1, self.w1_layout = packed, sm.HEADS_PACKED
+            self.w1 = w1
+            self.b1 = to_device(setup.b1, cfg.dtype, device)
+        self.lens = setup.lens.astype(np.int32).copy()
+        self.root = setup.root_tok.astype(np.int32).copy()
+        self.stride = cfg.n_heads + 1
+        d = setup.default
+        self.default = (np.asarray(d.parent, np.int32), np.asarray(d.depth, np.int32), np.asarray(d.rank, np.int32))
+        from .synth import PLANT_HI, PLANT_LO
+        self._plant_hi, self._plant_lo = PLANT_HI, PLANT_LO   # the input generator's planted logits
+
+    def plan(self):
+        """Active sequences and their tree sizes for the next step."""
+        sizes = sm.plan_tree_sizes(self.lens, self.setup.seq_cap, len(self.default[0]))
+        seqs = [b for b in range(self.cfg.B) if sizes[b] > 0]
+        return seqs, [int(sizes[b]) for b in seqs]
+
+    def step(self, t: int, inputs=None):
+        """One step; returns its record (host copies), or None when every slab is full."""
+        from . import synth
+        cfg, st, dev = self.cfg, self.setup, self.device
+        seqs, sizes = self.plan()
+        if not seqs:
+            return None
+        trees = [synth.tree_prefix(synth.Tree(*self.default), n) for n in sizes]
+        inp = inputs if inputs is not None else synth.decode_step_inputs(st, t, seqs, trees)
+        node_off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+        parent = np.concatenate([tr.parent for tr in trees]).astype(np.int32)
+        depth = np.concatenate([tr.depth for tr in trees]).astype(np.int32)
+        rank = np.concatenate([tr.rank for tr in trees]).astype(np.int32)
+        sumN = int(node_off[-1])
+        tr = sm.Trees(node_off, parent, depth, rank, device=dev)
+        base, L, caps = st.seq_base[seqs], self.lens[seqs].copy(), st.seq_cap[seqs]
+        # the tree's K/V rows (the base model's) into the slabs
+        rows = np.concatenate([int(base[i]) + int(L[i]) + np.arange(sizes[i]) for i in range(len(seqs))])
+        ri = torch.from_numpy(rows.astype(np.int64)).to(dev)
+        self.k[:, ri] = to_device(inp.tree_k, cfg.dtype, dev)
+        self.v[:, ri] = to_device(inp.tree_v, cfg.dtype, dev)
+        seq_len = torch.from_numpy(L).to(dev)
+        kv = sm.KVPool(self.k, self.v, seq_len, base, caps, L)
+        i32 = dict(dtype=torch.int32, device=dev)
+        B = len(seqs)
+        # heads
+        h = to_device(inp.hidden, cfg.dtype, dev)
+        layout = self.head_layout
+        if self.w1 is not None:
+            hh = torch.empty((cfg.n_heads, B, cfg.hidden), dtype=h.dtype, device=dev)
+            sm.medusa_resblock(self.dt, B, cfg.hidden, cfg.n_heads, h, self.w1, self.b1, hh,
+                               w1_layout=self.w1_layout)
+            h, layout = hh, layout | sm.HEADS_INPUT_PER_HEAD
+        logits = torch.empty((B, cfg.n_heads, cfg.vocab), dtype=torch.float32, device=dev) if self.keep_logits else None
+        ws_topk = sm.workspace_bytes(sm.WS_TOPK, self.dt, tr, None, cfg.n_heads, cfg.vocab)
+        ws_attn = sm.workspace_bytes(sm.WS_ATTN, self.dt, tr, kv, cfg.n_q)
+        ws_acc = sm.workspace_bytes(sm.WS_ACCEPT, self.dt, tr, None, sm.GREEDY)
+        ws_bytes = max(ws_topk, ws_attn, ws_acc, 16)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+        ids = torch.empty((B, cfg.n_heads, cfg.kmax), **i32)
+        tok = torch.empty(sumN, **i32)
+        root = torch.from_numpy(self.root[seqs].copy()).to(dev)
+        sm.medusa_topk(self.dt, tr, cfg.hidden, cfg.vocab, cfg.n_heads, cfg.topk, h, self.head_w, root, ids, tok,
+                       logits_out=logits, ws=ws, ws_bytes=ws_bytes, head_layout=layout)
+        # the base model's logits, with the planted walk at the chosen tokens
+        lg = to_device(inp.base_logits, cfg.dtype, dev)
+        pr, pc, pv = [], [], []
+        for i, plan in enumerate(inp.plans):
+            for u, c, val in plan:
+                pr.append(int(node_off[i]) + u)
+                pc.append(int(node_off[i]) + c)
+                pv.append(self._plant_hi if val > 0 else self._plant_lo)
+        if pr:
+            cols = tok[torch.tensor(pc, dtype=torch.int64, device=dev)].to(torch.int64)
+            lg[torch.tensor(pr, dtype=torch.int64, device=dev), cols] = torch.tensor(pv, dtype=lg.dtype, device=dev)
+        # attention, acceptance, next token, compaction
+        q = to_device(inp.q, cfg.dtype, dev)
+        out = torch.empty_like(q)
+        sm.tree_attn(self.dt, tr, kv, cfg.n_q, q, out, ws=ws, ws_bytes=ws_bytes)
+        acc = torch.empty(B, **i32)
+        path = torch.empty((B, self.stride), **i32)
+        nxt = torch.empty(B, **i32)
+        sm.accept(self.dt, tr, cfg.vocab, sm.GREEDY, lg, tok, acc, path, self.stride, nxt, ws=ws, ws_bytes=ws_bytes)
+        if st.temperature is not None:
+            sm.sample_next(self.dt, tr, cfg.vocab, st.temperature, st.sample_seed, t, lg, acc, path, self.stride, nxt)
+        sm.kv_compact(self.dt, tr, kv, acc, path, self.stride)
+        acc_h, nxt_h = acc.cpu().numpy(), nxt.cpu().numpy()
+        self.lens[seqs] = L + acc_h + 1
+        self.root[seqs] = nxt_h
+        return dict(step=t, seqs=seqs, sizes=sizes, z=None if logits is None else logits.cpu().numpy(),
+                    ids=ids.cpu().numpy(), tok=tok.cpu().numpy(), attn=out, acc=acc_h, path=path.cpu().numpy(),
+                    next_tok=nxt_h, seq_len=seq_len.cpu().numpy(), lens=self.lens.copy())
