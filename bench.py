@@ -194,6 +194,65 @@ def padded_report(torch, cfg, wl, step, steps, history=150):
                                  "GBps": round(attn_bytes / (ta * 1e-3) / 1e9, 1)}}
 
 
+def decode_report(torch, cfg, wl, steps=48, warmup=3):
+    """Multi-step decoding on the same batch: residual-block heads, the
+    sampled next token, trees sized each step from the slabs' free rows (each
+    slab has 64 + U[0, 160) free rows for the run, so some trees shrink), the
+    next token chained as the next root, one host read-back per step.  The
+    base model's per-step outputs (hidden states, queries, tree K/V rows,
+    logits) are Gaussian draws made on the device before timing; the host
+    planning, the planted walks and the read-back are inside the timed loop."""
+    from paper_2506_01986_amd import runner, synth
+    rng = np.random.default_rng(cfg.seed + 2000)
+    room = (64 + rng.integers(0, 160, cfg.B)).astype(np.int32)
+    setup = synth.decode_setup(cfg, cfg.seed + 2000, synth.t64(), room, resblock=True, temperature=0.8,
+                               lens=wl.lens, head_w=wl.head_w)
+    loop = runner.DecodeLoop(setup, keep_logits=False, timing=True)
+    nmax = cfg.B * setup.default.n
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(cfg.seed + 2000)
+    bf = torch.bfloat16
+    rnd = lambda *shape: torch.randn(*shape, generator=gen, device="cuda", dtype=bf)
+    pre = [dict(h=rnd(cfg.B, cfg.hidden), q=rnd(nmax, cfg.n_q, cfg.head_dim), k=rnd(cfg.n_kv, nmax, cfg.head_dim),
+                v=rnd(cfg.n_kv, nmax, cfg.head_dim), lg=rnd(nmax, cfg.vocab)) for _ in range(warmup + steps)]
+    prng = np.random.default_rng(cfg.seed + 2001)
+
+    def inputs_for(t):
+        seqs, sizes = loop.plan()
+        trees = [synth.tree_prefix(setup.default, n) for n in sizes]
+        plans, _ = synth.plant_walks(trees, setup.p_accept[seqs], prng)
+        n, x = int(sum(sizes)), pre[t]
+        return synth.StepInputs(hidden=x["h"][:len(seqs)], q=x["q"][:n], tree_k=x["k"][:, :n], tree_v=x["v"][:, :n],
+                                base_logits=x["lg"][:n], plans=plans)
+
+    for t in range(warmup):
+        loop.step(t, inputs_for(t), record=False)
+    torch.cuda.synchronize()
+    loop.events.clear()
+    acc_tokens = tree_tokens = done = 0
+    w0 = time.perf_counter()
+    for t in range(warmup, warmup + steps):
+        if not loop.plan()[0]:
+            break
+        rec = loop.step(t, inputs_for(t), record=False)
+        acc_tokens += int(np.sum(rec["acc"] + 1))
+        tree_tokens += int(sum(rec["sizes"]))
+        done += 1
+    wall = time.perf_counter() - w0
+    ph = {k: float(np.mean([e[k] for e in loop.events])) for k in loop.events[0]}
+    rb_bytes = cfg.n_heads * cfg.hidden * cfg.hidden * cfg.elem_bytes
+    return {"steps": done, "ms_per_step": round(wall / done * 1e3, 4),
+            "tree_tokens_per_step": round(tree_tokens / done, 1),
+            "accepted_tokens_per_step": round(acc_tokens / done, 2),
+            "accepted_tokens_per_s": round(acc_tokens / wall, 1),
+            "value": round(tree_tokens / wall, 1),
+            "full_slabs": int(np.sum(loop.lens >= setup.seq_cap)),
+            "phase_ms": {k: round(v, 5) for k, v in ph.items()},
+            "resblock": {"ms": round(ph["resblock"], 5), "weight_bytes": rb_bytes,
+                         "GBps": round(rb_bytes / (ph["resblock"] * 1e-3) / 1e9, 1),
+                         "hbm_frac": round(rb_bytes / (ph["resblock"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}}
+
+
 def budget_report(cfg, wl, device_bytes, reps=2000):
     """The memory model and Alg. 1's plan for the workload's model on this
     device (host calls of the library), with their host times and the
@@ -246,6 +305,7 @@ def main():
     ap.add_argument("--config", default="llama2_70b_b10")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-padded", action="store_true", help="skip the padded-batching comparison")
+    ap.add_argument("--no-decode", action="store_true", help="skip the multi-step decode run")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="also run a device-to-device copy of BYTES (counter calibration)")
     args = ap.parse_args()
@@ -382,6 +442,9 @@ def main():
                                                   * cfg.elem_bytes * cfg.layers)
         pr["step_time_vs_compaction"] = round(pr["ms_per_step"] / ms, 4)
         result["padded"] = pr
+    if not args.no_decode and cfg.dtype == "bf16":
+        print("[bench] multi-step decode", file=sys.stderr, flush=True)
+        result["decode"] = decode_report(torch, cfg, wl)
     if cfg.params:
         print("[bench] memory budget plan (host)", file=sys.stderr, flush=True)
         result["budget"] = budget_report(cfg, wl, torch.cuda.get_device_properties(0).total_memory)

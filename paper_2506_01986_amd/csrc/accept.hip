@@ -356,9 +356,13 @@ __device__ __forceinline__ void philox4x64_10(uint64_t (&x)[4], uint64_t k0, uin
 // Gumbel-max draw from softmax(z / T) of sequence b's last accepted row: the
 // argmax over v of fmaf(z_v, 1/T, G_v), G_v = -log(-log(u_v)), u_v from
 // Philox with key (seed, offset), counter (v / 4, b, 0, 0), word v % 4, as
-// ((x >> 40) + 1/2) / 2^24.  One block per sequence; ties by lower token id.
+// ((x >> 40) + 1/2) / 2^24.  One block per sequence (the keys cost two
+// logarithms and a Philox block per four tokens: all sixteen waves of the
+// block share the row); ties by lower token id.
+constexpr int kSampleThreads = 1024;
+
 template <int DT>
-__global__ __launch_bounds__(256) void sample_next_kernel(SampleArgs a) {
+__global__ __launch_bounds__(kSampleThreads) void sample_next_kernel(SampleArgs a) {
   const int b = blockIdx.x, tid = threadIdx.x;
   const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
   const int acc = a.accept_len[b];
@@ -368,7 +372,7 @@ __global__ __launch_bounds__(256) void sample_next_kernel(SampleArgs a) {
   const int64_t row = (int64_t)(n0 + node) * a.vocab;
   float best = -INFINITY;
   int arg = a.vocab;
-  for (int q = tid; 4 * q < a.vocab; q += 256) {
+  for (int q = tid; 4 * q < a.vocab; q += kSampleThreads) {
     uint64_t x[4] = {(uint64_t)q, (uint64_t)b, 0ull, 0ull};
     philox4x64_10(x, a.seed, a.offset);
 #pragma unroll
@@ -386,15 +390,16 @@ __global__ __launch_bounds__(256) void sample_next_kernel(SampleArgs a) {
     }
   }
   wave_argbest(best, arg);
-  __shared__ float sv[4];
-  __shared__ int si[4];
+  constexpr int kW = kSampleThreads / 64;
+  __shared__ float sv[kW];
+  __shared__ int si[kW];
   if ((tid & 63) == 0) {
     sv[tid >> 6] = best;
     si[tid >> 6] = arg;
   }
   __syncthreads();
   if (tid == 0) {
-    for (int w = 1; w < 4; ++w)
+    for (int w = 1; w < kW; ++w)
       if (better(sv[w], si[w], best, arg)) {
         best = sv[w];
         arg = si[w];
@@ -407,9 +412,9 @@ __global__ __launch_bounds__(256) void sample_next_kernel(SampleArgs a) {
 
 hipError_t launch_sample_next(int dt, const SampleArgs &a, int B, hipStream_t st) {
   if (dt == 1)
-    hipLaunchKernelGGL(sample_next_kernel<1>, dim3(B), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(sample_next_kernel<1>, dim3(B), dim3(kSampleThreads), 0, st, a);
   else
-    hipLaunchKernelGGL(sample_next_kernel<0>, dim3(B), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(sample_next_kernel<0>, dim3(B), dim3(kSampleThreads), 0, st, a);
   return hipGetLastError();
 }
 

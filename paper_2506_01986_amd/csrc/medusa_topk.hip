@@ -124,14 +124,10 @@ __device__ __forceinline__ uint4 ld16_stream(const uint4 *p) {
   return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p)));
 }
 
-// EPI 0: fp32 logits z[b][head][row].  EPI 1: a Medusa residual block, the
-// rows being hidden units: out[head][b][row] = h[b][row] + SiLU(acc + bias[head][row])
-// in bf16, with h the block's own input.
-template <int NB, int EPI>
+template <int NB>
 __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
     const uint16_t *__restrict__ h, int64_t h_head_stride, const uint4 *__restrict__ Wp, float *__restrict__ z,
-    const uint16_t *__restrict__ bias, uint16_t *__restrict__ hout, int B, int hidden, int vocab, int n_heads,
-    int nG, int nS) {
+    int B, int hidden, int vocab, int n_heads, int nG, int nS) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int head = blockIdx.y, b0 = blockIdx.z * 16 * NB;
   const int G = blockIdx.x * kWaves + wave;
@@ -184,29 +180,105 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
   for (int n = 0; n < NB; ++n) {
     const int b = b0 + 16 * n + (lane & 15);
     if (b >= B) continue;
-    if constexpr (EPI == 0) {
-      float *zr = z + ((int64_t)b * n_heads + head) * vocab;
+    float *zr = z + ((int64_t)b * n_heads + head) * vocab;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int row = 64 * G + t * 16 + 4 * kq;
+    for (int t = 0; t < 4; ++t) {
+      const int row = 64 * G + t * 16 + 4 * kq;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (row + j < vocab) zr[row + j] = acc[n][t][j];
-      }
-    } else {
-      const uint16_t *hin = h + head * h_head_stride + (int64_t)b * hidden;
-      const uint16_t *bh = bias + (int64_t)head * vocab;
-      uint16_t *o = hout + ((int64_t)head * B + b) * vocab;
+      for (int j = 0; j < 4; ++j)
+        if (row + j < vocab) zr[row + j] = acc[n][t][j];
+    }
+  }
+}
+
+// Medusa residual blocks on packed weights: out[head][b][row] =
+// h[b][row] + SiLU(sum_k W1[head][row][k] h[b][k] + b1[head][row]), in bf16.
+// A block's four waves share one 64-row group and split its k steps in four
+// contiguous ranges (hidden x hidden weights have 64x fewer row groups per
+// head than a vocabulary projection, so one wave per row group would leave
+// most compute units idle); the partial sums meet in LDS.
+constexpr int kResSplit = 4;
+
+template <int NB>
+__global__ __launch_bounds__(kResSplit * 64) void resblock_packed(
+    const uint16_t *__restrict__ h, const uint4 *__restrict__ Wp, const uint16_t *__restrict__ bias,
+    uint16_t *__restrict__ hout, int B, int hidden, int nG, int nS) {
+  __shared__ f32x4 red[kResSplit - 1][NB][4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int G = blockIdx.x, head = blockIdx.y, b0 = blockIdx.z * 16 * NB;
+  const int kq = lane >> 4;
+  const uint4 *wp = Wp + (int64_t)(head * nG + G) * nS * 4 * 64 + lane;
+  bool bvalid[NB];
+  const uint16_t *hp[NB];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int row = 64 * G + t * 16 + 4 * kq;
+  for (int n = 0; n < NB; ++n) {
+    const int b = b0 + 16 * n + (lane & 15);
+    bvalid[n] = b < B;
+    hp[n] = h + (int64_t)(bvalid[n] ? b : 0) * hidden + kq * 8;
+  }
+  f32x4 acc[NB][4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (row + j < vocab) {
-            const float y = acc[n][t][j] + bf16_to_f32(bh[row + j]);
-            o[row + j] = f32_to_bf16(bf16_to_f32(hin[row + j]) + y / (1.f + expf(-y)));
-          }
-      }
+  for (int n = 0; n < NB; ++n)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[n][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto step = [&](const uint4 (&a)[4], int s) {
+    const int k = 32 * s + 8 * kq;
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+      const bf16x8 bv = __builtin_bit_cast(bf16x8, ld16_or_zero(bvalid[n] && k < hidden, hp[n] + 32 * s));
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        acc[n][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[t]), bv, acc[n][t], 0, 0, 0);
+    }
+  };
+  const int s_end = (wave + 1) * nS / kResSplit;
+  int s = wave * nS / kResSplit;
+  for (; s + kPackedUnroll <= s_end; s += kPackedUnroll) {
+    uint4 a[kPackedUnroll][4];
+#pragma unroll
+    for (int u = 0; u < kPackedUnroll; ++u)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) a[u][t] = ld16_stream(wp + ((s + u) * 4 + t) * 64);
+#pragma unroll
+    for (int u = 0; u < kPackedUnroll; ++u) step(a[u], s + u);
+  }
+  for (; s < s_end; ++s) {
+    uint4 a[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) a[t] = ld16_stream(wp + (s * 4 + t) * 64);
+    step(a, s);
+  }
+  if (wave > 0) {
+#pragma unroll
+    for (int n = 0; n < NB; ++n)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) red[wave - 1][n][t][lane] = acc[n][t];
+  }
+  __syncthreads();
+  if (wave > 0) return;
+#pragma unroll
+  for (int w = 0; w < kResSplit - 1; ++w)
+#pragma unroll
+    for (int n = 0; n < NB; ++n)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[n][t] += red[w][n][t][lane];
+  // C layout: lane holds column (batch) lane&15, rows 4*(lane>>4) + 0..3 of each tile.
+#pragma unroll
+  for (int n = 0; n < NB; ++n) {
+    const int b = b0 + 16 * n + (lane & 15);
+    if (b >= B) continue;
+    const uint16_t *hin = h + (int64_t)b * hidden;
+    const uint16_t *bh = bias + (int64_t)head * hidden;
+    uint16_t *o = hout + ((int64_t)head * B + b) * hidden;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int row = 64 * G + t * 16 + 4 * kq;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (row + j < hidden) {
+          const float y = acc[n][t][j] + bf16_to_f32(bh[row + j]);
+          o[row + j] = f32_to_bf16(bf16_to_f32(hin[row + j]) + y / (1.f + expf(-y)));
+        }
     }
   }
 }
@@ -476,9 +548,9 @@ hipError_t launch_head_logits(int dt, const void *h, int64_t h_head_stride, cons
     const int nb = B <= 16 ? 1 : 2;
     const int nG = packed_row_groups(vocab), nS = packed_k_steps(hidden);
     dim3 grid((nG + kWaves - 1) / kWaves, n_heads, (B + 16 * nb - 1) / (16 * nb));
-    auto kern = nb == 1 ? head_logits_packed<1, 0> : head_logits_packed<2, 0>;
+    auto kern = nb == 1 ? head_logits_packed<1> : head_logits_packed<2>;
     hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0, st, static_cast<const uint16_t *>(h), h_head_stride,
-                       static_cast<const uint4 *>(w), z, nullptr, nullptr, B, hidden, vocab, n_heads, nG, nS);
+                       static_cast<const uint4 *>(w), z, B, hidden, vocab, n_heads, nG, nS);
   } else if (dt == 1) {
     const int nb = B <= 16 ? 1 : 2;
     dim3 grid((vocab + kWaves * kRowsPerWave - 1) / (kWaves * kRowsPerWave), n_heads,
@@ -499,11 +571,11 @@ hipError_t launch_resblock(int dt, const void *h, const void *w1, const void *b1
   if (dt == 1) {
     const int nb = B <= 16 ? 1 : 2;
     const int nG = packed_row_groups(hidden), nS = packed_k_steps(hidden);
-    dim3 grid((nG + kWaves - 1) / kWaves, n_heads, (B + 16 * nb - 1) / (16 * nb));
-    auto kern = nb == 1 ? head_logits_packed<1, 1> : head_logits_packed<2, 1>;
-    hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0, st, static_cast<const uint16_t *>(h), (int64_t)0,
-                       static_cast<const uint4 *>(w1), nullptr, static_cast<const uint16_t *>(b1),
-                       static_cast<uint16_t *>(out), B, hidden, hidden, n_heads, nG, nS);
+    dim3 grid(nG, n_heads, (B + 16 * nb - 1) / (16 * nb));
+    auto kern = nb == 1 ? resblock_packed<1> : resblock_packed<2>;
+    hipLaunchKernelGGL(kern, grid, dim3(kResSplit * 64), 0, st, static_cast<const uint16_t *>(h),
+                       static_cast<const uint4 *>(w1), static_cast<const uint16_t *>(b1),
+                       static_cast<uint16_t *>(out), B, hidden, nG, nS);
   } else {
     dim3 grid((hidden + 3) / 4, n_heads);
     hipLaunchKernelGGL(head_logits_f32<1>, grid, dim3(256), 0, st, static_cast<const float *>(h), (int64_t)0,

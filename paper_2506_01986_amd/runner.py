@@ -15,7 +15,10 @@ from .synth import Workload
 
 
 def to_device(x: np.ndarray, dtype: str, device) -> torch.Tensor:
-    """Stored array (float32, or uint16 bf16 bits) -> device tensor of that type."""
+    """Stored array (float32, or uint16 bf16 bits) -> device tensor of that type
+    (a tensor already on the device passes through)."""
+    if isinstance(x, torch.Tensor):
+        return x
     if dtype == "fp32":
         return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(device)
     t = torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).to(device)
@@ -143,8 +146,9 @@ class DecodeLoop:
     accepted lengths and next tokens once per step: they size the next step.
     """
 
-    def __init__(self, setup, device="cuda", keep_logits: bool = True):
+    def __init__(self, setup, device="cuda", keep_logits: bool = True, timing: bool = False):
         cfg = setup.cfg
+        self.timing, self.events = timing, []
         self.setup, self.cfg, self.device, self.keep_logits = setup, cfg, device, keep_logits
         self.dt = sm.FP32 if cfg.dtype == "fp32" else sm.BF16
         self.k = to_device(setup.pool_k, cfg.dtype, device)
@@ -182,8 +186,10 @@ class DecodeLoop:
         seqs = [b for b in range(self.cfg.B) if sizes[b] > 0]
         return seqs, [int(sizes[b]) for b in seqs]
 
-    def step(self, t: int, inputs=None):
-        """One step; returns its record (host copies), or None when every slab is full."""
+    def step(self, t: int, inputs=None, record: bool = True):
+        """One step; returns its record (host copies when `record`), or None when
+        every slab is full.  The step's integer arrays go to the device in one
+        copy, and the accepted lengths and next tokens come back in one."""
         from . import synth
         cfg, st, dev = self.cfg, self.setup, self.device
         seqs, sizes = self.plan()
@@ -191,66 +197,90 @@ class DecodeLoop:
             return None
         trees = [synth.tree_prefix(synth.Tree(*self.default), n) for n in sizes]
         inp = inputs if inputs is not None else synth.decode_step_inputs(st, t, seqs, trees)
+        B = len(seqs)
         node_off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+        sumN = int(node_off[-1])
         parent = np.concatenate([tr.parent for tr in trees]).astype(np.int32)
         depth = np.concatenate([tr.depth for tr in trees]).astype(np.int32)
         rank = np.concatenate([tr.rank for tr in trees]).astype(np.int32)
-        sumN = int(node_off[-1])
-        tr = sm.Trees(node_off, parent, depth, rank, device=dev)
         base, L, caps = st.seq_base[seqs], self.lens[seqs].copy(), st.seq_cap[seqs]
+        rows = np.concatenate([int(base[i]) + int(L[i]) + np.arange(sizes[i]) for i in range(B)]).astype(np.int32)
+        plant = np.array([(int(node_off[i]) + u, int(node_off[i]) + c, 1 if val > 0 else 0)
+                          for i, plan in enumerate(inp.plans) for u, c, val in plan], np.int32).reshape(-1, 3)
+        # one upload: [node_off | parent | depth | rank | root | L | rows | planted (row, child, hi)]
+        parts = [node_off, parent, depth, rank, self.root[seqs].astype(np.int32), L.astype(np.int32), rows,
+                 plant.T.reshape(-1)]
+        offs = np.concatenate([[0], np.cumsum([len(a) for a in parts])])
+        buf = torch.from_numpy(np.concatenate(parts)).to(dev)
+        view = [buf[int(offs[i]):int(offs[i + 1])] for i in range(len(parts))]
+        tr = sm.Trees(node_off, parent, depth, rank, dev_arrays=view[:4])
+        root, seq_len, rows_d = view[4], view[5], view[6]
+        plant_d = view[7].view(3, -1) if plant.size else None
         # the tree's K/V rows (the base model's) into the slabs
-        rows = np.concatenate([int(base[i]) + int(L[i]) + np.arange(sizes[i]) for i in range(len(seqs))])
-        ri = torch.from_numpy(rows.astype(np.int64)).to(dev)
+        ri = rows_d.to(torch.int64)
         self.k[:, ri] = to_device(inp.tree_k, cfg.dtype, dev)
         self.v[:, ri] = to_device(inp.tree_v, cfg.dtype, dev)
-        seq_len = torch.from_numpy(L).to(dev)
         kv = sm.KVPool(self.k, self.v, seq_len, base, caps, L)
         i32 = dict(dtype=torch.int32, device=dev)
-        B = len(seqs)
+        ev = {}
+
+        def mark(name):
+            if self.timing:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                ev[name] = e
+
         # heads
         h = to_device(inp.hidden, cfg.dtype, dev)
+        mark("start")
         layout = self.head_layout
         if self.w1 is not None:
             hh = torch.empty((cfg.n_heads, B, cfg.hidden), dtype=h.dtype, device=dev)
             sm.medusa_resblock(self.dt, B, cfg.hidden, cfg.n_heads, h, self.w1, self.b1, hh,
                                w1_layout=self.w1_layout)
             h, layout = hh, layout | sm.HEADS_INPUT_PER_HEAD
+        mark("resblock")
         logits = torch.empty((B, cfg.n_heads, cfg.vocab), dtype=torch.float32, device=dev) if self.keep_logits else None
-        ws_topk = sm.workspace_bytes(sm.WS_TOPK, self.dt, tr, None, cfg.n_heads, cfg.vocab)
-        ws_attn = sm.workspace_bytes(sm.WS_ATTN, self.dt, tr, kv, cfg.n_q)
-        ws_acc = sm.workspace_bytes(sm.WS_ACCEPT, self.dt, tr, None, sm.GREEDY)
-        ws_bytes = max(ws_topk, ws_attn, ws_acc, 16)
+        ws_bytes = max(sm.workspace_bytes(sm.WS_TOPK, self.dt, tr, None, cfg.n_heads, cfg.vocab),
+                       sm.workspace_bytes(sm.WS_ATTN, self.dt, tr, kv, cfg.n_q),
+                       sm.workspace_bytes(sm.WS_ACCEPT, self.dt, tr, None, sm.GREEDY), 16)
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
         ids = torch.empty((B, cfg.n_heads, cfg.kmax), **i32)
         tok = torch.empty(sumN, **i32)
-        root = torch.from_numpy(self.root[seqs].copy()).to(dev)
         sm.medusa_topk(self.dt, tr, cfg.hidden, cfg.vocab, cfg.n_heads, cfg.topk, h, self.head_w, root, ids, tok,
                        logits_out=logits, ws=ws, ws_bytes=ws_bytes, head_layout=layout)
+        mark("medusa_topk")
         # the base model's logits, with the planted walk at the chosen tokens
         lg = to_device(inp.base_logits, cfg.dtype, dev)
-        pr, pc, pv = [], [], []
-        for i, plan in enumerate(inp.plans):
-            for u, c, val in plan:
-                pr.append(int(node_off[i]) + u)
-                pc.append(int(node_off[i]) + c)
-                pv.append(self._plant_hi if val > 0 else self._plant_lo)
-        if pr:
-            cols = tok[torch.tensor(pc, dtype=torch.int64, device=dev)].to(torch.int64)
-            lg[torch.tensor(pr, dtype=torch.int64, device=dev), cols] = torch.tensor(pv, dtype=lg.dtype, device=dev)
+        if plant.size:
+            cols = tok[plant_d[1].to(torch.int64)].to(torch.int64)
+            vals = torch.where(plant_d[2] > 0, float(self._plant_hi), float(self._plant_lo)).to(lg.dtype)
+            lg[plant_d[0].to(torch.int64), cols] = vals
         # attention, acceptance, next token, compaction
         q = to_device(inp.q, cfg.dtype, dev)
         out = torch.empty_like(q)
+        mark("plant")
         sm.tree_attn(self.dt, tr, kv, cfg.n_q, q, out, ws=ws, ws_bytes=ws_bytes)
-        acc = torch.empty(B, **i32)
+        mark("tree_attn")
+        res = torch.empty((2, B), **i32)            # accepted lengths, next tokens: read back together
+        acc, nxt = res[0], res[1]
         path = torch.empty((B, self.stride), **i32)
-        nxt = torch.empty(B, **i32)
         sm.accept(self.dt, tr, cfg.vocab, sm.GREEDY, lg, tok, acc, path, self.stride, nxt, ws=ws, ws_bytes=ws_bytes)
+        mark("accept")
         if st.temperature is not None:
             sm.sample_next(self.dt, tr, cfg.vocab, st.temperature, st.sample_seed, t, lg, acc, path, self.stride, nxt)
+        mark("sample_next")
         sm.kv_compact(self.dt, tr, kv, acc, path, self.stride)
-        acc_h, nxt_h = acc.cpu().numpy(), nxt.cpu().numpy()
+        mark("kv_compact")
+        res_h = res.cpu().numpy()
+        acc_h, nxt_h = res_h[0].copy(), res_h[1].copy()
+        if self.timing:
+            names = list(ev)
+            self.events.append({b: ev[a].elapsed_time(ev[b]) for a, b in zip(names, names[1:])})
         self.lens[seqs] = L + acc_h + 1
         self.root[seqs] = nxt_h
-        return dict(step=t, seqs=seqs, sizes=sizes, z=None if logits is None else logits.cpu().numpy(),
-                    ids=ids.cpu().numpy(), tok=tok.cpu().numpy(), attn=out, acc=acc_h, path=path.cpu().numpy(),
-                    next_tok=nxt_h, seq_len=seq_len.cpu().numpy(), lens=self.lens.copy())
+        rec = dict(step=t, seqs=seqs, sizes=sizes, acc=acc_h, next_tok=nxt_h, lens=self.lens.copy())
+        if record:
+            rec.update(z=None if logits is None else logits.cpu().numpy(), ids=ids.cpu().numpy(),
+                       tok=tok.cpu().numpy(), attn=out, path=path.cpu().numpy(), seq_len=seq_len.cpu().numpy())
+        return rec

@@ -496,9 +496,10 @@ class StepInputs:
 
 
 def decode_setup(cfg: Config, seed: int, default: Tree, room: Sequence[int], resblock: bool = True,
-                 temperature: float | None = 0.8, lens: Sequence[int] | None = None) -> DecodeSetup:
+                 temperature: float | None = 0.8, lens: Sequence[int] | None = None,
+                 head_w: np.ndarray | None = None) -> DecodeSetup:
     """Initial state of a multi-step run: each slab holds its committed rows
-    and room[b] free rows for the whole run."""
+    and room[b] free rows for the whole run (head_w: reuse these head weights)."""
     ss = dict(zip(STREAMS, np.random.SeedSequence(seed).spawn(len(STREAMS))))
     rng = {k: np.random.Generator(np.random.PCG64(v)) for k, v in ss.items()}
     B, d, dt = cfg.B, cfg.head_dim, cfg.dtype
@@ -525,8 +526,9 @@ def decode_setup(cfg: Config, seed: int, default: Tree, room: Sequence[int], res
     if dt == "fp32":
         pk, pv = pk.view(np.float32), pv.view(np.float32)
     hw = ss["head_w"].spawn(3)
-    head_w = _store(normals(hw[0], cfg.n_heads * cfg.vocab * cfg.hidden, cfg.w_std), dt)
-    head_w = head_w.reshape(cfg.n_heads, cfg.vocab, cfg.hidden)
+    if head_w is None:
+        head_w = _store(normals(hw[0], cfg.n_heads * cfg.vocab * cfg.hidden, cfg.w_std), dt)
+        head_w = head_w.reshape(cfg.n_heads, cfg.vocab, cfg.hidden)
     w1 = b1 = None
     if resblock:
         w1 = _store(normals(hw[1], cfg.n_heads * cfg.hidden * cfg.hidden, cfg.w_std), dt)
