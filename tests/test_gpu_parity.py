@@ -230,6 +230,17 @@ EDGES = {
     "fp32_gqa": (edge_cfg(dtype="fp32", B=3, n_q=6, n_kv=2, head_dim=64, hidden=40, vocab=333, w_std=1.0),
                  lambda r: [synth.t16(), synth.random_tree(r, 30), synth.tree_from_rank_paths([()])],
                  [5, 0, 200]),
+    # the deepest trees: 15 heads (paths of 16 nodes), binary branching
+    "deep15": (edge_cfg(B=3, n_q=4, n_kv=2, hidden=32, vocab=64, n_heads=15, topk=(2,) * 15, p_accept=0.85),
+               lambda r: [synth.chain_tree(16), synth.random_tree(r, 60, max_depth=15, max_kids=2),
+                          synth.random_tree(r, 128, max_depth=15, max_kids=2)], [3, 50, 0]),
+    # the widest top-k (32 per head) and a 32-child root
+    "topk32": (edge_cfg(B=2, n_q=2, n_kv=1, hidden=64, vocab=100, n_heads=2, topk=(32, 32)),
+               lambda r: [synth.random_tree(r, 128, max_depth=2, max_kids=32), synth.star_tree(33)], [10, 300]),
+    # the largest batch (4096 sequences: 128 launch groups per stage), the smallest hidden size
+    "b4096": (edge_cfg(B=4096, n_q=1, n_kv=1, hidden=8, vocab=16, n_heads=1, topk=(4,)),
+              lambda r: [synth.random_tree(r, int(r.integers(1, 6)), max_depth=1, max_kids=4) for _ in range(4096)],
+              [int(x) for x in np.random.default_rng(6).integers(0, 31, 4096)]),
 }
 
 
