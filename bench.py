@@ -11,8 +11,10 @@ at 1.1 x live tokens).
 
 Prints one JSON line: the step throughput in verified tree tokens/s (sum of the
 tree sizes / step time), per-stage times and achieved bandwidth from HIP events
-on the stream the kernels run on, the roofline entry of the dominant kernel,
-and the CPU oracle's throughput on the same workload.
+on the stream the kernels run on, the roofline entry of the dominant kernel
+(the head projection, timed by itself over back-to-back launches), and the CPU
+oracle's throughput on the same workload; then the padded-batching variant, a
+multi-step decode run and the memory-budget plan on the same batch.
 """
 
 from __future__ import annotations
@@ -36,7 +38,10 @@ STAGE_KERNELS = {"medusa_topk": ["head_logits_packed", "topk_rows"],
                  "tree_attn": ["tree_attn_bf16", "tree_attn_combine"],
                  "accept": ["row_argbest_all", "accept_walk"], "kv_compact": ["kv_compact_kernel"]}
 STAGE_SOURCES = {"medusa_topk": "medusa_topk.hip", "tree_attn": "tree_attn.hip",
-                 "accept": "accept.hip", "kv_compact": "kv_compact.hip"}
+                 "accept": "accept.hip", "kv_compact": "kv_compact.hip",
+                 "head_logits_packed": "medusa_topk.hip"}
+# The dominant kernel of a stage, timed by itself for the roofline entry.
+DOMINANT_KERNEL = {"medusa_topk": "head_logits_packed"}
 
 
 def source_sha(stage):
@@ -87,6 +92,31 @@ def algorithmic_bytes(wl, acc):
     c = int(np.sum(acc + 1)) * cfg.vocab * s + sumN * 4
     d = 2 * int(np.sum(acc + 1)) * 2 * cfg.n_kv * cfg.head_dim * s
     return {"medusa_topk": a, "tree_attn": b, "accept": c, "kv_compact": d}
+
+
+def projection_kernel(torch, sm, step, cfg, steps):
+    """Average duration of the head projection kernel alone (the dominant
+    kernel of stage a): `steps` back-to-back launches through
+    specmemo_head_logits on the kernels' stream, HIP events at both ends.
+    Returns (ms, algorithmic bytes: weights + hidden states read, fp32 logits
+    written)."""
+    z = torch.empty((cfg.B, cfg.n_heads, cfg.vocab), dtype=torch.float32, device="cuda")
+
+    def call():
+        sm.head_logits(step.dt, cfg.B, cfg.hidden, cfg.vocab, cfg.n_heads, step.h, step.head_w, z,
+                       head_layout=step.head_layout)
+    for _ in range(2):
+        call()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    s = cfg.elem_bytes
+    nbytes = cfg.n_heads * cfg.vocab * cfg.hidden * s + cfg.B * cfg.hidden * s + cfg.B * cfg.n_heads * cfg.vocab * 4
+    return e0.elapsed_time(e1) / steps, nbytes
 
 
 def attention_flops(wl):
@@ -410,6 +440,19 @@ def main():
     st["tree_attn+kv_compact"] = {"ms": round(float(at), 5), "GBps": round(ab / (at * 1e-3) / 1e9, 1),
                                   "hbm_frac": round(ab / (at * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     dom = max(names, key=lambda n: st[n]["ms"])
+    if DOMINANT_KERNEL.get(dom) == "head_logits_packed" and step.head_layout == sm.HEADS_PACKED:
+        print("[bench] projection kernel alone", file=sys.stderr, flush=True)
+        kms, kbytes = projection_kernel(torch, sm, step, cfg, args.steps)
+        kgbs = kbytes / (kms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "kernel": "head_logits_packed", "stage": dom, "achieved": round(kgbs, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(kgbs / HBM_PEAK_GBS, 4),
+                    "traffic": measured_traffic("head_logits_packed", cfg.name), "algorithmic_bytes": kbytes,
+                    "ms": round(kms, 5), "source_sha256_16": source_sha("head_logits_packed")}
+    else:
+        roofline = {"bound": "hbm", "kernel": dom, "kernels": STAGE_KERNELS[dom], "achieved": st[dom]["GBps"],
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": st[dom]["hbm_frac"],
+                    "traffic": measured_traffic(dom, cfg.name), "algorithmic_bytes": st[dom]["algorithmic_bytes"],
+                    "ms": st[dom]["ms"], "source_sha256_16": source_sha(dom)}
     if args.copy_calibration:
         src = torch.empty(args.copy_calibration, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -426,9 +469,7 @@ def main():
                                f"KV {cfg.kv_len_dist} {list(cfg.kv_len)}, pool {cfg.pool}",
                    "batch": cfg.B, "tree_tokens": wl.total_nodes, "kv_tokens": int(np.sum(wl.lens)),
                    "accepted_tokens": int(np.sum(acc + 1))},
-        "roofline": {"bound": "hbm", "kernel": dom, "kernels": STAGE_KERNELS[dom], "achieved": st[dom]["GBps"],
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": st[dom]["hbm_frac"],
-                     "traffic": measured_traffic(dom, cfg.name), "source_sha256_16": source_sha(dom)},
+        "roofline": roofline,
         "accepted_tokens_per_s": round(float(np.sum(acc + 1)) / (ms * 1e-3), 1),
         "wall_ms_per_step": round(wall / args.steps * 1e3, 5),
         "ms_per_step_with_stage_events": round(float(per_stage.sum(axis=1).mean()), 5),

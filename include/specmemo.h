@@ -138,6 +138,15 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
                          float *logits_out, int32_t *topk_ids, float *topk_vals,
                          int32_t *node_tok, void *ws, size_t ws_bytes, void *stream);
 
+/* The head projection of (a) alone: logits_out[b][i][v] = sum_c
+ * head_w[i][v][c] * h[b][c] (fp32 accumulation), for callers that need the
+ * logits rather than the tree (and to time the projection kernel by itself).
+ * Same layouts, flags and requirements as specmemo_medusa_topk; logits_out:
+ * device fp32 [B][n_heads][vocab], 16-byte aligned; 1 <= B <=
+ * SPECMEMO_MAX_BATCH. */
+int specmemo_head_logits(specmemo_dtype dt, int32_t B, int32_t hidden, int32_t vocab, int32_t n_heads, const void *h,
+                         const void *head_w, int32_t head_layout, float *logits_out, void *stream);
+
 /* Medusa residual-block heads.  The paper gives only a size per head; this
  * reading gives each head one residual block before its vocabulary projection:
  *   out[i][b][c] = h[b][c] + SiLU(sum_k w1[i][c][k] h[b][k] + b1[i][c]),

@@ -414,6 +414,28 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
   return hip_status(launch_topk(a, ti.B, st), "top-k launch");
 }
 
+int specmemo_head_logits(specmemo_dtype dt, int32_t B, int32_t hidden, int32_t vocab, int32_t n_heads, const void *h,
+                         const void *head_w, int32_t head_layout, float *logits_out, void *stream) {
+  int rc;
+  if ((rc = check_dtype(dt))) return rc;
+  const bool per_head_input = head_layout & SPECMEMO_HEADS_INPUT_PER_HEAD;
+  head_layout &= ~SPECMEMO_HEADS_INPUT_PER_HEAD;
+  if (head_layout != SPECMEMO_HEADS_ROWMAJOR && head_layout != SPECMEMO_HEADS_PACKED)
+    return fail(SPECMEMO_E_ARG, "unknown head_layout %d", head_layout);
+  if (head_layout == SPECMEMO_HEADS_PACKED && dt != SPECMEMO_BF16)
+    return fail(SPECMEMO_E_DTYPE, "packed heads are bf16 only");
+  if (B < 1 || B > SPECMEMO_MAX_BATCH) return fail(SPECMEMO_E_ARG, "B=%d outside [1, %d]", B, SPECMEMO_MAX_BATCH);
+  if (n_heads < 1 || n_heads > SPECMEMO_MAX_DEPTH) return fail(SPECMEMO_E_ARG, "n_heads=%d outside [1, %d]", n_heads, SPECMEMO_MAX_DEPTH);
+  if (vocab < 1) return fail(SPECMEMO_E_ARG, "vocab=%d", vocab);
+  if (hidden < 8 || hidden % 8) return fail(SPECMEMO_E_ARG, "hidden=%d must be a positive multiple of 8", hidden);
+  if (!al(h, 16) || !al(head_w, 16) || !al(logits_out, 16))
+    return fail(SPECMEMO_E_ARG, "h / head_w / logits_out must be non-NULL and 16-byte aligned");
+  const int64_t h_head_stride = per_head_input ? (int64_t)B * hidden : 0;
+  return hip_status(launch_head_logits(dt, h, h_head_stride, head_w, head_layout == SPECMEMO_HEADS_PACKED, logits_out,
+                                       B, hidden, vocab, n_heads, static_cast<hipStream_t>(stream)),
+                    "head projection launch");
+}
+
 int specmemo_medusa_resblock(specmemo_dtype dt, int32_t B, int32_t hidden, int32_t n_heads, const void *h,
                              const void *w1, int32_t w1_layout, const void *b1, void *out, void *stream) {
   int rc;

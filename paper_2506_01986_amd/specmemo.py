@@ -88,6 +88,8 @@ def load():
             getattr(lib, f).restype = C.c_int
         i64 = C.c_int64
         u64 = C.c_uint64
+        lib.specmemo_head_logits.argtypes = [i32, i32, i32, i32, i32, vp, vp, i32, vp, vp]
+        lib.specmemo_head_logits.restype = C.c_int
         lib.specmemo_medusa_resblock.argtypes = [i32, i32, i32, i32, vp, vp, i32, vp, vp, vp]
         lib.specmemo_medusa_resblock.restype = C.c_int
         lib.specmemo_sample_next.argtypes = [i32, PT, i32, f32, u64, u64, vp, vp, vp, i32, vp, vp]
@@ -219,6 +221,12 @@ def medusa_topk(dt: int, trees: Trees, hidden: int, vocab: int, n_heads: int, to
                                        _ptr(head_w), head_layout, _ptr(root_tok), _ptr(logits_out),
                                        _ptr(topk_ids), _ptr(topk_vals), _ptr(node_tok), _ptr(ws), ws_bytes,
                                        _stream(stream)))
+
+
+def head_logits(dt: int, B: int, hidden: int, vocab: int, n_heads: int, h, head_w, logits_out,
+                head_layout: int = HEADS_ROWMAJOR, stream=None):
+    _check(load().specmemo_head_logits(dt, B, hidden, vocab, n_heads, _ptr(h), _ptr(head_w), head_layout,
+                                       _ptr(logits_out), _stream(stream)))
 
 
 def medusa_resblock(dt: int, B: int, hidden: int, n_heads: int, h, w1, b1, out, w1_layout: int = HEADS_PACKED,

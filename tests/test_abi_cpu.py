@@ -219,3 +219,28 @@ def test_padded_batching_errors():
         sm.tree_attn_padded(sm.BF16, t, roomy, None, 4, FAKE, FAKE, ws=FAKE, ws_bytes=1 << 30, stream=0)
     assert e.value.name == "E_ARG"
     assert sm.workspace_bytes(sm.WS_PAD, sm.BF16, t, None, 0) >= 4
+
+
+@cpu_only
+def test_projection_resblock_and_sampling_errors():
+    def logits(**k):
+        a = dict(dt=sm.BF16, B=2, hidden=64, vocab=100, n_heads=2, h=FAKE, head_w=FAKE, logits_out=FAKE,
+                 head_layout=sm.HEADS_PACKED)
+        a.update(k)
+        sm.head_logits(a["dt"], a["B"], a["hidden"], a["vocab"], a["n_heads"], a["h"], a["head_w"], a["logits_out"],
+                       head_layout=a["head_layout"], stream=0)
+    expect("E_HIP", logits)                                     # every host check passes
+    expect("E_DTYPE", logits, dt=sm.FP32)                       # packed heads are bf16 only
+    expect("E_ARG", logits, head_layout=4)
+    expect("E_ARG", logits, hidden=60)
+    expect("E_ARG", logits, B=0)
+    expect("E_ARG", logits, logits_out=None)
+    expect("E_HIP", logits, head_layout=sm.HEADS_PACKED | sm.HEADS_INPUT_PER_HEAD)
+    expect("E_ARG", sm.medusa_resblock, sm.BF16, 2, 64, 2, FAKE, FAKE, FAKE, FAKE, w1_layout=sm.HEADS_ROWMAJOR, stream=0)
+    expect("E_DTYPE", sm.medusa_resblock, sm.FP32, 2, 64, 2, FAKE, FAKE, FAKE, FAKE, w1_layout=sm.HEADS_PACKED,
+           stream=0)
+    t = FakeTrees([synth.t16()])
+    for temp in (0.0, -1.0, float("inf"), 1e-45):
+        expect("E_ARG", sm.sample_next, sm.BF16, t, 100, temp, 1, 0, FAKE, FAKE, FAKE, 4, FAKE, stream=0)
+    expect("E_ARG", sm.sample_next, sm.BF16, t, 100, 1.0, 1, 0, FAKE, FAKE, FAKE, 3, FAKE, stream=0)   # stride < depth + 1
+    expect("E_HIP", sm.sample_next, sm.BF16, t, 100, 1.0, 1, 0, FAKE, FAKE, FAKE, 4, FAKE, stream=0)
