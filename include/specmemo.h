@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SPECMEMO_ABI_VERSION 5
+#define SPECMEMO_ABI_VERSION 6
 #define SPECMEMO_MAX_TREE_NODES 128 /* nodes per sequence's tree */
 #define SPECMEMO_MAX_DEPTH 15       /* tree depth (= Medusa heads) */
 #define SPECMEMO_MAX_TOPK 32        /* top-k per head */
@@ -267,7 +267,8 @@ int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specme
  * key_valid: device uint32 flags over the pool's rows, bit (r % 32) of word
  * r / 32 for pool row r: 1 = a token, 0 = a pad token.  The array holds
  * specmemo_key_mask_words(cap_total) words (the kernels read up to three words
- * past the last row's).  Only committed rows (slab rows below L_b) are
+ * past the last row's); the calls take its length, key_valid_words, and
+ * reject a shorter array.  Only committed rows (slab rows below L_b) are
  * consulted; this step's tree rows are always tokens. */
 
 /* Words of a key_valid array for a pool of cap_total rows (0 if cap_total < 1). */
@@ -279,8 +280,8 @@ int64_t specmemo_key_mask_words(int64_t cap_total);
  * key_valid must be non-NULL and 16-byte aligned.  A row whose committed keys
  * are all pads still sees its tree path. */
 int specmemo_tree_attn_padded(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
-                              const uint32_t *key_valid, int32_t n_q, float scale, const void *q, void *out,
-                              void *ws, size_t ws_bytes, void *stream);
+                              const uint32_t *key_valid, int64_t key_valid_words, int32_t n_q, float scale,
+                              const void *q, void *out, void *ws, size_t ws_bytes, void *stream);
 
 /* (d') Padded KV update, in place of specmemo_kv_compact.  With
  * tau_b = accept_len[b] + 1 and the uniform length T = max_b tau_b over the
@@ -303,7 +304,8 @@ int specmemo_tree_attn_padded(specmemo_dtype dt, const specmemo_trees *t, const 
  * (the uniform length). */
 int specmemo_kv_pad_update(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
                            const int32_t *accept_len, const int32_t *path, int32_t path_stride,
-                           uint32_t *key_valid, int32_t *pos, void *ws, size_t ws_bytes, void *stream);
+                           uint32_t *key_valid, int64_t key_valid_words, int32_t *pos, void *ws, size_t ws_bytes,
+                           void *stream);
 
 /* ---- Memory budget and tree construction (host only) -------------------------
  *

@@ -540,9 +540,12 @@ int64_t specmemo_key_mask_words(int64_t cap_total) {
 }
 
 int specmemo_tree_attn_padded(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
-                              const uint32_t *key_valid, int32_t n_q, float scale, const void *q, void *out,
-                              void *ws, size_t ws_bytes, void *stream) {
+                              const uint32_t *key_valid, int64_t key_valid_words, int32_t n_q, float scale,
+                              const void *q, void *out, void *ws, size_t ws_bytes, void *stream) {
   if (!al(key_valid, 16)) return fail(SPECMEMO_E_ARG, "key_valid must be non-NULL and 16-byte aligned");
+  if (kv && key_valid_words < specmemo_key_mask_words(kv->cap_total))
+    return fail(SPECMEMO_E_ARG, "key_valid holds %lld words, %lld needed", static_cast<long long>(key_valid_words),
+                static_cast<long long>(specmemo_key_mask_words(kv->cap_total)));
   return tree_attn_impl(dt, t, kv, key_valid, n_q, scale, q, out, ws, ws_bytes, stream);
 }
 
@@ -691,7 +694,10 @@ int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specme
 
 int specmemo_kv_pad_update(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
                            const int32_t *accept_len, const int32_t *path, int32_t path_stride, uint32_t *key_valid,
-                           int32_t *pos, void *ws, size_t ws_bytes, void *stream) {
+                           int64_t key_valid_words, int32_t *pos, void *ws, size_t ws_bytes, void *stream) {
+  if (kv && key_valid_words < specmemo_key_mask_words(kv->cap_total))
+    return fail(SPECMEMO_E_ARG, "key_valid holds %lld words, %lld needed", static_cast<long long>(key_valid_words),
+                static_cast<long long>(specmemo_key_mask_words(kv->cap_total)));
   return compact_impl(dt, t, kv, accept_len, path, path_stride, true, key_valid, pos, ws, ws_bytes, stream);
 }
 

@@ -96,9 +96,9 @@ def load():
         lib.specmemo_sample_next.restype = C.c_int
         lib.specmemo_key_mask_words.argtypes = [i64]
         lib.specmemo_key_mask_words.restype = i64
-        lib.specmemo_tree_attn_padded.argtypes = [i32, PT, PK, vp, i32, f32, vp, vp, vp, sz, vp]
+        lib.specmemo_tree_attn_padded.argtypes = [i32, PT, PK, vp, i64, i32, f32, vp, vp, vp, sz, vp]
         lib.specmemo_tree_attn_padded.restype = C.c_int
-        lib.specmemo_kv_pad_update.argtypes = [i32, PT, PK, vp, vp, i32, vp, vp, vp, sz, vp]
+        lib.specmemo_kv_pad_update.argtypes = [i32, PT, PK, vp, vp, i32, vp, i64, vp, vp, sz, vp]
         lib.specmemo_kv_pad_update.restype = C.c_int
         lib.specmemo_mem_kv_bytes.argtypes = [i32, i32, i32, i32, i64, i32]
         lib.specmemo_mem_buffer_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
@@ -295,18 +295,26 @@ def unpack_key_valid(words, cap_total: int) -> np.ndarray:
     return np.unpackbits(w.view(np.uint8), bitorder="little")[:cap_total]
 
 
+def _words(key_valid, words):
+    if words is not None:
+        return words
+    return int(key_valid.numel()) if hasattr(key_valid, "numel") else len(key_valid)
+
+
 def tree_attn_padded(dt: int, trees: Trees, kv: KVPool, key_valid, n_q: int, q, out, scale: float = 0.0, ws=None,
-                     ws_bytes: int = 0, stream=None):
+                     ws_bytes: int = 0, stream=None, key_valid_words=None):
     ts, ks = trees.struct(), kv.struct()
-    _check(load().specmemo_tree_attn_padded(dt, C.byref(ts), C.byref(ks), _ptr(key_valid), n_q, scale, _ptr(q),
-                                            _ptr(out), _ptr(ws), ws_bytes, _stream(stream)))
+    _check(load().specmemo_tree_attn_padded(dt, C.byref(ts), C.byref(ks), _ptr(key_valid),
+                                            _words(key_valid, key_valid_words), n_q, scale, _ptr(q), _ptr(out),
+                                            _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def kv_pad_update(dt: int, trees: Trees, kv: KVPool, accept_len, path, path_stride: int, key_valid, pos, ws=None,
-                  ws_bytes: int = 0, stream=None):
+                  ws_bytes: int = 0, stream=None, key_valid_words=None):
     ts, ks = trees.struct(), kv.struct()
     _check(load().specmemo_kv_pad_update(dt, C.byref(ts), C.byref(ks), _ptr(accept_len), _ptr(path), path_stride,
-                                         _ptr(key_valid), _ptr(pos), _ptr(ws), ws_bytes, _stream(stream)))
+                                         _ptr(key_valid), _words(key_valid, key_valid_words), _ptr(pos), _ptr(ws),
+                                         ws_bytes, _stream(stream)))
 
 
 # ---- memory budget and tree construction (host) ------------------------------

@@ -31,7 +31,7 @@ def test_library_loads_and_exports_every_declared_function():
     assert {"specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert sm.abi_version() == 5
+    assert sm.abi_version() == 6
 
 
 class FakeTrees(sm.Trees):
@@ -202,8 +202,9 @@ def test_padded_batching_errors():
     assert sm.key_mask_words(1) == 4 and sm.key_mask_words(64) == 5 and sm.key_mask_words(65) == 6
     assert sm.key_mask_words(0) == 0
 
-    def pad(kv, ws_bytes=256, key_valid=FAKE, pos=FAKE):
-        sm.kv_pad_update(sm.BF16, t, kv, FAKE, FAKE, 5, key_valid, pos, ws=FAKE, ws_bytes=ws_bytes, stream=0)
+    def pad(kv, ws_bytes=256, key_valid=FAKE, pos=FAKE, words=None):
+        sm.kv_pad_update(sm.BF16, t, kv, FAKE, FAKE, 5, key_valid, pos, ws=FAKE, ws_bytes=ws_bytes, stream=0,
+                         key_valid_words=sm.key_mask_words(kv.cap_total) if words is None else words)
 
     roomy = FakeKV([10, 10], [80, 40], [0, 100])
     expect("E_HIP", pad, roomy)                           # every host check passes
@@ -215,9 +216,15 @@ def test_padded_batching_errors():
     expect("E_WORKSPACE", pad, roomy, ws_bytes=2)
     expect("E_ARG", pad, roomy, key_valid=None)
     expect("E_ARG", pad, roomy, pos=None)
+    expect("E_ARG", pad, roomy, words=sm.key_mask_words(roomy.cap_total) - 1)   # a flag array too short
     with pytest.raises(sm.SpecmemoError) as e:
-        sm.tree_attn_padded(sm.BF16, t, roomy, None, 4, FAKE, FAKE, ws=FAKE, ws_bytes=1 << 30, stream=0)
+        sm.tree_attn_padded(sm.BF16, t, roomy, None, 4, FAKE, FAKE, ws=FAKE, ws_bytes=1 << 30, stream=0,
+                            key_valid_words=1 << 20)
     assert e.value.name == "E_ARG"
+    with pytest.raises(sm.SpecmemoError) as e:
+        sm.tree_attn_padded(sm.BF16, t, roomy, FAKE, 4, FAKE, FAKE, ws=FAKE, ws_bytes=1 << 30, stream=0,
+                            key_valid_words=3)
+    assert e.value.name == "E_ARG" and "words" in str(e.value)
     assert sm.workspace_bytes(sm.WS_PAD, sm.BF16, t, None, 0) >= 4
 
 
