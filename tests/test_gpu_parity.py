@@ -237,6 +237,9 @@ EDGES = {
     # the widest top-k (32 per head) and a 32-child root
     "topk32": (edge_cfg(B=2, n_q=2, n_kv=1, hidden=64, vocab=100, n_heads=2, topk=(32, 32)),
                lambda r: [synth.random_tree(r, 128, max_depth=2, max_kids=32), synth.star_tree(33)], [10, 300]),
+    # multi-query attention: 64 query heads on one KV head, 8192 query rows per sequence
+    "mqa64": (edge_cfg(B=2, n_q=64, n_kv=1, hidden=64, vocab=300),
+              lambda r: [synth.random_tree(r, 128), synth.t16()], [300, 2000]),
     # the largest batch (4096 sequences: 128 launch groups per stage), the smallest hidden size
     "b4096": (edge_cfg(B=4096, n_q=1, n_kv=1, hidden=8, vocab=16, n_heads=1, topk=(4,)),
               lambda r: [synth.random_tree(r, int(r.integers(1, 6)), max_depth=1, max_kids=4) for _ in range(4096)],
