@@ -230,8 +230,9 @@ def decode_report(torch, cfg, wl, steps=48, warmup=3):
     slab has 64 + U[0, 160) free rows for the run, so some trees shrink), the
     next token chained as the next root, one host read-back per step.  The
     base model's per-step outputs (hidden states, queries, tree K/V rows,
-    logits) are Gaussian draws made on the device before timing; the host
-    planning, the planted walks and the read-back are inside the timed loop."""
+    logits) are Gaussian draws made on the device before timing, and so are
+    the planted walks on full-size trees; the host planning, the walks on
+    pruned trees and the read-back are inside the timed loop."""
     from paper_2506_01986_amd import runner, synth
     rng = np.random.default_rng(cfg.seed + 2000)
     room = (64 + rng.integers(0, 160, cfg.B)).astype(np.int32)
@@ -246,30 +247,37 @@ def decode_report(torch, cfg, wl, steps=48, warmup=3):
     pre = [dict(h=rnd(cfg.B, cfg.hidden), q=rnd(nmax, cfg.n_q, cfg.head_dim), k=rnd(cfg.n_kv, nmax, cfg.head_dim),
                 v=rnd(cfg.n_kv, nmax, cfg.head_dim), lg=rnd(nmax, cfg.vocab)) for _ in range(warmup + steps)]
     prng = np.random.default_rng(cfg.seed + 2001)
+    # the planted walks on full-size trees, drawn before timing like the
+    # other model outputs; a pruned tree's walk is drawn when it is needed
+    full = [synth.plant_walks([setup.default] * cfg.B, setup.p_accept, prng)[0] for _ in range(warmup + steps)]
 
-    def inputs_for(t):
-        seqs, sizes = loop.plan()
-        trees = [synth.tree_prefix(setup.default, n) for n in sizes]
-        plans, _ = synth.plant_walks(trees, setup.p_accept[seqs], prng)
+    def inputs_for(t, plan):
+        seqs, sizes = plan
+        plans = [full[t][b] if n == setup.default.n else
+                 synth.plant_walks([synth.tree_prefix(setup.default, n)], setup.p_accept[[b]], prng)[0][0]
+                 for b, n in zip(seqs, sizes)]
         n, x = int(sum(sizes)), pre[t]
         return synth.StepInputs(hidden=x["h"][:len(seqs)], q=x["q"][:n], tree_k=x["k"][:, :n], tree_v=x["v"][:, :n],
                                 base_logits=x["lg"][:n], plans=plans)
 
     for t in range(warmup):
-        loop.step(t, inputs_for(t), record=False)
+        plan = loop.plan()
+        loop.step(t, inputs_for(t, plan), record=False, plan=plan)
     torch.cuda.synchronize()
     loop.events.clear()
     acc_tokens = tree_tokens = done = 0
     w0 = time.perf_counter()
     for t in range(warmup, warmup + steps):
-        if not loop.plan()[0]:
+        plan = loop.plan()
+        if not plan[0]:
             break
-        rec = loop.step(t, inputs_for(t), record=False)
+        rec = loop.step(t, inputs_for(t, plan), record=False, plan=plan)
         acc_tokens += int(np.sum(rec["acc"] + 1))
         tree_tokens += int(sum(rec["sizes"]))
         done += 1
     wall = time.perf_counter() - w0
-    ph = {k: float(np.mean([e[k] for e in loop.events])) for k in loop.events[0]}
+    phases = loop.phase_ms()
+    ph = {k: float(np.mean([e[k] for e in phases])) for k in phases[0]}
     rb_bytes = cfg.n_heads * cfg.hidden * cfg.hidden * cfg.elem_bytes
     return {"steps": done, "ms_per_step": round(wall / done * 1e3, 4),
             "tree_tokens_per_step": round(tree_tokens / done, 1),

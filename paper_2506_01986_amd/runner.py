@@ -179,6 +179,8 @@ class DecodeLoop:
         self.default = (np.asarray(d.parent, np.int32), np.asarray(d.depth, np.int32), np.asarray(d.rank, np.int32))
         from .synth import PLANT_HI, PLANT_LO
         self._plant_hi, self._plant_lo = PLANT_HI, PLANT_LO   # the input generator's planted logits
+        self._tree_cache = {}
+        self._pin = [(None, None), (None, None)]
 
     def plan(self):
         """Active sequences and their tree sizes for the next step."""
@@ -186,41 +188,70 @@ class DecodeLoop:
         seqs = [b for b in range(self.cfg.B) if sizes[b] > 0]
         return seqs, [int(sizes[b]) for b in seqs]
 
-    def step(self, t: int, inputs=None, record: bool = True):
+    def _tree_arrays(self, sizes):
+        """The step's trees (prefixes of the default tree) as a library tree
+        batch with its device arrays, and the size of the projection's and
+        acceptance's workspace; kept per size tuple (most steps repeat one)."""
+        key = tuple(sizes)
+        hit = self._tree_cache.get(key)
+        if hit is None:
+            from . import synth
+            trees = [synth.tree_prefix(synth.Tree(*self.default), n) for n in sizes]
+            node_off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+            host = [node_off] + [np.concatenate([getattr(tr, f) for tr in trees]).astype(np.int32)
+                                 for f in ("parent", "depth", "rank")]
+            dev = torch.from_numpy(np.concatenate(host)).pin_memory().to(self.device, non_blocking=True)
+            tr = sm.Trees(*host, dev_arrays=list(dev.split([len(a) for a in host])))
+            ws = max(sm.workspace_bytes(sm.WS_TOPK, self.dt, tr, None, self.cfg.n_heads, self.cfg.vocab),
+                     sm.workspace_bytes(sm.WS_ACCEPT, self.dt, tr, None, sm.GREEDY))
+            hit = (trees, tr, ws)
+            if len(self._tree_cache) < 256:
+                self._tree_cache[key] = hit
+        return hit
+
+    def _upload(self, slot: int, parts):
+        """Concatenate int32 arrays into pinned host memory and copy them to
+        the device asynchronously (two independent slots); returns the device
+        buffer.  A slot's host memory is rewritten only after the previous
+        step's read-back, which waits for its copy."""
+        n = sum(len(a) for a in parts)
+        pin, dbuf = self._pin[slot]
+        if pin is None or pin.numel() < n:
+            cap = max(n, 2 * (0 if pin is None else pin.numel()))
+            pin = torch.empty(cap, dtype=torch.int32, pin_memory=True)
+            dbuf = torch.empty(cap, dtype=torch.int32, device=self.device)
+            self._pin[slot] = (pin, dbuf)
+        np.concatenate(parts, out=pin.numpy()[:n])
+        dbuf[:n].copy_(pin[:n], non_blocking=True)
+        return dbuf
+
+    def phase_ms(self):
+        """Per-step stage times (ms) from the events of the steps run with
+        timing on."""
+        out = []
+        for ev in self.events:
+            names = list(ev)
+            out.append({b: ev[a].elapsed_time(ev[b]) for a, b in zip(names, names[1:])})
+        return out
+
+    def step(self, t: int, inputs=None, record: bool = True, plan=None):
         """One step; returns its record (host copies when `record`), or None when
-        every slab is full.  The step's integer arrays go to the device in one
-        copy, and the accepted lengths and next tokens come back in one."""
+        every slab is full.  The launches come in the order that keeps the
+        device busy: the residual blocks (they need only the hidden states),
+        the projection and top-k (after a small upload of the roots and
+        lengths), then the model outputs' writes and the rest.  The accepted
+        lengths and next tokens come back in one read-back.  `plan`, when
+        given, is what plan() returns for the current lengths."""
         from . import synth
         cfg, st, dev = self.cfg, self.setup, self.device
-        seqs, sizes = self.plan()
+        seqs, sizes = self.plan() if plan is None else plan
         if not seqs:
             return None
-        trees = [synth.tree_prefix(synth.Tree(*self.default), n) for n in sizes]
-        inp = inputs if inputs is not None else synth.decode_step_inputs(st, t, seqs, trees)
+        if inputs is None:
+            inputs = synth.decode_step_inputs(st, t, seqs, self._tree_arrays(sizes)[0])
+        inp = inputs
         B = len(seqs)
-        node_off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
-        sumN = int(node_off[-1])
-        parent = np.concatenate([tr.parent for tr in trees]).astype(np.int32)
-        depth = np.concatenate([tr.depth for tr in trees]).astype(np.int32)
-        rank = np.concatenate([tr.rank for tr in trees]).astype(np.int32)
-        base, L, caps = st.seq_base[seqs], self.lens[seqs].copy(), st.seq_cap[seqs]
-        rows = np.concatenate([int(base[i]) + int(L[i]) + np.arange(sizes[i]) for i in range(B)]).astype(np.int32)
-        plant = np.array([(int(node_off[i]) + u, int(node_off[i]) + c, 1 if val > 0 else 0)
-                          for i, plan in enumerate(inp.plans) for u, c, val in plan], np.int32).reshape(-1, 3)
-        # one upload: [node_off | parent | depth | rank | root | L | rows | planted (row, child, hi)]
-        parts = [node_off, parent, depth, rank, self.root[seqs].astype(np.int32), L.astype(np.int32), rows,
-                 plant.T.reshape(-1)]
-        offs = np.concatenate([[0], np.cumsum([len(a) for a in parts])])
-        buf = torch.from_numpy(np.concatenate(parts)).to(dev)
-        view = [buf[int(offs[i]):int(offs[i + 1])] for i in range(len(parts))]
-        tr = sm.Trees(node_off, parent, depth, rank, dev_arrays=view[:4])
-        root, seq_len, rows_d = view[4], view[5], view[6]
-        plant_d = view[7].view(3, -1) if plant.size else None
-        # the tree's K/V rows (the base model's) into the slabs
-        ri = rows_d.to(torch.int64)
-        self.k[:, ri] = to_device(inp.tree_k, cfg.dtype, dev)
-        self.v[:, ri] = to_device(inp.tree_v, cfg.dtype, dev)
-        kv = sm.KVPool(self.k, self.v, seq_len, base, caps, L)
+        s = torch.cuda.current_stream().cuda_stream
         i32 = dict(dtype=torch.int32, device=dev)
         ev = {}
 
@@ -230,53 +261,74 @@ class DecodeLoop:
                 e.record()
                 ev[name] = e
 
-        # heads
         h = to_device(inp.hidden, cfg.dtype, dev)
         mark("start")
         layout = self.head_layout
         if self.w1 is not None:
             hh = torch.empty((cfg.n_heads, B, cfg.hidden), dtype=h.dtype, device=dev)
             sm.medusa_resblock(self.dt, B, cfg.hidden, cfg.n_heads, h, self.w1, self.b1, hh,
-                               w1_layout=self.w1_layout)
+                               w1_layout=self.w1_layout, stream=s)
             h, layout = hh, layout | sm.HEADS_INPUT_PER_HEAD
         mark("resblock")
+        trees, tr, ws_fixed = self._tree_arrays(sizes)
+        node_off = tr.node_off_h
+        sumN = int(node_off[-1])
+        base, L, caps = st.seq_base[seqs], self.lens[seqs].copy(), st.seq_cap[seqs]
+        small = self._upload(0, [self.root[seqs].astype(np.int32), L.astype(np.int32)])
+        root, seq_len = small[:B], small[B:2 * B]
+        kv = sm.KVPool(self.k, self.v, seq_len, base, caps, L)
+        mark("upload")
         logits = torch.empty((B, cfg.n_heads, cfg.vocab), dtype=torch.float32, device=dev) if self.keep_logits else None
-        ws_bytes = max(sm.workspace_bytes(sm.WS_TOPK, self.dt, tr, None, cfg.n_heads, cfg.vocab),
-                       sm.workspace_bytes(sm.WS_ATTN, self.dt, tr, kv, cfg.n_q),
-                       sm.workspace_bytes(sm.WS_ACCEPT, self.dt, tr, None, sm.GREEDY), 16)
+        ws_bytes = max(ws_fixed, sm.workspace_bytes(sm.WS_ATTN, self.dt, tr, kv, cfg.n_q), 16)
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
         ids = torch.empty((B, cfg.n_heads, cfg.kmax), **i32)
         tok = torch.empty(sumN, **i32)
         sm.medusa_topk(self.dt, tr, cfg.hidden, cfg.vocab, cfg.n_heads, cfg.topk, h, self.head_w, root, ids, tok,
-                       logits_out=logits, ws=ws, ws_bytes=ws_bytes, head_layout=layout)
+                       logits_out=logits, ws=ws, ws_bytes=ws_bytes, head_layout=layout, stream=s)
         mark("medusa_topk")
-        # the base model's logits, with the planted walk at the chosen tokens
+        # The base model's outputs, written while the projection runs: the
+        # tree's K/V rows at slab rows seq_base + L + local index, the logits
+        # with the planted walk at the tokens the heads chose.
+        rows = (np.repeat(base.astype(np.int64) + L - node_off[:-1], sizes) + np.arange(sumN)).astype(np.int32)
+        cnt = [len(p) for p in inp.plans]
+        plant = np.array([(u, c, 1 if val > 0 else 0) for p in inp.plans for (u, c, val) in p],
+                         np.int32).reshape(-1, 3)
+        if plant.size:
+            shift = np.repeat(node_off[:-1], cnt)
+            plant[:, 0] += shift
+            plant[:, 1] += shift
+        big = self._upload(1, [rows, np.ascontiguousarray(plant.T).reshape(-1)])
+        ri = big[:sumN].to(torch.int64)
+        self.k.index_copy_(1, ri, to_device(inp.tree_k, cfg.dtype, dev))
+        self.v.index_copy_(1, ri, to_device(inp.tree_v, cfg.dtype, dev))
         lg = to_device(inp.base_logits, cfg.dtype, dev)
         if plant.size:
+            plant_d = big[sumN:sumN + plant.size].view(3, -1)
             cols = tok[plant_d[1].to(torch.int64)].to(torch.int64)
             vals = torch.where(plant_d[2] > 0, float(self._plant_hi), float(self._plant_lo)).to(lg.dtype)
             lg[plant_d[0].to(torch.int64), cols] = vals
         # attention, acceptance, next token, compaction
         q = to_device(inp.q, cfg.dtype, dev)
         out = torch.empty_like(q)
-        mark("plant")
-        sm.tree_attn(self.dt, tr, kv, cfg.n_q, q, out, ws=ws, ws_bytes=ws_bytes)
+        mark("model")
+        sm.tree_attn(self.dt, tr, kv, cfg.n_q, q, out, ws=ws, ws_bytes=ws_bytes, stream=s)
         mark("tree_attn")
         res = torch.empty((2, B), **i32)            # accepted lengths, next tokens: read back together
         acc, nxt = res[0], res[1]
         path = torch.empty((B, self.stride), **i32)
-        sm.accept(self.dt, tr, cfg.vocab, sm.GREEDY, lg, tok, acc, path, self.stride, nxt, ws=ws, ws_bytes=ws_bytes)
+        sm.accept(self.dt, tr, cfg.vocab, sm.GREEDY, lg, tok, acc, path, self.stride, nxt, ws=ws, ws_bytes=ws_bytes,
+                  stream=s)
         mark("accept")
         if st.temperature is not None:
-            sm.sample_next(self.dt, tr, cfg.vocab, st.temperature, st.sample_seed, t, lg, acc, path, self.stride, nxt)
+            sm.sample_next(self.dt, tr, cfg.vocab, st.temperature, st.sample_seed, t, lg, acc, path, self.stride, nxt,
+                           stream=s)
         mark("sample_next")
-        sm.kv_compact(self.dt, tr, kv, acc, path, self.stride)
+        sm.kv_compact(self.dt, tr, kv, acc, path, self.stride, stream=s)
         mark("kv_compact")
         res_h = res.cpu().numpy()
         acc_h, nxt_h = res_h[0].copy(), res_h[1].copy()
         if self.timing:
-            names = list(ev)
-            self.events.append({b: ev[a].elapsed_time(ev[b]) for a, b in zip(names, names[1:])})
+            self.events.append(ev)
         self.lens[seqs] = L + acc_h + 1
         self.root[seqs] = nxt_h
         rec = dict(step=t, seqs=seqs, sizes=sizes, acc=acc_h, next_tok=nxt_h, lens=self.lens.copy())
