@@ -107,7 +107,7 @@ int check_kv(int dt, const specmemo_kv *kv, const TreeInfo &ti, const int32_t *n
     const int64_t base = kv->seq_base_h[b], cap = kv->seq_cap_h[b], L = kv->seq_len_h[b];
     const int N = node_off_h[b + 1] - node_off_h[b];
     if (L < 0 || cap < 0 || base < 0) return fail(SPECMEMO_E_ARG, "sequence %d: negative base/cap/len", b);
-    if (base + cap > kv->cap_total)
+    if (base > kv->cap_total - cap)   // base + cap > cap_total, without overflow for any base
       return fail(SPECMEMO_E_BUDGET, "sequence %d: slab [%lld, %lld) outside the pool of %lld rows", b, (long long)base,
                   (long long)(base + cap), (long long)kv->cap_total);
     if (L + N > cap)

@@ -136,6 +136,8 @@ def test_budget_errors():
     expect("E_BUDGET", attn, t, FakeKV([10, 10], [25, 26], [0, 30]))            # 10 + 16 > 25
     expect("E_BUDGET", attn, t, FakeKV([10, 10], [26, 26], [0, 20]))            # slabs overlap
     expect("E_BUDGET", attn, t, FakeKV([10, 10], [26, 26], [0, 30], cap_total=50))
+    # a slab base near the int64 limit: base + cap would overflow
+    expect("E_BUDGET", attn, t, FakeKV([10, 10], [26, 26], [0, 2 ** 63 - 10], cap_total=100))
     with pytest.raises(sm.SpecmemoError) as e:
         sm.kv_compact(sm.BF16, t, FakeKV([10, 10], [25, 26], [0, 30]), FAKE, FAKE, 5, stream=0)
     assert e.value.name == "E_BUDGET"
