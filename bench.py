@@ -224,6 +224,35 @@ def padded_report(torch, cfg, wl, step, steps, history=150):
                                  "GBps": round(attn_bytes / (ta * 1e-3) / 1e9, 1)}}
 
 
+def measured_peaks(torch, reps=10):
+    """What this device reaches outside the library, to set the spec peaks in
+    context: a 2 GiB device-to-device copy (bytes read + written per second)
+    and an 8192^3 bf16 matrix product through torch (the vendor library).
+    Neither replaces the spec peaks of the roofline entry."""
+    n = 1 << 31
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    a = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+    t_copy = timed(lambda: dst.copy_(src))
+    t_mm = timed(lambda: torch.matmul(a, b))
+    del src, dst, a, b
+    return {"copy_GBps": round(2 * n / t_copy / 1e9, 1), "copy_bytes": 2 * n,
+            "gemm_bf16_TFLOPs": round(2 * 8192 ** 3 / t_mm / 1e12, 1), "gemm_shape": [8192, 8192, 8192]}
+
+
 def decode_report(torch, cfg, wl, steps=48, warmup=3):
     """Multi-step decoding on the same batch: residual-block heads, the
     sampled next token, trees sized each step from the slabs' free rows (each
@@ -484,6 +513,12 @@ def main():
         "graph": {"ms_per_step": round(graph_ms, 5), "value": round(wl.total_nodes / (graph_ms * 1e-3), 1)},
         "stages": st,
     }
+    print("[bench] measured peaks (copy, library GEMM)", file=sys.stderr, flush=True)
+    mp = measured_peaks(torch)
+    mp["dominant_kernel_frac_of_copy"] = round(roofline["achieved"] / mp["copy_GBps"], 4)
+    if cfg.dtype == "bf16":
+        mp["attention_frac_of_gemm"] = round(st["tree_attn"]["TFLOPs"] / mp["gemm_bf16_TFLOPs"], 4)
+    result["measured_peaks"] = mp
     if not args.no_padded:
         print("[bench] padded batching variant", file=sys.stderr, flush=True)
         pr = padded_report(torch, cfg, wl, step, args.steps)
