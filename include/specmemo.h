@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SPECMEMO_ABI_VERSION 6
+#define SPECMEMO_ABI_VERSION 7
 #define SPECMEMO_MAX_TREE_NODES 128 /* nodes per sequence's tree */
 #define SPECMEMO_MAX_DEPTH 15       /* tree depth (= Medusa heads) */
 #define SPECMEMO_MAX_TOPK 32        /* top-k per head */
@@ -254,6 +254,20 @@ int specmemo_sample_next(specmemo_dtype dt, const specmemo_trees *t, int32_t voc
 int specmemo_kv_compact(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
                         const int32_t *accept_len, const int32_t *path, int32_t path_stride,
                         void *stream);
+
+/* (c) + (d) fused: specmemo_accept followed by specmemo_kv_compact, with the
+ * compaction done by the acceptance's second pass (one launch fewer; the
+ * cited passages are those of the two calls).  Arguments, outputs,
+ * workspace (SPECMEMO_WS_ACCEPT) and checks are those of the two calls
+ * together; a rejected call changes nothing.  Every sequence is compacted
+ * along the path this call picks, and kv->seq_len[b] becomes
+ * L_b + accept_len[b] + 1.  The results equal those of the two calls in
+ * sequence, bit for bit. */
+int specmemo_accept_compact(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
+                            int32_t vocab, specmemo_accept_mode mode, float temperature, float eps,
+                            float delta, const void *base_logits, const int32_t *node_tok,
+                            int32_t *accept_len, int32_t *path, int32_t path_stride,
+                            int32_t *next_tok, void *ws, size_t ws_bytes, void *stream);
 
 /* ---- Padded batching (Sec. 3.3, Fig. 8) --------------------------------------
  *

@@ -10,6 +10,7 @@
 // has no dependent row loads, only one token per node crosses to it.  Typical
 // mode needs every node's softmax statistics: one block per row computes
 // them, then one block per sequence evaluates the edges and picks the path.
+#include "compact_rows.h"
 #include "device.h"
 #include "internal.h"
 
@@ -193,13 +194,15 @@ __global__ __launch_bounds__(kNT) void row_argbest_all(AcceptArgs a) {
   if (threadIdx.x == 0) a.best[blockIdx.x] = tok;
 }
 
-// Greedy mode, pass 2: one wave per sequence walks from the root to the child
-// carrying the current node's arg-best token (unique: sibling tokens differ),
-// with the tree's parents, tokens and arg-best tokens in LDS (at most
-// kMaxNodes = 128 nodes, two per lane).
-__global__ __launch_bounds__(64) void accept_walk(AcceptArgs a) {
+// Greedy mode, pass 2: one wave walks sequence b's tree from the root to the
+// child carrying the current node's arg-best token (unique: sibling tokens
+// differ), with the tree's parents, tokens and arg-best tokens in LDS (at
+// most kMaxNodes = 128 nodes, two per lane).  Returns the accepted length;
+// lane j holds path entry j in p_mine (lanes past the end hold -1), and
+// next_tok is the last accepted node's arg-best token.
+__device__ __forceinline__ int greedy_walk(const AcceptArgs &a, int b, int &p_mine, int &next_tok) {
   __shared__ int s_par[kMaxNodes], s_tok[kMaxNodes], s_best[kMaxNodes];
-  const int b = blockIdx.x, lane = threadIdx.x;
+  const int lane = threadIdx.x;
   const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
   for (int n = lane; n < N; n += 64) {
     s_par[n] = n == 0 ? -1 : a.parent[n0 + n];
@@ -207,7 +210,8 @@ __global__ __launch_bounds__(64) void accept_walk(AcceptArgs a) {
     s_best[n] = a.best[n0 + n];
   }
   __syncthreads();
-  int cur = 0, len = 0, p_mine = lane == 0 ? 0 : -1;   // lane j keeps path entry j
+  int cur = 0, len = 0;
+  p_mine = lane == 0 ? 0 : -1;   // lane j keeps path entry j
   for (;;) {
     const int tok = s_best[cur];
     const bool m0 = lane < N && s_par[lane] == cur && s_tok[lane] == tok;
@@ -219,11 +223,45 @@ __global__ __launch_bounds__(64) void accept_walk(AcceptArgs a) {
     ++len;
     if (lane == len) p_mine = cur;
   }
+  next_tok = s_best[cur];
+  return len;
+}
+
+__device__ __forceinline__ void write_acceptance(const AcceptArgs &a, int b, int len, int p_mine, int next_tok) {
+  const int lane = threadIdx.x;
   if (lane == 0) {
     a.accept_len[b] = len;
-    a.next_tok[b] = s_best[cur];
+    a.next_tok[b] = next_tok;
   }
   for (int j = lane; j < a.path_stride; j += 64) a.path[(int64_t)b * a.path_stride + j] = j < 64 ? p_mine : -1;
+}
+
+// One wave per sequence.
+__global__ __launch_bounds__(64) void accept_walk(AcceptArgs a) {
+  const int b = blockIdx.x;
+  int p_mine, next_tok;
+  const int len = greedy_walk(a, b, p_mine, next_tok);
+  write_acceptance(a, b, len, p_mine, next_tok);
+}
+
+// Acceptance and compaction in one pass: one wave per (sequence, KV head,
+// K|V) of a launch group walks the sequence's tree and moves that slab's
+// accepted rows; the wave of (KV head 0, K) also writes the acceptance
+// outputs and the new length.  The walk is repeated per wave (a few LDS
+// rounds over at most 128 nodes) so that no wave waits for another.
+__global__ __launch_bounds__(64) void accept_walk_compact(AcceptArgs a, CompactArgs c) {
+  const int s = blockIdx.x, kvh = blockIdx.y, which = blockIdx.z;
+  const int b = c.b0 + s;
+  int p_mine, next_tok;
+  const int len = greedy_walk(a, b, p_mine, next_tok);
+  const bool writer = kvh == 0 && which == 0;
+  if (writer) write_acceptance(a, b, len, p_mine, next_tok);
+  int src[kMaxPath];
+#pragma unroll
+  for (int j = 0; j < kMaxPath; ++j) src[j] = __builtin_amdgcn_readlane(p_mine, j);
+  const CompactSeq S = c.seq[s];
+  move_rows(c, S, kvh, which, len, src, threadIdx.x, 64);
+  if (writer && threadIdx.x == 0) c.seq_len[b] = S.L + len + 1;
 }
 
 // Typical mode, pass 1: per row u, x = z_u / T: lse_u = log sum exp x and
@@ -274,9 +312,12 @@ __global__ __launch_bounds__(256) void row_softmax_stats(AcceptArgs a) {
   }
 }
 
-// Typical mode, pass 2: one block per sequence.
+// Typical mode, pass 2, by one block: the edges of sequence b's tree, the
+// cumulative acceptance and the path pick; writes accept_len, path and
+// next_tok and returns the accepted length, with the path in s_path for the
+// whole block.
 template <int DT>
-__global__ __launch_bounds__(kNT) void accept_typical(AcceptArgs a) {
+__device__ __forceinline__ int typical_pick(const AcceptArgs &a, int b, int *s_path) {
   __shared__ float sv[kWaves];
   __shared__ int si[kWaves];
   __shared__ float lp[kMaxNodes];
@@ -285,7 +326,7 @@ __global__ __launch_bounds__(kNT) void accept_typical(AcceptArgs a) {
   __shared__ int ok[kMaxNodes];
   __shared__ int par[kMaxNodes], dep[kMaxNodes];
   __shared__ int s_best;
-  const int b = blockIdx.x, tid = threadIdx.x;
+  const int tid = threadIdx.x;
   const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
   for (int c = tid; c < N; c += kNT) {
     const int u = a.parent[n0 + c];
@@ -322,14 +363,43 @@ __global__ __launch_bounds__(kNT) void accept_typical(AcceptArgs a) {
   float v;
   int tok;
   row_argbest<DT>(a.logits, n0 + best, a.vocab, sv, si, v, tok);
+  const int len = dep[best];
   if (tid == 0) {
-    const int len = dep[best];
     a.accept_len[b] = len;
     a.next_tok[b] = tok;
     int32_t *p = a.path + (int64_t)b * a.path_stride;
     for (int j = 0; j < a.path_stride; ++j) p[j] = -1;
-    for (int u = best, j = len; u >= 0 && j >= 0; u = par[u], --j) p[j] = u;
+    for (int u = best, j = len; u >= 0 && j >= 0; u = par[u], --j) {
+      p[j] = u;
+      s_path[j] = u;
+    }
   }
+  __syncthreads();
+  return len;
+}
+
+// One block per sequence.
+template <int DT>
+__global__ __launch_bounds__(kNT) void accept_typical(AcceptArgs a) {
+  __shared__ int s_path[kMaxPath];
+  typical_pick<DT>(a, blockIdx.x, s_path);
+}
+
+// Acceptance and compaction in one pass: one block per sequence of a launch
+// group picks the path, then its waves move the accepted rows of the 2 n_kv
+// (KV head, K|V) slabs.
+template <int DT>
+__global__ __launch_bounds__(kNT) void accept_typical_compact(AcceptArgs a, CompactArgs c) {
+  __shared__ int s_path[kMaxPath];
+  const int s = blockIdx.x, b = c.b0 + s;
+  const int len = typical_pick<DT>(a, b, s_path);
+  int src[kMaxPath];
+#pragma unroll
+  for (int j = 0; j < kMaxPath; ++j) src[j] = j <= len ? s_path[j] : -1;
+  const CompactSeq S = c.seq[s];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int p = wave; p < 2 * c.n_kv; p += kWaves) move_rows(c, S, p >> 1, p & 1, len, src, lane, 64);
+  if (threadIdx.x == 0) c.seq_len[b] = S.L + len + 1;
 }
 
 // ---- sampled next token ---------------------------------------------------------
@@ -418,22 +488,39 @@ hipError_t launch_sample_next(int dt, const SampleArgs &a, int B, hipStream_t st
   return hipGetLastError();
 }
 
-hipError_t launch_accept(int dt, const AcceptArgs &a, int total_nodes, hipStream_t st) {
+hipError_t launch_accept_rows(int dt, const AcceptArgs &a, int total_nodes, hipStream_t st) {
   if (a.mode == 0) {
     if (dt == 1)
       hipLaunchKernelGGL(row_argbest_all<1>, dim3(total_nodes), dim3(kNT), 0, st, a);
     else
       hipLaunchKernelGGL(row_argbest_all<0>, dim3(total_nodes), dim3(kNT), 0, st, a);
-    hipLaunchKernelGGL(accept_walk, dim3(a.B), dim3(64), 0, st, a);
+  } else if (dt == 1) {
+    hipLaunchKernelGGL(row_softmax_stats<1>, dim3(total_nodes), dim3(256), 0, st, a);
   } else {
-    if (dt == 1) {
-      hipLaunchKernelGGL(row_softmax_stats<1>, dim3(total_nodes), dim3(256), 0, st, a);
-      hipLaunchKernelGGL(accept_typical<1>, dim3(a.B), dim3(kNT), 0, st, a);
-    } else {
-      hipLaunchKernelGGL(row_softmax_stats<0>, dim3(total_nodes), dim3(256), 0, st, a);
-      hipLaunchKernelGGL(accept_typical<0>, dim3(a.B), dim3(kNT), 0, st, a);
-    }
+    hipLaunchKernelGGL(row_softmax_stats<0>, dim3(total_nodes), dim3(256), 0, st, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_accept(int dt, const AcceptArgs &a, int total_nodes, hipStream_t st) {
+  hipError_t e = launch_accept_rows(dt, a, total_nodes, st);
+  if (e != hipSuccess) return e;
+  if (a.mode == 0)
+    hipLaunchKernelGGL(accept_walk, dim3(a.B), dim3(64), 0, st, a);
+  else if (dt == 1)
+    hipLaunchKernelGGL(accept_typical<1>, dim3(a.B), dim3(kNT), 0, st, a);
+  else
+    hipLaunchKernelGGL(accept_typical<0>, dim3(a.B), dim3(kNT), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_accept_compact(int dt, const AcceptArgs &a, const CompactArgs &c, hipStream_t st) {
+  if (a.mode == 0)
+    hipLaunchKernelGGL(accept_walk_compact, dim3(c.nseq, c.n_kv, 2), dim3(64), 0, st, a, c);
+  else if (dt == 1)
+    hipLaunchKernelGGL(accept_typical_compact<1>, dim3(c.nseq), dim3(kNT), 0, st, a, c);
+  else
+    hipLaunchKernelGGL(accept_typical_compact<0>, dim3(c.nseq), dim3(kNT), 0, st, a, c);
   return hipGetLastError();
 }
 

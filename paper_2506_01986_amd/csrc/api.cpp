@@ -291,6 +291,53 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
   }
 }
 
+// Validation and kernel arguments of the acceptance (nothing is launched).
+int accept_args(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, specmemo_accept_mode mode, float temperature,
+                float eps, float delta, const void *base_logits, const int32_t *node_tok, int32_t *accept_len,
+                int32_t *path, int32_t path_stride, int32_t *next_tok, void *ws, size_t ws_bytes, TreeInfo *ti,
+                AcceptArgs *out) {
+  int rc;
+  if ((rc = check_dtype(dt))) return rc;
+  if ((rc = check_trees(t, ti))) return rc;
+  if (vocab < 1) return fail(SPECMEMO_E_ARG, "vocab=%d", vocab);
+  if (mode != SPECMEMO_ACCEPT_GREEDY && mode != SPECMEMO_ACCEPT_TYPICAL) return fail(SPECMEMO_E_ARG, "unknown mode %d", mode);
+  if (path_stride < ti->max_depth + 1) return fail(SPECMEMO_E_ARG, "path_stride=%d < max depth + 1 = %d", path_stride, ti->max_depth + 1);
+  if (!al(base_logits, 16)) return fail(SPECMEMO_E_ARG, "base_logits must be non-NULL and 16-byte aligned");
+  if (!al(node_tok, 4) || !al(accept_len, 4) || !al(path, 4) || !al(next_tok, 4))
+    return fail(SPECMEMO_E_ARG, "node_tok / accept_len / path / next_tok must be non-NULL and 4-byte aligned");
+  AcceptArgs &a = *out;
+  a = AcceptArgs{};
+  a.logits = base_logits;
+  a.node_tok = node_tok;
+  a.node_off = t->node_off;
+  a.parent = t->parent;
+  a.depth = t->depth;
+  a.vocab = vocab;
+  a.mode = mode;
+  a.path_stride = path_stride;
+  a.B = ti->B;
+  a.accept_len = accept_len;
+  a.path = path;
+  a.next_tok = next_tok;
+  if (mode == SPECMEMO_ACCEPT_TYPICAL) {
+    if (!(temperature > 0.f) || !(eps > 0.f) || !(delta > 0.f) || !std::isfinite(temperature))
+      return fail(SPECMEMO_E_ARG, "typical mode needs temperature, eps, delta > 0");
+    const size_t need = (size_t)ti->total * 2 * sizeof(float);
+    if (!al(ws, 16) || ws_bytes < need)
+      return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
+    a.stats = static_cast<float *>(ws);
+    a.inv_temp = 1.0f / temperature;
+    a.log_eps = std::log(eps);
+    a.log_delta = std::log(delta);
+  } else {
+    const size_t need = (size_t)ti->total * sizeof(int32_t);
+    if (!al(ws, 16) || ws_bytes < need)
+      return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
+    a.best = static_cast<int32_t *>(ws);
+  }
+  return SPECMEMO_OK;
+}
+
 // Top-k workspace: fp32 logits (unless the caller keeps them) then the slice candidates.
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t topk_logit_bytes(int B, int n_heads, int vocab) { return align256((size_t)B * n_heads * vocab * sizeof(float)); }
@@ -553,45 +600,11 @@ int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, s
                     float temperature, float eps, float delta, const void *base_logits, const int32_t *node_tok,
                     int32_t *accept_len, int32_t *path, int32_t path_stride, int32_t *next_tok, void *ws,
                     size_t ws_bytes, void *stream) {
-  int rc;
-  if ((rc = check_dtype(dt))) return rc;
   TreeInfo ti;
-  if ((rc = check_trees(t, &ti))) return rc;
-  if (vocab < 1) return fail(SPECMEMO_E_ARG, "vocab=%d", vocab);
-  if (mode != SPECMEMO_ACCEPT_GREEDY && mode != SPECMEMO_ACCEPT_TYPICAL) return fail(SPECMEMO_E_ARG, "unknown mode %d", mode);
-  if (path_stride < ti.max_depth + 1) return fail(SPECMEMO_E_ARG, "path_stride=%d < max depth + 1 = %d", path_stride, ti.max_depth + 1);
-  if (!al(base_logits, 16)) return fail(SPECMEMO_E_ARG, "base_logits must be non-NULL and 16-byte aligned");
-  if (!al(node_tok, 4) || !al(accept_len, 4) || !al(path, 4) || !al(next_tok, 4))
-    return fail(SPECMEMO_E_ARG, "node_tok / accept_len / path / next_tok must be non-NULL and 4-byte aligned");
-  AcceptArgs a{};
-  a.logits = base_logits;
-  a.node_tok = node_tok;
-  a.node_off = t->node_off;
-  a.parent = t->parent;
-  a.depth = t->depth;
-  a.vocab = vocab;
-  a.mode = mode;
-  a.path_stride = path_stride;
-  a.B = ti.B;
-  a.accept_len = accept_len;
-  a.path = path;
-  a.next_tok = next_tok;
-  if (mode == SPECMEMO_ACCEPT_TYPICAL) {
-    if (!(temperature > 0.f) || !(eps > 0.f) || !(delta > 0.f) || !std::isfinite(temperature))
-      return fail(SPECMEMO_E_ARG, "typical mode needs temperature, eps, delta > 0");
-    const size_t need = (size_t)ti.total * 2 * sizeof(float);
-    if (!al(ws, 16) || ws_bytes < need)
-      return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
-    a.stats = static_cast<float *>(ws);
-    a.inv_temp = 1.0f / temperature;
-    a.log_eps = std::log(eps);
-    a.log_delta = std::log(delta);
-  } else {
-    const size_t need = (size_t)ti.total * sizeof(int32_t);
-    if (!al(ws, 16) || ws_bytes < need)
-      return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
-    a.best = static_cast<int32_t *>(ws);
-  }
+  AcceptArgs a;
+  const int rc = accept_args(dt, t, vocab, mode, temperature, eps, delta, base_logits, node_tok, accept_len, path,
+                             path_stride, next_tok, ws, ws_bytes, &ti, &a);
+  if (rc) return rc;
   return hip_status(launch_accept(dt, a, ti.total, static_cast<hipStream_t>(stream)), "acceptance launch");
 }
 
@@ -629,30 +642,19 @@ namespace {
 
 // Compaction (padded = false) or the padded update (Sec. 3.3): the same
 // checks and row moves, launched per group of sequences.
-int compact_impl(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, const int32_t *accept_len,
-                 const int32_t *path, int32_t path_stride, bool padded, uint32_t *key_valid, int32_t *pos, void *ws,
-                 size_t ws_bytes, void *stream) {
+// Validation of the compaction's arguments and its launch-independent kernel
+// arguments (nothing is launched).
+int compact_args(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, const int32_t *accept_len,
+                 const int32_t *path, int32_t path_stride, const TreeInfo &ti, CompactArgs *out) {
   int rc;
-  if ((rc = check_dtype(dt))) return rc;
-  TreeInfo ti;
-  if ((rc = check_trees(t, &ti))) return rc;
   if ((rc = check_kv(dt, kv, ti, t->node_off_h))) return rc;
   if (!al(kv->seq_len, 4)) return fail(SPECMEMO_E_ARG, "kv->seq_len must be non-NULL and 4-byte aligned");
   if (!al(accept_len, 4) || !al(path, 4)) return fail(SPECMEMO_E_ARG, "accept_len / path must be non-NULL and 4-byte aligned");
   if (path_stride < 1) return fail(SPECMEMO_E_ARG, "path_stride=%d", path_stride);
   const int elem = dt == SPECMEMO_BF16 ? 2 : 4;
   if ((kv->head_dim * elem) % 4) return fail(SPECMEMO_E_ARG, "row bytes must be a multiple of 4");
-  if (padded) {
-    if (!al(key_valid, 4) || !al(pos, 4)) return fail(SPECMEMO_E_ARG, "key_valid / pos must be non-NULL and 4-byte aligned");
-    if (!al(ws, 4) || ws_bytes < 4)
-      return fail(SPECMEMO_E_WORKSPACE, "workspace of 4 bytes needed (4-byte aligned), got %zu", ws ? ws_bytes : 0);
-    // every sequence may grow by the batch's longest acceptance: the deepest tree + 1
-    for (int b = 0; b < ti.B; ++b)
-      if ((int64_t)kv->seq_len_h[b] + ti.max_depth + 1 > kv->seq_cap_h[b])
-        return fail(SPECMEMO_E_BUDGET, "seq_len[%d]=%d + uniform length up to %d exceeds seq_cap=%d", b,
-                    kv->seq_len_h[b], ti.max_depth + 1, kv->seq_cap_h[b]);
-  }
-  CompactArgs a{};
+  CompactArgs &a = *out;
+  a = CompactArgs{};
   a.k = kv->k;
   a.v = kv->v;
   a.cap_total = kv->cap_total;
@@ -663,6 +665,39 @@ int compact_impl(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *
   a.path = path;
   a.parent = t->parent;
   a.seq_len = kv->seq_len;
+  return SPECMEMO_OK;
+}
+
+// The per-sequence table of one launch group: sequences b0 .. b0 + nseq - 1.
+void compact_group(const specmemo_trees *t, const specmemo_kv *kv, int b0, int B, CompactArgs *a) {
+  a->nseq = std::min(kMaxSeqPerLaunch, B - b0);
+  a->b0 = b0;
+  for (int i = 0; i < a->nseq; ++i) {
+    const int b = b0 + i;
+    a->seq[i] = CompactSeq{kv->seq_base_h[b], kv->seq_len_h[b], t->node_off_h[b + 1] - t->node_off_h[b],
+                           kv->seq_cap_h[b], t->node_off_h[b]};
+  }
+}
+
+int compact_impl(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, const int32_t *accept_len,
+                 const int32_t *path, int32_t path_stride, bool padded, uint32_t *key_valid, int32_t *pos, void *ws,
+                 size_t ws_bytes, void *stream) {
+  int rc;
+  if ((rc = check_dtype(dt))) return rc;
+  TreeInfo ti;
+  if ((rc = check_trees(t, &ti))) return rc;
+  CompactArgs a;
+  if ((rc = compact_args(dt, t, kv, accept_len, path, path_stride, ti, &a))) return rc;
+  if (padded) {
+    if (!al(key_valid, 4) || !al(pos, 4)) return fail(SPECMEMO_E_ARG, "key_valid / pos must be non-NULL and 4-byte aligned");
+    if (!al(ws, 4) || ws_bytes < 4)
+      return fail(SPECMEMO_E_WORKSPACE, "workspace of 4 bytes needed (4-byte aligned), got %zu", ws ? ws_bytes : 0);
+    // every sequence may grow by the batch's longest acceptance: the deepest tree + 1
+    for (int b = 0; b < ti.B; ++b)
+      if ((int64_t)kv->seq_len_h[b] + ti.max_depth + 1 > kv->seq_cap_h[b])
+        return fail(SPECMEMO_E_BUDGET, "seq_len[%d]=%d + uniform length up to %d exceeds seq_cap=%d", b,
+                    kv->seq_len_h[b], ti.max_depth + 1, kv->seq_cap_h[b]);
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   int32_t *uniform = static_cast<int32_t *>(ws);
   if (padded) {
@@ -670,13 +705,7 @@ int compact_impl(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *
     if (e != hipSuccess) return hip_status(e, "pad length launch");
   }
   for (int b0 = 0; b0 < ti.B; b0 += kMaxSeqPerLaunch) {
-    a.nseq = std::min(kMaxSeqPerLaunch, ti.B - b0);
-    a.b0 = b0;
-    for (int i = 0; i < a.nseq; ++i) {
-      const int b = b0 + i;
-      a.seq[i] = CompactSeq{kv->seq_base_h[b], kv->seq_len_h[b], t->node_off_h[b + 1] - t->node_off_h[b],
-                            kv->seq_cap_h[b], t->node_off_h[b]};
-    }
+    compact_group(t, kv, b0, ti.B, &a);
     hipError_t e = padded ? launch_kv_pad_update(a, uniform, key_valid, pos, st) : launch_kv_compact(a, st);
     if (e != hipSuccess) return hip_status(e, padded ? "padded update launch" : "compaction launch");
   }
@@ -699,6 +728,27 @@ int specmemo_kv_pad_update(specmemo_dtype dt, const specmemo_trees *t, const spe
     return fail(SPECMEMO_E_ARG, "key_valid holds %lld words, %lld needed", static_cast<long long>(key_valid_words),
                 static_cast<long long>(specmemo_key_mask_words(kv->cap_total)));
   return compact_impl(dt, t, kv, accept_len, path, path_stride, true, key_valid, pos, ws, ws_bytes, stream);
+}
+
+int specmemo_accept_compact(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, int32_t vocab,
+                            specmemo_accept_mode mode, float temperature, float eps, float delta,
+                            const void *base_logits, const int32_t *node_tok, int32_t *accept_len, int32_t *path,
+                            int32_t path_stride, int32_t *next_tok, void *ws, size_t ws_bytes, void *stream) {
+  TreeInfo ti;
+  AcceptArgs a;
+  CompactArgs c;
+  int rc = accept_args(dt, t, vocab, mode, temperature, eps, delta, base_logits, node_tok, accept_len, path,
+                       path_stride, next_tok, ws, ws_bytes, &ti, &a);
+  if (rc) return rc;
+  if ((rc = compact_args(dt, t, kv, accept_len, path, path_stride, ti, &c))) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_accept_rows(dt, a, ti.total, st);
+  if (e != hipSuccess) return hip_status(e, "acceptance launch");
+  for (int b0 = 0; b0 < ti.B; b0 += kMaxSeqPerLaunch) {
+    compact_group(t, kv, b0, ti.B, &c);
+    if ((e = launch_accept_compact(dt, a, c, st)) != hipSuccess) return hip_status(e, "acceptance and compaction launch");
+  }
+  return ok();
 }
 
 }  // extern "C"

@@ -123,6 +123,10 @@ struct CompactArgs {
   CompactSeq seq[kMaxSeqPerLaunch];
 };
 hipError_t launch_kv_compact(const CompactArgs &a, hipStream_t st);
+// Acceptance with the compaction fused into its second pass (one launch group
+// of sequences; the row pass of launch_accept_rows must precede it).
+hipError_t launch_accept_rows(int dt, const AcceptArgs &a, int total_nodes, hipStream_t st);
+hipError_t launch_accept_compact(int dt, const AcceptArgs &a, const CompactArgs &c, hipStream_t st);
 // Padded batching: the batch's uniform acceptance length into *uniform (one
 // block), then the row moves and the per-sequence bookkeeping.
 hipError_t launch_pad_length(const int32_t *node_off, const int32_t *parent, const int32_t *accept_len,

@@ -7,11 +7,8 @@
 // sequence length grows by accept_len + 1; the rest of the tree rows become
 // free scratch for the next step.
 //
-// One wave per (sequence, KV head, K|V).  Each lane owns a fixed set of 4-byte
-// columns of a row and reads that column of every source row into registers
-// before writing any destination, so overlapping sources and destinations
-// (path = 0, 2, 7, ...: destination 2 is also the source of destination 1)
-// need no barrier: no two lanes touch the same bytes.
+// One wave per (sequence, KV head, K|V) moves the rows (compact_rows.h).
+#include "compact_rows.h"
 #include "device.h"
 #include "internal.h"
 
@@ -47,22 +44,6 @@ __device__ __forceinline__ bool is_root_path(const int32_t *parent, int node0, i
   return ok;
 }
 
-// Rows L + src[j] -> L + j, j = 0..acc, of one KV head's K or V slab.
-__device__ __forceinline__ void move_rows(const CompactArgs &a, const CompactSeq &S, int kvh, int which, int acc,
-                                          const int (&src)[kMaxPath]) {
-  uint32_t *slab = static_cast<uint32_t *>(which ? a.v : a.k) +
-                   ((int64_t)kvh * a.cap_total + S.base) * a.row_dwords;
-  for (int c = threadIdx.x; c < a.row_dwords; c += 64) {
-    uint32_t tmp[kMaxPath];
-#pragma unroll
-    for (int j = 0; j < kMaxPath; ++j)
-      if (j <= acc) tmp[j] = slab[(int64_t)(S.L + src[j]) * a.row_dwords + c];
-#pragma unroll
-    for (int j = 0; j < kMaxPath; ++j)
-      if (j <= acc) slab[(int64_t)(S.L + j) * a.row_dwords + c] = tmp[j];
-  }
-}
-
 __global__ __launch_bounds__(64) void kv_compact_kernel(CompactArgs a) {
   const int s = blockIdx.x, kvh = blockIdx.y, which = blockIdx.z;
   const CompactSeq S = a.seq[s];
@@ -71,7 +52,7 @@ __global__ __launch_bounds__(64) void kv_compact_kernel(CompactArgs a) {
   const int acc = load_path(a.accept_len, a.path, a.path_stride, b, S.N, src);
   // an invalid path, or one that does not fit the slab, leaves the sequence untouched
   if (acc < 0 || S.L + acc + 1 > S.cap) return;
-  move_rows(a, S, kvh, which, acc, src);
+  move_rows(a, S, kvh, which, acc, src, threadIdx.x, 64);
   if (kvh == 0 && which == 0 && threadIdx.x == 0) a.seq_len[b] = S.L + acc + 1;
 }
 
@@ -110,7 +91,7 @@ __global__ __launch_bounds__(64) void kv_pad_update_kernel(CompactArgs a, const 
   int src[kMaxPath];
   const int acc = load_path(a.accept_len, a.path, a.path_stride, b, S.N, src);
   if (acc < 0 || !is_root_path(a.parent, S.node0, acc, src)) return;
-  move_rows(a, S, kvh, which, acc, src);
+  move_rows(a, S, kvh, which, acc, src, threadIdx.x, 64);
   if (kvh != 0 || which != 0) return;
   const int T = *uniform, tau = acc + 1;
   const int64_t r0 = S.base + S.L;

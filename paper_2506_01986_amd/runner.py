@@ -110,6 +110,19 @@ class VerifyStep:
     def kv_compact(self, stream=None):
         sm.kv_compact(self.dt, self.trees, self.kv, self.accept_len, self.path, self.path_stride, stream=stream)
 
+    def accept_compact(self, stream=None):
+        """Acceptance and compaction in one call (the fused entry point)."""
+        sm.accept_compact(self.dt, self.trees, self.kv, self.cfg.vocab, self.mode, self.base_logits, self.node_tok,
+                          self.accept_len, self.path, self.path_stride, self.next_tok, temperature=self.temperature,
+                          eps=self.eps, delta=self.delta, ws=self.ws, ws_bytes=self.ws_bytes, stream=stream)
+
+    def reset_pool(self):
+        """Restore the workload's pool and committed lengths on the device."""
+        c = self.cfg
+        self.k.copy_(to_device(self.wl.pool_k, c.dtype, self.device))
+        self.v.copy_(to_device(self.wl.pool_v, c.dtype, self.device))
+        self.seq_len.copy_(torch.from_numpy(self.wl.lens.copy()))
+
     def tree_attn_padded(self, stream=None):
         sm.tree_attn_padded(self.dt, self.trees, self.kv, self.key_valid, self.cfg.n_q, self.q, self.out, ws=self.ws,
                             ws_bytes=self.ws_bytes, stream=stream)
@@ -123,6 +136,12 @@ class VerifyStep:
         self.tree_attn(stream)
         self.accept(stream)
         self.kv_compact(stream)
+
+    def run_fused(self, stream=None):
+        """The step with acceptance and compaction fused into one call."""
+        self.medusa_topk(stream)
+        self.tree_attn(stream)
+        self.accept_compact(stream)
 
     def run_padded(self, stream=None):
         """The step of the padded-batching variant: pad tokens masked in
@@ -141,8 +160,8 @@ class DecodeLoop:
     full slab ends its sequence), the step's model outputs uploaded (the tree's
     K/V rows written at slab rows L_b ..), residual-block heads and the
     projection with top-k, the planted base-model logits (written on the device
-    at the tokens the heads chose), tree attention, greedy acceptance, the
-    next token (greedy or sampled), compaction.  The host reads back the
+    at the tokens the heads chose), tree attention, greedy acceptance with the
+    compaction (one call), the next token (greedy or sampled).  The host reads back the
     accepted lengths and next tokens once per step: they size the next step.
     """
 
@@ -239,7 +258,8 @@ class DecodeLoop:
         every slab is full.  The launches come in the order that keeps the
         device busy: the residual blocks (they need only the hidden states),
         the projection and top-k (after a small upload of the roots and
-        lengths), then the model outputs' writes and the rest.  The accepted
+        lengths), then the model outputs' writes, attention, acceptance with
+        compaction (one call) and the sampled next token.  The accepted
         lengths and next tokens come back in one read-back.  `plan`, when
         given, is what plan() returns for the current lengths."""
         from . import synth
@@ -316,15 +336,15 @@ class DecodeLoop:
         res = torch.empty((2, B), **i32)            # accepted lengths, next tokens: read back together
         acc, nxt = res[0], res[1]
         path = torch.empty((B, self.stride), **i32)
-        sm.accept(self.dt, tr, cfg.vocab, sm.GREEDY, lg, tok, acc, path, self.stride, nxt, ws=ws, ws_bytes=ws_bytes,
-                  stream=s)
-        mark("accept")
+        # acceptance with the compaction fused in; the sampled next token reads
+        # only the logits and the accepted path, so it may follow the compaction
+        sm.accept_compact(self.dt, tr, kv, cfg.vocab, sm.GREEDY, lg, tok, acc, path, self.stride, nxt, ws=ws,
+                          ws_bytes=ws_bytes, stream=s)
+        mark("accept_compact")
         if st.temperature is not None:
             sm.sample_next(self.dt, tr, cfg.vocab, st.temperature, st.sample_seed, t, lg, acc, path, self.stride, nxt,
                            stream=s)
         mark("sample_next")
-        sm.kv_compact(self.dt, tr, kv, acc, path, self.stride, stream=s)
-        mark("kv_compact")
         res_h = res.cpu().numpy()
         acc_h, nxt_h = res_h[0].copy(), res_h[1].copy()
         if self.timing:

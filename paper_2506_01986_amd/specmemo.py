@@ -80,11 +80,13 @@ def load():
         lib.specmemo_tree_attn.argtypes = [i32, PT, PK, i32, f32, vp, vp, vp, sz, vp]
         lib.specmemo_accept.argtypes = [i32, PT, i32, i32, f32, f32, f32, vp, vp, vp, vp, i32, vp, vp, sz, vp]
         lib.specmemo_kv_compact.argtypes = [i32, PT, PK, vp, vp, i32, vp]
+        lib.specmemo_accept_compact.argtypes = [i32, PT, PK, i32, i32, f32, f32, f32, vp, vp, vp, vp, i32, vp, vp, sz, vp]
         lib.specmemo_workspace_bytes.argtypes = [i32, i32, PT, PK, i32, i32]
         lib.specmemo_workspace_bytes.restype = C.c_size_t
         lib.specmemo_last_error.restype = C.c_char_p
         lib.specmemo_abi_version.restype = C.c_int32
-        for f in ("specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"):
+        for f in ("specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact",
+                  "specmemo_accept_compact"):
             getattr(lib, f).restype = C.c_int
         i64 = C.c_int64
         u64 = C.c_uint64
@@ -264,6 +266,15 @@ def accept(dt: int, trees: Trees, vocab: int, mode: int, base_logits, node_tok, 
     _check(load().specmemo_accept(dt, C.byref(ts), vocab, mode, temperature, eps, delta, _ptr(base_logits),
                                   _ptr(node_tok), _ptr(accept_len), _ptr(path), path_stride, _ptr(next_tok),
                                   _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def accept_compact(dt: int, trees: Trees, kv: KVPool, vocab: int, mode: int, base_logits, node_tok, accept_len, path,
+                   path_stride: int, next_tok, temperature: float = 1.0, eps: float = 0.09, delta: float = 0.3,
+                   ws=None, ws_bytes: int = 0, stream=None):
+    ts, ks = trees.struct(), kv.struct()
+    _check(load().specmemo_accept_compact(dt, C.byref(ts), C.byref(ks), vocab, mode, temperature, eps, delta,
+                                          _ptr(base_logits), _ptr(node_tok), _ptr(accept_len), _ptr(path),
+                                          path_stride, _ptr(next_tok), _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def kv_compact(dt: int, trees: Trees, kv: KVPool, accept_len, path, path_stride: int, stream=None):

@@ -31,7 +31,7 @@ def test_library_loads_and_exports_every_declared_function():
     assert {"specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert sm.abi_version() == 6
+    assert sm.abi_version() == 7
 
 
 class FakeTrees(sm.Trees):
@@ -253,3 +253,24 @@ def test_projection_resblock_and_sampling_errors():
         expect("E_ARG", sm.sample_next, sm.BF16, t, 100, temp, 1, 0, FAKE, FAKE, FAKE, 4, FAKE, stream=0)
     expect("E_ARG", sm.sample_next, sm.BF16, t, 100, 1.0, 1, 0, FAKE, FAKE, FAKE, 3, FAKE, stream=0)   # stride < depth + 1
     expect("E_HIP", sm.sample_next, sm.BF16, t, 100, 1.0, 1, 0, FAKE, FAKE, FAKE, 4, FAKE, stream=0)
+
+
+@cpu_only
+def test_fused_acceptance_and_compaction_errors():
+    # the fused call takes the checks of both calls: acceptance first, then the pool
+    t = FakeTrees([synth.t16(), synth.t16()])
+
+    def fused(kv, mode=sm.GREEDY, stride=4, ws_bytes=1 << 20, **kw):
+        sm.accept_compact(sm.BF16, t, kv, 1000, mode, FAKE, FAKE, FAKE, FAKE, stride, FAKE, ws=FAKE,
+                          ws_bytes=ws_bytes, stream=0, **kw)
+    ok_kv = FakeKV([10, 10], [26, 26], [0, 30])
+    assert "path_stride" in expect("E_ARG", fused, ok_kv, stride=2)
+    expect("E_WORKSPACE", fused, ok_kv, ws_bytes=4 * 31)                  # one int32 per node: 32 needed
+    expect("E_WORKSPACE", fused, ok_kv, mode=sm.TYPICAL, ws_bytes=4 * 32)  # typical: two floats per node
+    expect("E_ARG", fused, ok_kv, mode=sm.TYPICAL, temperature=-1.0)
+    expect("E_BUDGET", fused, FakeKV([10, 10], [25, 26], [0, 30]))       # 10 + 16 > 25
+    expect("E_BUDGET", fused, FakeKV([10, 10], [26, 26], [0, 20]))       # slabs overlap
+    bad = FakeKV([10, 10], [26, 26], [0, 30])
+    bad.seq_len = FAKE + 2                                                # misaligned device seq_len
+    expect("E_ARG", fused, bad)
+    expect("E_DTYPE", fused, FakeKV([10, 10], [26, 26], [0, 30], d=64))   # bf16 needs d = 128

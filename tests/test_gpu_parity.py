@@ -189,6 +189,28 @@ def run_parity(torch, wl, max_attn_rows=None, typical=True, label="", pack_heads
     assert np.array_equal(Vg.view(np.uint8), V0.view(np.uint8))
     assert np.array_equal(step.seq_len.cpu().numpy(), new_len)
     say(f"[parity]   stage d ok: accepted {acc.tolist()[:10]}")
+
+    # (c) + (d) fused into one call, from the original pool, both modes
+    for mode, name in modes:
+        say(f"[parity]   stages c+d fused, {name}")
+        step.reset_pool()
+        step.mode = mode
+        step.accept_compact()
+        torch.cuda.synchronize()
+        if mode == sm.GREEDY:
+            ra, rp, rn = oracle.accept_greedy(lg, tok64, wl.node_off, wl.parent, wl.depth, stride)
+        else:
+            ra, rp, rn = oracle.accept_typical(lg, tok64, wl.node_off, wl.parent, wl.depth, stride,
+                                               step.temperature, step.eps, step.delta)
+        assert np.array_equal(step.accept_len.cpu().numpy(), ra)
+        assert np.array_equal(step.path.cpu().numpy(), rp)
+        assert np.array_equal(step.next_tok.cpu().numpy(), rn)
+        K0, V0 = wl.pool_k.copy(), wl.pool_v.copy()
+        new_len = oracle.kv_compact(K0, V0, wl.seq_base, wl.lens, ra, rp)
+        assert np.array_equal(runner.to_host_storage(step.k, cfg.dtype).view(np.uint8), K0.view(np.uint8))
+        assert np.array_equal(runner.to_host_storage(step.v, cfg.dtype).view(np.uint8), V0.view(np.uint8))
+        assert np.array_equal(step.seq_len.cpu().numpy(), new_len)
+    step.mode = sm.GREEDY
     return step
 
 
@@ -453,12 +475,14 @@ def test_greedy_argbest_rows(torch_cuda, vocab):
         assert np.array_equal(acc.cpu().numpy(), ra) and np.array_equal(path.cpu().numpy(), rp)
 
 
-def test_graph_replay(torch_cuda):
-    """The four calls of a step captured in one HIP graph.  Every replay, with
-    eager work between replays (the pool restored, every output poisoned),
-    reproduces the eager step bit for bit: no call records a memset, an
-    allocation or a host synchronisation, and the kernels read nothing that
-    capture freezes except their arguments."""
+@pytest.mark.parametrize("fused", [False, True], ids=["four_calls", "accept_compact"])
+def test_graph_replay(torch_cuda, fused):
+    """The calls of a step (four, or three with acceptance and compaction
+    fused) captured in one HIP graph.  Every replay, with eager work between
+    replays (the pool restored, every output poisoned), reproduces the eager
+    step bit for bit: no call records a memset, an allocation or a host
+    synchronisation, and the kernels read nothing that capture freezes except
+    their arguments."""
     import torch
     from paper_2506_01986_amd import runner
     rng = np.random.default_rng(21)
@@ -481,13 +505,14 @@ def test_graph_replay(torch_cuda):
             t.fill_(-7)
         step.out.zero_()
 
+    run = step.run_fused if fused else step.run
     restore_and_poison()
-    step.run()
+    run()
     torch.cuda.synchronize()
     ref = [t.clone() for t in outs]
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        step.run()
+        run()
     torch.cuda.synchronize()
     for r in range(3):
         say(f"graph replay {r}")
