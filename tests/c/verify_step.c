@@ -3,7 +3,10 @@
  * compaction) on device memory that this program allocates itself through the
  * HIP runtime's C API, on a stream of its own.
  *
- * Usage: verify_step DIR
+ * Usage: verify_step DIR [fused]
+ *
+ * With "fused", acceptance and compaction run as one call
+ * (specmemo_accept_compact) instead of specmemo_accept + specmemo_kv_compact.
  *
  * DIR holds meta.txt ("dt B hidden vocab n_heads n_q n_kv head_dim cap_total
  * path_stride" then the n_heads top-k sizes) and one raw little-endian file
@@ -84,8 +87,9 @@ static void fetch(const char *name, const void *dev, size_t bytes) {
 }
 
 int main(int argc, char **argv) {
-  if (argc != 2) die("usage", "verify_step DIR", 2);
+  if (argc < 2 || argc > 3 || (argc == 3 && strcmp(argv[2], "fused") != 0)) die("usage", "verify_step DIR [fused]", 2);
   g_dir = argv[1];
+  const int fused = argc == 3;
   if (specmemo_abi_version() != SPECMEMO_ABI_VERSION) die("library", "ABI version differs from the header's", 2);
 
   int dt_i, B, hidden, vocab, n_heads, n_q, n_kv, head_dim, path_stride;
@@ -165,9 +169,14 @@ int main(int argc, char **argv) {
   SPECMEMO_CHECK(specmemo_medusa_topk(dt, &t, hidden, vocab, n_heads, topk, h_d, w_d, SPECMEMO_HEADS_ROWMAJOR, root_d,
                                       z_d, ids_d, NULL, tok_d, ws, ws_bytes, stream));
   SPECMEMO_CHECK(specmemo_tree_attn(dt, &t, &kv, n_q, 0.0f, q_d, out_d, ws, ws_bytes, stream));
-  SPECMEMO_CHECK(specmemo_accept(dt, &t, vocab, SPECMEMO_ACCEPT_GREEDY, 1.0f, 0.09f, 0.3f, lg_d, tok_d, acc_d, path_d,
-                                 path_stride, nxt_d, ws, ws_bytes, stream));
-  SPECMEMO_CHECK(specmemo_kv_compact(dt, &t, &kv, acc_d, path_d, path_stride, stream));
+  if (fused) {
+    SPECMEMO_CHECK(specmemo_accept_compact(dt, &t, &kv, vocab, SPECMEMO_ACCEPT_GREEDY, 1.0f, 0.09f, 0.3f, lg_d, tok_d,
+                                           acc_d, path_d, path_stride, nxt_d, ws, ws_bytes, stream));
+  } else {
+    SPECMEMO_CHECK(specmemo_accept(dt, &t, vocab, SPECMEMO_ACCEPT_GREEDY, 1.0f, 0.09f, 0.3f, lg_d, tok_d, acc_d,
+                                   path_d, path_stride, nxt_d, ws, ws_bytes, stream));
+    SPECMEMO_CHECK(specmemo_kv_compact(dt, &t, &kv, acc_d, path_d, path_stride, stream));
+  }
   HIP_CHECK(hipStreamSynchronize(stream));
   HIP_CHECK(hipStreamDestroy(stream));
 
@@ -187,6 +196,6 @@ int main(int argc, char **argv) {
   for (size_t i = 0; i < sizeof dev / sizeof dev[0]; ++i) HIP_CHECK(hipFree(dev[i]));
   void *host[] = {node_off, parent, depth, rank, seq_base, seq_len, seq_cap, k_h, v_h, h, w, q, lg, root};
   for (size_t i = 0; i < sizeof host / sizeof host[0]; ++i) free(host[i]);
-  printf("verify_step: ok (B=%d, %zu nodes)\n", B, N);
+  printf("verify_step: ok (B=%d, %zu nodes%s)\n", B, N, fused ? ", fused acceptance and compaction" : "");
   return 0;
 }

@@ -1,7 +1,8 @@
 """The C ABI from C: the header compiles as strict C99 and as C++, and a plain
 C program (tests/c/verify_step.c) that allocates device memory with the HIP
-runtime's C API runs one verify step through the library; its outputs match
-the oracle's to the same bar as the Python-driven parity tests."""
+runtime's C API runs one verify step through the library (the four stage
+calls, or three with acceptance and compaction fused); its outputs match the
+oracle's to the same bar as the Python-driven parity tests."""
 
 import os
 import subprocess
@@ -59,8 +60,9 @@ def _workload(dtype):
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("fused", [False, True], ids=["four_calls", "accept_compact"])
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_c_program_verify_step_matches_the_oracle(tmp_path, dtype):
+def test_c_program_verify_step_matches_the_oracle(tmp_path, dtype, fused):
     sm.load()
     exe = build_consumer(tmp_path)
     wl = _workload(dtype)
@@ -79,8 +81,8 @@ def test_c_program_verify_step_matches_the_oracle(tmp_path, dtype):
                       ("k", wl.pool_k), ("v", wl.pool_v), ("h", wl.hidden), ("head_w", wl.head_w), ("q", wl.q),
                       ("base_logits", lg), ("root_tok", wl.root_tok)):
         (d / f"{name}.bin").write_bytes(np.ascontiguousarray(arr).tobytes())
-    print(f"[c_abi] {dtype}: B={cfg.B} sumN={wl.total_nodes} L={wl.lens.tolist()}", flush=True)
-    r = subprocess.run([exe, str(d)], capture_output=True, text=True, timeout=120)
+    print(f"[c_abi] {dtype} fused={fused}: B={cfg.B} sumN={wl.total_nodes} L={wl.lens.tolist()}", flush=True)
+    r = subprocess.run([exe, str(d)] + (["fused"] if fused else []), capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
     store = np.float32 if dtype == "fp32" else np.uint16
 
