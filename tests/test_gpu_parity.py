@@ -539,3 +539,22 @@ def test_run_to_run_determinism(torch_cuda):
     for a, b in zip(*outs):
         assert torch.equal(a.view(torch.uint8) if a.dtype != torch.int32 else a,
                            b.view(torch.uint8) if b.dtype != torch.int32 else b)
+
+
+@pytest.mark.parametrize("env", [{"SPECMEMO_ATTN_ROWS": "64"}, {"SPECMEMO_ATTN_ROWS": "256"},
+                                 {"SPECMEMO_ATTN_XCD": "0"}, {"SPECMEMO_ATTN_CHUNK": "256"},
+                                 {"SPECMEMO_ATTN_CHUNK": "0"}],
+                         ids=["rows64", "rows256", "no_xcd_order", "chunk256", "no_split"])
+def test_attention_tuning_overrides(torch_cuda, env):
+    """The attention's tuning variables (read once per process) change the
+    work split, not the result: each runs in a child process of its own,
+    one after the other, against the oracle."""
+    import os
+    import subprocess
+    import sys
+    child = os.path.join(os.path.dirname(os.path.abspath(__file__)), "attn_override_check.py")
+    say(f"[override] {env}")
+    r = subprocess.run([sys.executable, child], env={**os.environ, **env}, capture_output=True, text=True,
+                       timeout=240)
+    say(r.stdout.strip())
+    assert r.returncode == 0, r.stdout + r.stderr[-3000:]
