@@ -11,8 +11,9 @@ budget holds).  Per step, for the sequences whose slab still has room:
      written at slab rows L_b ..;
   3. residual-block heads (when given), projection, top-k, tree tokens, with
      the previous step's next token as the root;
-  4. the planted base-model logits, tree attention, greedy acceptance, and the
-     next token, greedy or sampled (Gumbel-max with Philox);
+  4. the planted base-model logits, tree attention, greedy or typical
+     acceptance (App. A.1), and the next token, the acceptance's or sampled
+     (Gumbel-max with Philox);
   5. compaction; L_b grows by the accepted tokens, the next token becomes the
      next root.
 
@@ -74,7 +75,11 @@ def run(setup: synth.DecodeSetup, steps: int, attn_rows=None):
         lg = synth.plant_logits(inp.base_logits, node_off, inp.plans, tok, cfg.dtype)
         sel = attn_rows(t, int(node_off[-1]), cfg.n_q) if attn_rows else None
         out = oracle.tree_attn(inp.q, K, V, node_off, parent, L, base, cfg.n_kv, sel=sel)
-        acc, path, nxt = oracle.accept_greedy(lg, tok, node_off, parent, depth, stride)
+        if setup.typical is not None:
+            T, eps, delta = setup.typical
+            acc, path, nxt = oracle.accept_typical(lg, tok, node_off, parent, depth, stride, T, eps, delta)
+        else:
+            acc, path, nxt = oracle.accept_greedy(lg, tok, node_off, parent, depth, stride)
         best = second = None
         if setup.temperature is not None:
             nxt, best, second = oracle.sample_next(lg, node_off, acc, path, setup.temperature,

@@ -160,8 +160,9 @@ class DecodeLoop:
     full slab ends its sequence), the step's model outputs uploaded (the tree's
     K/V rows written at slab rows L_b ..), residual-block heads and the
     projection with top-k, the planted base-model logits (written on the device
-    at the tokens the heads chose), tree attention, greedy acceptance with the
-    compaction (one call), the next token (greedy or sampled).  The host reads back the
+    at the tokens the heads chose), tree attention, greedy or typical
+    acceptance with the compaction (one call), the next token (the
+    acceptance's or sampled).  The host reads back the
     accepted lengths and next tokens once per step: they size the next step.
     """
 
@@ -199,6 +200,8 @@ class DecodeLoop:
         from .synth import PLANT_HI, PLANT_LO
         self._plant_hi, self._plant_lo = PLANT_HI, PLANT_LO   # the input generator's planted logits
         self._tree_cache = {}
+        self.mode = sm.GREEDY if setup.typical is None else sm.TYPICAL
+        self.typical = {} if setup.typical is None else dict(zip(("temperature", "eps", "delta"), setup.typical))
         self._pin = [(None, None), (None, None)]
 
     def plan(self):
@@ -222,7 +225,7 @@ class DecodeLoop:
             dev = torch.from_numpy(np.concatenate(host)).pin_memory().to(self.device, non_blocking=True)
             tr = sm.Trees(*host, dev_arrays=list(dev.split([len(a) for a in host])))
             ws = max(sm.workspace_bytes(sm.WS_TOPK, self.dt, tr, None, self.cfg.n_heads, self.cfg.vocab),
-                     sm.workspace_bytes(sm.WS_ACCEPT, self.dt, tr, None, sm.GREEDY))
+                     sm.workspace_bytes(sm.WS_ACCEPT, self.dt, tr, None, self.mode))
             hit = (trees, tr, ws)
             if len(self._tree_cache) < 256:
                 self._tree_cache[key] = hit
@@ -338,8 +341,8 @@ class DecodeLoop:
         path = torch.empty((B, self.stride), **i32)
         # acceptance with the compaction fused in; the sampled next token reads
         # only the logits and the accepted path, so it may follow the compaction
-        sm.accept_compact(self.dt, tr, kv, cfg.vocab, sm.GREEDY, lg, tok, acc, path, self.stride, nxt, ws=ws,
-                          ws_bytes=ws_bytes, stream=s)
+        sm.accept_compact(self.dt, tr, kv, cfg.vocab, self.mode, lg, tok, acc, path, self.stride, nxt, ws=ws,
+                          ws_bytes=ws_bytes, stream=s, **self.typical)
         mark("accept_compact")
         if st.temperature is not None:
             sm.sample_next(self.dt, tr, cfg.vocab, st.temperature, st.sample_seed, t, lg, acc, path, self.stride, nxt,

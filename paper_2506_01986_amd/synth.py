@@ -479,6 +479,7 @@ class DecodeSetup:
     p_accept: np.ndarray        # float64 [B] planted acceptance per level
     temperature: float | None   # sampled next token at this temperature, or greedy (None)
     sample_seed: int
+    typical: tuple | None = None  # (temperature, eps, delta): typical acceptance; None: greedy
 
     @property
     def cap_total(self) -> int:
@@ -497,9 +498,10 @@ class StepInputs:
 
 def decode_setup(cfg: Config, seed: int, default: Tree, room: Sequence[int], resblock: bool = True,
                  temperature: float | None = 0.8, lens: Sequence[int] | None = None,
-                 head_w: np.ndarray | None = None) -> DecodeSetup:
+                 head_w: np.ndarray | None = None, typical: tuple | None = None) -> DecodeSetup:
     """Initial state of a multi-step run: each slab holds its committed rows
-    and room[b] free rows for the whole run (head_w: reuse these head weights)."""
+    and room[b] free rows for the whole run (head_w: reuse these head weights;
+    typical: (temperature, eps, delta) of typical acceptance, else greedy)."""
     ss = dict(zip(STREAMS, np.random.SeedSequence(seed).spawn(len(STREAMS))))
     rng = {k: np.random.Generator(np.random.PCG64(v)) for k, v in ss.items()}
     B, d, dt = cfg.B, cfg.head_dim, cfg.dtype
@@ -539,7 +541,7 @@ def decode_setup(cfg: Config, seed: int, default: Tree, room: Sequence[int], res
     p = pr.uniform(cfg.p_range[0], cfg.p_range[1], size=B) if cfg.p_accept is None else np.full(B, cfg.p_accept)
     return DecodeSetup(cfg=cfg, seed=seed, lens=L, seq_base=base, seq_cap=caps, pool_k=pk, pool_v=pv,
                        default=default, head_w=head_w, w1=w1, b1=b1, root_tok=root, p_accept=p,
-                       temperature=temperature, sample_seed=seed * 7919 + 17)
+                       temperature=temperature, sample_seed=seed * 7919 + 17, typical=typical)
 
 
 def tree_prefix(t: Tree, n: int) -> Tree:

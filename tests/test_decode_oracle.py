@@ -17,12 +17,13 @@ def _cfg(dtype="bf16", **kw):
     return configs.Config(**base)
 
 
-@pytest.mark.parametrize("resblock,temperature", [(False, None), (True, None), (True, 0.8)])
-def test_decode_loop_bookkeeping(resblock, temperature):
+@pytest.mark.parametrize("resblock,temperature,typical", [(False, None, None), (True, None, None), (True, 0.8, None),
+                                                          (True, None, (0.7, 0.09, 0.3))])
+def test_decode_loop_bookkeeping(resblock, temperature, typical):
     cfg = _cfg()
     default = synth.t64()
     room = [200, 70, 9]                     # the third slab fills up within a few steps, the second shrinks its trees
-    st = synth.decode_setup(cfg, 5, default, room, resblock=resblock, temperature=temperature)
+    st = synth.decode_setup(cfg, 5, default, room, resblock=resblock, temperature=temperature, typical=typical)
     recs, K, V, lens = decode.run(st, 12)
     L = st.lens.astype(np.int64).copy()
     expect_rows = {b: [(st.pool_k[:, int(st.seq_base[b]) + r], st.pool_v[:, int(st.seq_base[b]) + r])
@@ -48,7 +49,7 @@ def test_decode_loop_bookkeeping(resblock, temperature):
             assert tok[o] == root[b]                                   # the previous step's next token
             acc = int(rec["acc"][i])
             path = rec["path"][i, :acc + 1]
-            # greedy acceptance of planted logits follows the planted walk
+            # greedy or typical acceptance of planted logits follows the planted walk
             planted = [0] + [c for (u, c, v) in inp.plans[i] if v > 0]
             assert path.tolist() == planted
             # the accepted tree rows, in path order, join the committed rows
@@ -81,3 +82,19 @@ def test_sampled_tokens_differ_from_greedy_and_follow_the_seed():
     assert not np.array_equal(rg[0]["next_tok"], rs[0]["next_tok"])
     again, *_ = decode.run(st_s, 3)
     assert all(np.array_equal(a["next_tok"], b["next_tok"]) for a, b in zip(rs, again))
+
+
+def test_typical_with_vanishing_thresholds_accepts_the_deepest_nodes():
+    # with eps and delta near zero every edge passes typical acceptance, so each
+    # step accepts a deepest node of its tree; greedy acceptance follows the
+    # planted walks, which mostly stop earlier
+    cfg = _cfg()
+    common = dict(resblock=False, temperature=None)
+    st_t = synth.decode_setup(cfg, 8, synth.t64(), [400] * 3, typical=(0.7, 1e-30, 1e-30), **common)
+    st_g = synth.decode_setup(cfg, 8, synth.t64(), [400] * 3, **common)
+    rt, *_ = decode.run(st_t, 3)
+    rg, *_ = decode.run(st_g, 3)
+    for rec in rt:
+        for n, a in zip(rec["sizes"], rec["acc"]):
+            assert a == int(synth.tree_prefix(st_t.default, n).depth.max())
+    assert any(int(a) < 4 for rec in rg for a in rec["acc"])

@@ -125,13 +125,20 @@ DECODE = {
     # fp32 path
     "fp32": (dict(dtype="fp32", B=2, n_q=4, n_kv=2, head_dim=64, hidden=40, vocab=333, w_std=1.0), [90, 12], True,
              1.5, 8),
+    # typical acceptance (App. A.1) with the sampled next token
+    "typical": (dict(dtype="bf16", B=3, n_q=8, n_kv=2, hidden=64, vocab=500), [300, 70, 9], True, 0.8, 10,
+                (0.7, 0.09, 0.3)),
+    # typical acceptance with vanishing thresholds: every step accepts a deepest node
+    "typical_deepest": (dict(dtype="bf16", B=3, n_q=8, n_kv=2, hidden=64, vocab=500), [300, 200, 60], False, None, 8,
+                        (0.7, 1e-30, 1e-30)),
 }
 
 
 @pytest.mark.parametrize("name", list(DECODE))
 def test_decode_loop(torch_cuda, name):
     from paper_2506_01986_amd import runner
-    kw, room, resblock, temperature, steps = DECODE[name]
+    kw, room, resblock, temperature, steps, *rest = DECODE[name]
+    typical = rest[0] if rest else None
     base = dict(name=name, head_dim=128, n_heads=4, topk=(10, 10, 10, 10), tree="T64", kv_len=(5, 200),
                 kv_len_dist="uniform", seed=11, w_std=0.05, p_accept=0.7)
     base.update(kw)
@@ -139,7 +146,7 @@ def test_decode_loop(torch_cuda, name):
     default = synth.t64()
     if name == "greedy_t128":
         default = synth.Tree(*(np.asarray(a, np.int32) for a in ob.build_tree(128, 45, 4, 10)))
-    st = synth.decode_setup(cfg, 11, default, room, resblock=resblock, temperature=temperature)
+    st = synth.decode_setup(cfg, 11, default, room, resblock=resblock, temperature=temperature, typical=typical)
     say(f"[decode] {name}: lens {st.lens.tolist()} caps {st.seq_cap.tolist()} steps {steps}")
     recs, K, V, lens = odec.run(st, steps)
     loop = runner.DecodeLoop(st)

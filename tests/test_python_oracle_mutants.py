@@ -93,6 +93,8 @@ DECODE = [
     ("lengths_not_advanced", "lens[seqs] = new_len", "pass", ["test_decode_loop_bookkeeping"]),
     ("sampling_ignored", "        if setup.temperature is not None:\n",
      "        if False:\n", ["test_sampled_tokens_differ_from_greedy_and_follow_the_seed"]),
+    ("typical_ignored", "        if setup.typical is not None:\n", "        if False:\n",
+     ["test_typical_with_vanishing_thresholds_accepts_the_deepest_nodes"]),
 ]
 
 
