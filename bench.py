@@ -507,6 +507,13 @@ def main():
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(kgbs / HBM_PEAK_GBS, 4),
                     "traffic": measured_traffic("head_logits_packed", cfg.name), "algorithmic_bytes": kbytes,
                     "ms": round(kms, 5), "source_sha256_16": source_sha("head_logits_packed")}
+    elif dom == "tree_attn" and cfg.dtype == "bf16":
+        # attention above the ridge point (FLOP per algorithmic byte > 2.5 PFLOP/s / 8 TB/s): matrix-core bound
+        roofline = {"bound": "mfma", "kernel": dom, "kernels": STAGE_KERNELS[dom], "achieved": st[dom]["TFLOPs"],
+                    "peak": MFMA_PEAK_TFLOPS[cfg.dtype], "unit": "TFLOP/s", "frac": st[dom]["mfma_frac"],
+                    "traffic": measured_traffic(dom, cfg.name), "algorithmic_flops": st[dom]["flops"],
+                    "algorithmic_bytes": st[dom]["algorithmic_bytes"], "ms": st[dom]["ms"],
+                    "source_sha256_16": source_sha(dom)}
     else:
         roofline = {"bound": "hbm", "kernel": dom, "kernels": STAGE_KERNELS[dom], "achieved": st[dom]["GBps"],
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": st[dom]["hbm_frac"],
@@ -542,7 +549,8 @@ def main():
     if not args.copy_calibration:       # a counter run keeps the calibration copy the only large copy
         print("[bench] measured peaks (copy, library GEMM)", file=sys.stderr, flush=True)
         mp = measured_peaks(torch)
-        mp["dominant_kernel_frac_of_copy"] = round(roofline["achieved"] / mp["copy_GBps"], 4)
+        if roofline["unit"] == "GB/s":
+            mp["dominant_kernel_frac_of_copy"] = round(roofline["achieved"] / mp["copy_GBps"], 4)
         if cfg.dtype == "bf16":
             mp["attention_frac_of_gemm"] = round(st["tree_attn"]["TFLOPs"] / mp["gemm_bf16_TFLOPs"], 4)
         result["measured_peaks"] = mp
