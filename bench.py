@@ -268,51 +268,60 @@ def decode_report(torch, cfg, wl, steps=48, warmup=3):
     base model's per-step outputs (hidden states, queries, tree K/V rows,
     logits) are Gaussian draws made on the device before timing, and so are
     the planted walks on full-size trees; the host planning, the walks on
-    pruned trees and the read-back are inside the timed loop."""
+    pruned trees and the read-back are inside the timed loop.  The run is
+    timed without events, then repeated with an event after every phase for
+    the phase table."""
     from paper_2506_01986_amd import runner, synth
     rng = np.random.default_rng(cfg.seed + 2000)
     room = (64 + rng.integers(0, 160, cfg.B)).astype(np.int32)
-    setup = synth.decode_setup(cfg, cfg.seed + 2000, synth.t64(), room, resblock=True, temperature=0.8,
-                               lens=wl.lens, head_w=wl.head_w)
-    loop = runner.DecodeLoop(setup, keep_logits=False, timing=True)
-    nmax = cfg.B * setup.default.n
+    nmax = cfg.B * synth.t64().n
     gen = torch.Generator(device="cuda")
     gen.manual_seed(cfg.seed + 2000)
     bf = torch.bfloat16
     rnd = lambda *shape: torch.randn(*shape, generator=gen, device="cuda", dtype=bf)
     pre = [dict(h=rnd(cfg.B, cfg.hidden), q=rnd(nmax, cfg.n_q, cfg.head_dim), k=rnd(cfg.n_kv, nmax, cfg.head_dim),
                 v=rnd(cfg.n_kv, nmax, cfg.head_dim), lg=rnd(nmax, cfg.vocab)) for _ in range(warmup + steps)]
-    prng = np.random.default_rng(cfg.seed + 2001)
-    # the planted walks on full-size trees, drawn before timing like the
-    # other model outputs; a pruned tree's walk is drawn when it is needed
-    full = [synth.plant_walks([setup.default] * cfg.B, setup.p_accept, prng)[0] for _ in range(warmup + steps)]
 
-    def inputs_for(t, plan):
-        seqs, sizes = plan
-        plans = [full[t][b] if n == setup.default.n else
-                 synth.plant_walks([synth.tree_prefix(setup.default, n)], setup.p_accept[[b]], prng)[0][0]
-                 for b, n in zip(seqs, sizes)]
-        n, x = int(sum(sizes)), pre[t]
-        return synth.StepInputs(hidden=x["h"][:len(seqs)], q=x["q"][:n], tree_k=x["k"][:, :n], tree_v=x["v"][:, :n],
-                                base_logits=x["lg"][:n], plans=plans)
+    def run(timing):
+        # the same run each time: fresh slabs, the same draws
+        setup = synth.decode_setup(cfg, cfg.seed + 2000, synth.t64(), room, resblock=True, temperature=0.8,
+                                   lens=wl.lens, head_w=wl.head_w)
+        loop = runner.DecodeLoop(setup, keep_logits=False, timing=timing)
+        prng = np.random.default_rng(cfg.seed + 2001)
+        # the planted walks on full-size trees, drawn before timing like the
+        # other model outputs; a pruned tree's walk is drawn when it is needed
+        full = [synth.plant_walks([setup.default] * cfg.B, setup.p_accept, prng)[0] for _ in range(warmup + steps)]
 
-    for t in range(warmup):
-        plan = loop.plan()
-        loop.step(t, inputs_for(t, plan), record=False, plan=plan)
-    torch.cuda.synchronize()
-    loop.events.clear()
-    acc_tokens = tree_tokens = done = 0
-    w0 = time.perf_counter()
-    for t in range(warmup, warmup + steps):
-        plan = loop.plan()
-        if not plan[0]:
-            break
-        rec = loop.step(t, inputs_for(t, plan), record=False, plan=plan)
-        acc_tokens += int(np.sum(rec["acc"] + 1))
-        tree_tokens += int(sum(rec["sizes"]))
-        done += 1
-    wall = time.perf_counter() - w0
-    phases = loop.phase_ms()
+        def inputs_for(t, plan):
+            seqs, sizes = plan
+            plans = [full[t][b] if n == setup.default.n else
+                     synth.plant_walks([synth.tree_prefix(setup.default, n)], setup.p_accept[[b]], prng)[0][0]
+                     for b, n in zip(seqs, sizes)]
+            n, x = int(sum(sizes)), pre[t]
+            return synth.StepInputs(hidden=x["h"][:len(seqs)], q=x["q"][:n], tree_k=x["k"][:, :n],
+                                    tree_v=x["v"][:, :n], base_logits=x["lg"][:n], plans=plans)
+
+        for t in range(warmup):
+            plan = loop.plan()
+            loop.step(t, inputs_for(t, plan), record=False, plan=plan)
+        torch.cuda.synchronize()
+        loop.events.clear()
+        acc_tokens = tree_tokens = done = 0
+        w0 = time.perf_counter()
+        for t in range(warmup, warmup + steps):
+            plan = loop.plan()
+            if not plan[0]:
+                break
+            rec = loop.step(t, inputs_for(t, plan), record=False, plan=plan)
+            acc_tokens += int(np.sum(rec["acc"] + 1))
+            tree_tokens += int(sum(rec["sizes"]))
+            done += 1
+        return time.perf_counter() - w0, done, acc_tokens, tree_tokens, loop, setup
+
+    # the loop's own time, then the same run again with an event after every phase
+    wall, done, acc_tokens, tree_tokens, loop, setup = run(False)
+    wall_ev, done_ev, *_, loop_ev, _ = run(True)
+    phases = loop_ev.phase_ms()
     ph = {k: float(np.mean([e[k] for e in phases])) for k in phases[0]}
     rb_bytes = cfg.n_heads * cfg.hidden * cfg.hidden * cfg.elem_bytes
     return {"steps": done, "ms_per_step": round(wall / done * 1e3, 4),
@@ -321,6 +330,7 @@ def decode_report(torch, cfg, wl, steps=48, warmup=3):
             "accepted_tokens_per_s": round(acc_tokens / wall, 1),
             "value": round(tree_tokens / wall, 1),
             "full_slabs": int(np.sum(loop.lens >= setup.seq_cap)),
+            "ms_per_step_with_phase_events": round(wall_ev / done_ev * 1e3, 4),
             "phase_ms": {k: round(v, 5) for k, v in ph.items()},
             "resblock": {"ms": round(ph["resblock"], 5), "weight_bytes": rb_bytes,
                          "GBps": round(rb_bytes / (ph["resblock"] * 1e-3) / 1e9, 1),
