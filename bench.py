@@ -137,12 +137,23 @@ def attention_flops(wl):
     return 4 * cfg.head_dim * cfg.n_q * keys
 
 
-def cpu_baseline(wl, min_seconds=10.0, max_reps=20):
+def cpu_baseline(wl, min_seconds=10.0, max_reps=20, budget=None):
     """The oracle on the same workload, timed on this host's cores.
 
     The whole step is repeated until at least `min_seconds` of oracle time have
-    passed (at most `max_reps` times); the mean is reported.
+    passed (at most `max_reps` times); the mean is reported.  `budget`
+    (device bytes, default tree, model terms) adds the oracle's time for the
+    two plans whose library times the budget report gives.
     """
+    out = {}
+    if budget is not None:
+        from oracle import budget as ob
+        device_bytes, tree, model = budget
+        for name, mem in (("fits", device_bytes), ("exhaustive", 0)):
+            t0 = time.perf_counter()
+            for _ in range(20):
+                ob.plan_budget(mem, batch=wl.cfg.B, default_tree=tuple(map(list, tree)), **model)
+            out[name] = round((time.perf_counter() - t0) / 20 * 1e6, 1)
     reps, total, stage_tot = 0, 0.0, np.zeros(4)
     while reps < max_reps and (reps == 0 or total < min_seconds):
         secs, stages = _oracle_step(wl)
@@ -156,7 +167,8 @@ def cpu_baseline(wl, min_seconds=10.0, max_reps=20):
                       f"{reps} repetitions",
             "seconds": round(total, 3), "seconds_per_step": round(mean, 3),
             "stage_seconds": {n: round(float(t) / reps, 3)
-                              for n, t in zip(["medusa_topk", "tree_attn", "accept", "kv_compact"], stage_tot)}}
+                              for n, t in zip(["medusa_topk", "tree_attn", "accept", "kv_compact"], stage_tot)},
+            **({"budget_plan_us": out} if out else {})}
 
 
 def _oracle_step(wl):
@@ -337,17 +349,22 @@ def decode_report(torch, cfg, wl, steps=48, warmup=3):
                          "hbm_frac": round(rb_bytes / (ph["resblock"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}}
 
 
-def budget_report(cfg, wl, device_bytes, reps=2000):
-    """The memory model and Alg. 1's plan for the workload's model on this
-    device (host calls of the library), with their host times and the
-    oracle's time for the same plans."""
-    from oracle import budget as ob
-    from paper_2506_01986_amd import specmemo as sm
+def budget_model(cfg, wl):
+    """The default tree and the model terms of Alg. 1's plan for this workload."""
     tree = (wl.trees[0].parent, wl.trees[0].depth, wl.trees[0].rank)
     model = dict(base_model_bytes=cfg.params * cfg.elem_bytes, head_bytes=cfg.hidden * cfg.vocab * cfg.elem_bytes,
                  layers=cfg.layers, n_kv=cfg.n_kv, head_dim=cfg.head_dim, vocab=cfg.vocab,
                  elem_bytes=cfg.elem_bytes, query_count=1, query_length=int(cfg.kv_len[1]),
                  default_heads=cfg.n_heads)
+    return tree, model
+
+
+def budget_report(cfg, wl, device_bytes, reps=2000):
+    """The memory model and Alg. 1's plan for the workload's model on this
+    device (host calls of the library), with their host times (the oracle's
+    times for the same plans are part of the CPU baseline)."""
+    from paper_2506_01986_amd import specmemo as sm
+    tree, model = budget_model(cfg, wl)
     plan = sm.plan_budget(device_bytes, batch=cfg.B, default_tree=tree, **model)
     # the largest batch of full-length sequences that keeps the default tree and heads
     lo, hi = 0, 1 << 20
@@ -361,12 +378,7 @@ def budget_report(cfg, wl, device_bytes, reps=2000):
         t0 = time.perf_counter()
         for _ in range(reps):
             sm.plan_budget(mem, batch=cfg.B, default_tree=tree, **model)
-        lib_us = (time.perf_counter() - t0) / reps * 1e6
-        t0 = time.perf_counter()
-        n_or = max(1, reps // 100)
-        for _ in range(n_or):
-            ob.plan_budget(mem, batch=cfg.B, default_tree=tuple(map(list, tree)), **model)
-        timings[name] = {"lib_us": round(lib_us, 2), "oracle_us": round((time.perf_counter() - t0) / n_or * 1e6, 1)}
+        timings[name] = {"lib_us": round((time.perf_counter() - t0) / reps * 1e6, 2)}
     sizes = sm.plan_tree_sizes(wl.lens, wl.seq_cap, int(wl.trees[0].n))
     t0 = time.perf_counter()
     for _ in range(reps):
@@ -579,7 +591,10 @@ def main():
         result["budget"] = budget_report(cfg, wl, torch.cuda.get_device_properties(0).total_memory)
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(wl)
+        budget = None
+        if cfg.params:
+            budget = (torch.cuda.get_device_properties(0).total_memory, *budget_model(cfg, wl))
+        result["cpu_baseline"] = cpu_baseline(wl, budget=budget)
     print(json.dumps(result), flush=True)
 
 
