@@ -230,7 +230,8 @@ int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab,
  * next_tok[b] is drawn from softmax(z / T) of the last accepted node's row,
  * z = base_logits[node_off[b] + path[b][accept_len[b]]], by the Gumbel-max
  * rule: the argmax over v of fmaf(z_v, 1/T, G_v) in fp32, with 1/T rounded
- * once to fp32, G_v = -log(-log(u_v)) and u_v = ((x >> 40) + 1/2) / 2^24 for
+ * once to fp32, G_v = -log(-log(u_v)) and u_v = ((x >> 41) + 1/2) / 2^23
+ * (exact in fp32, within [2^-24, 1 - 2^-24], so G_v is finite) for
  * x the 64-bit word v % 4 of Philox4x64-10 (Salmon et al., SC 2011) with key
  * (seed, offset) and counter (v / 4, b, 0, 0).  Ties go to the lower id.  A
  * caller draws a fresh sample per step by changing offset.  Sequences whose

@@ -220,14 +220,24 @@ def philox4x64_10(ctr, key) -> np.ndarray:
     return out
 
 
+def gumbel(words) -> np.ndarray:
+    """Standard Gumbel values -log(-log u) of 64-bit random words, with
+    u = (top 23 bits + 1/2) / 2^23, in float64."""
+    x = np.ascontiguousarray(words, dtype=np.uint64).reshape(-1)
+    g = np.empty(len(x), np.float64)
+    lib().oracle_gumbel(len(x), _p(x), _p(g))
+    return g
+
+
 def sample_next(logits, node_off, accept_len, path, temperature: float, seed: int, offset: int):
     """Gumbel-max draw from softmax(z / T) of each sequence's last accepted
-    node.  Returns (next_tok, best key, second-best key) of each sequence."""
+    node, keys in float64.  Returns (next_tok, best key, second-best key) of
+    each sequence."""
     sumN, vocab = logits.shape
     node_off, acc, path = _i32(node_off), _i32(accept_len), _i32(path)
     B, stride = path.shape
     tok = np.empty(B, np.int32)
-    best, second = np.empty(B, np.float32), np.empty(B, np.float32)
+    best, second = np.empty(B, np.float64), np.empty(B, np.float64)
     inv_t = np.float32(1.0) / np.float32(temperature)
     lib().oracle_sample_next(_dt(logits), B, _p(node_off), vocab, C.c_float(inv_t), C.c_uint64(seed),
                              C.c_uint64(offset), _p(logits), _p(acc), _p(path), stride, _p(tok), _p(best),

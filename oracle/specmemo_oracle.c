@@ -363,25 +363,32 @@ void oracle_philox4x64_10(int n, const uint64_t *ctr, const uint64_t *key, uint6
  * last accepted node's row, by the Gumbel-max rule: the argmax over v of
  * z_v / T + G_v with G_v = -log(-log(u_v)) standard Gumbel.  u_v comes from
  * Philox4x64-10 with key (seed, offset) and counter (v / 4, b, 0, 0), output
- * word v % 4: u = ((x >> 40) + 1/2) / 2^24.  The keys are formed in fp32 as
- * the kernel forms them (fmaf(z, 1/T, G), 1/T rounded once to fp32), so that
- * both sides take the argmax decision in the same precision; ties go to the
- * lower token id. */
+ * word v % 4: u = (k + 1/2) / 2^23 with k the word's top 23 bits, so that
+ * 0 < u < 1 for every word and G is finite.  The oracle forms u, G and the
+ * keys in fp64 from this definition (1/T is the caller's fp32 value); ties go
+ * to the lower token id. */
+void oracle_gumbel(int n, const uint64_t *x, double *g) {
+  for (int i = 0; i < n; ++i) {
+    double u = ((double)(x[i] >> 41) + 0.5) / 8388608.0;   /* 2^23 */
+    g[i] = -log(-log(u));
+  }
+}
+
 void oracle_sample_next(int dt, int B, const int *node_off, int vocab, float inv_temp, uint64_t seed,
                         uint64_t offset, const void *logits, const int *accept_len, const int *path, int stride,
-                        int *next_tok, float *best_key, float *second_key) {
+                        int *next_tok, double *best_key, double *second_key) {
   for (int b = 0; b < B; ++b) {
     int64_t row = node_off[b] + path[(int64_t)b * stride + accept_len[b]];
     uint64_t key[2] = {seed, offset};
-    float best = -INFINITY, second = -INFINITY;
+    double best = -INFINITY, second = -INFINITY;
     int arg = -1;
     for (int v0 = 0; v0 < vocab; v0 += 4) {
       uint64_t ctr[4] = {(uint64_t)(v0 / 4), (uint64_t)b, 0, 0}, x[4];
+      double g[4];
       philox4x64_10(ctr, key, x);
+      oracle_gumbel(4, x, g);
       for (int j = 0; j < 4 && v0 + j < vocab; ++j) {
-        float u = ((float)(x[j] >> 40) + 0.5f) * 0x1p-24f;
-        float g = -logf(-logf(u));
-        float s = fmaf((float)widen(logits, dt, row * vocab + v0 + j), inv_temp, g);
+        double s = widen(logits, dt, row * vocab + v0 + j) * (double)inv_temp + g[j];
         if (s > best) {
           second = best;
           best = s;

@@ -426,7 +426,7 @@ __device__ __forceinline__ void philox4x64_10(uint64_t (&x)[4], uint64_t k0, uin
 // Gumbel-max draw from softmax(z / T) of sequence b's last accepted row: the
 // argmax over v of fmaf(z_v, 1/T, G_v), G_v = -log(-log(u_v)), u_v from
 // Philox with key (seed, offset), counter (v / 4, b, 0, 0), word v % 4, as
-// ((x >> 40) + 1/2) / 2^24.  One block per sequence (the keys cost two
+// ((x >> 41) + 1/2) / 2^23 (strictly inside (0, 1), so G_v is finite).  One block per sequence (the keys cost two
 // logarithms and a Philox block per four tokens: all sixteen waves of the
 // block share the row); ties by lower token id.
 constexpr int kSampleThreads = 1024;
@@ -449,7 +449,8 @@ __global__ __launch_bounds__(kSampleThreads) void sample_next_kernel(SampleArgs 
     for (int j = 0; j < 4; ++j) {
       const int v = 4 * q + j;
       if (v < a.vocab) {
-        const float u = ((float)(x[j] >> 40) + 0.5f) * 0x1p-24f;
+        // 23 random bits: (k + 1/2) 2^-23 is exact in fp32 and lies in [2^-24, 1 - 2^-24]
+        const float u = ((float)(x[j] >> 41) + 0.5f) * 0x1p-23f;
         const float g = -logf(-logf(u));
         const float s = fmaf(ld<DT>(a.logits, row + v), a.inv_temp, g);
         if (better(s, v, best, arg)) {

@@ -376,6 +376,17 @@ def make(cfg: Config, seed: int | None = None, with_heads: bool = True,
                     store_dtype=dt)
 
 
+def redraw_hidden(cfg: Config, seed: int, b: int, attempt: int) -> np.ndarray:
+    """A replacement last hidden state for sequence ``b``: the ``attempt``-th
+    re-draw (attempt >= 1), N(0, 1) from ``SeedSequence([seed, 2, b, attempt])``,
+    stored like the original row.  A test that needs a batch whose head logits
+    hold no near-ties picks the attempt; the draw itself depends on nothing
+    else."""
+    assert attempt >= 1
+    ss = np.random.SeedSequence([seed, 2, b, attempt])
+    return _store(normals(ss, cfg.hidden), cfg.dtype)
+
+
 def planted_logits(wl: Workload, node_tok: np.ndarray) -> np.ndarray:
     """Copy of the base logits with the planted walk written in.
 

@@ -42,10 +42,13 @@ MUTANTS = [
      ["test_resblock_equals_torch_linear_silu"]),
     ("philox_weyl", "k1 += 0xBB67AE8584CAA73Bull;", "k1 += 0xBB67AE8584CAA73Aull;",
      ["test_philox_equals_numpy_stream"]),
-    ("gumbel_sign", "float g = -logf(-logf(u));", "float g = logf(-logf(u));",
-     ["test_sampled_token_follows_softmax"]),
-    ("temperature_dropped", "float s = fmaf((float)widen(logits, dt, row * vocab + v0 + j), inv_temp, g);",
-     "float s = (float)widen(logits, dt, row * vocab + v0 + j) + g;",
+    ("gumbel_sign", "g[i] = -log(-log(u));", "g[i] = log(-log(u));",
+     ["test_sampled_token_follows_softmax", "test_gumbel_words_give_finite_standard_gumbel_values"]),
+    ("gumbel_24_bits", "double u = ((double)(x[i] >> 41) + 0.5) / 8388608.0;",
+     "double u = (double)(float)(((float)(x[i] >> 40) + 0.5f) * 0x1p-24f);",
+     ["test_gumbel_words_give_finite_standard_gumbel_values"]),
+    ("temperature_dropped", "double s = widen(logits, dt, row * vocab + v0 + j) * (double)inv_temp + g[j];",
+     "double s = widen(logits, dt, row * vocab + v0 + j) + g[j];",
      ["test_sampled_token_follows_softmax"]),
     ("seq_len_off_by_one", "seq_len[b] = L + a + 1;", "seq_len[b] = L + a;",
      ["test_compaction_moves_accepted_rows_only"]),

@@ -605,3 +605,22 @@ def test_sampling_reads_the_last_accepted_row():
     path = np.tile(np.arange(n, dtype=np.int32), (B, 1))
     tok, _, _ = oracle.sample_next(logits, node_off, acc, path, 1.0, 5, 0)
     assert tok.tolist() == [0 * n + 0, 1 * n + 3, 2 * n + 2]
+
+
+def test_gumbel_words_give_finite_standard_gumbel_values():
+    # Every 64-bit word maps to a finite value: the extreme words (all zeros,
+    # all ones) included, where a 24-bit uniform rounded in fp32 would reach
+    # u = 1 and G = +inf.  Only the top 23 bits count, and G grows with them.
+    extremes = np.array([0, 2 ** 64 - 1, 2 ** 41 - 1, 2 ** 63, (2 ** 23 - 1) << 41], np.uint64)
+    g = oracle.gumbel(extremes)
+    assert np.all(np.isfinite(g))
+    assert g[0] == g[2] and g[1] == g[4]
+    assert g[0] < g[3] < g[1]
+    # The 2^23 equally likely top-bit patterns form a midpoint grid over (0, 1):
+    # the mean and variance of -log(-log u) over it are the standard Gumbel
+    # law's, Euler's constant and pi^2 / 6 (closed forms), up to the grid error.
+    k = np.arange(2 ** 23, dtype=np.uint64) << np.uint64(41)
+    gg = oracle.gumbel(k)
+    assert np.all(np.diff(gg) > 0)
+    assert abs(gg.mean() - np.euler_gamma) < 1e-5
+    assert abs(gg.var() - np.pi ** 2 / 6) < 1e-3
