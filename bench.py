@@ -11,6 +11,12 @@ Llama-2-70B-shaped batch of 10 sequences (64 query / 8 KV heads x 128, hidden
 8192, vocab 32000, 4 heads, 64-node tree, KV lengths U[512, 4096], slabs capped
 at 1.1 x live tokens).
 
+The headline is timed with cold caches: the per-step buffers (queries, KV
+pool, base logits, outputs, workspace) have several replicas, step k runs on
+replica k mod R, and R replicas exceed twice the 256 MB MALL, so no step finds
+its data in the caches; the same step on one replica (warm) is reported
+beside it.
+
 Prints one JSON line: the step throughput in verified tree tokens/s (sum of the
 tree sizes / step time), per-stage times and achieved bandwidth from HIP events
 on the stream the kernels run on, the roofline entry of the dominant kernel
@@ -85,8 +91,9 @@ def algorithmic_bytes(wl, acc):
       lists and the tree tokens.
     tree_attn: each sequence's committed and tree K/V rows once (2 * n_kv *
       head_dim elements per row) plus the queries read and outputs written.
-    accept: the logit rows of the nodes on the accepted paths (greedy walk)
-      and the node tokens.
+    accept: every node's logit row (sum N_b * vocab * s: a node's row decides
+      whether its children are accepted, and which nodes end up on the path
+      is known only after reading them) and the node tokens.
     kv_compact: the accepted rows of K and V, read and written once.
     """
     cfg = wl.cfg
@@ -96,7 +103,7 @@ def algorithmic_bytes(wl, acc):
         + cfg.B * cfg.n_heads * cfg.kmax * 8 + sumN * 4
     kv_rows = int(np.sum(wl.lens)) + sumN
     b = kv_rows * 2 * cfg.n_kv * cfg.head_dim * s + 2 * sumN * cfg.n_q * cfg.head_dim * s
-    c = int(np.sum(acc + 1)) * cfg.vocab * s + sumN * 4
+    c = sumN * cfg.vocab * s + sumN * 4
     d = 2 * int(np.sum(acc + 1)) * 2 * cfg.n_kv * cfg.head_dim * s
     return {"medusa_topk": a, "tree_attn": b, "accept": c, "kv_compact": d}
 
@@ -160,15 +167,41 @@ def cpu_baseline(wl, min_seconds=10.0, max_reps=20, budget=None):
         reps += 1
         total += secs
         stage_tot += stages
-    cores = len(os.sched_getaffinity(0))
+    import oracle
+    cores = oracle.threads()
     mean = total / reps
+    # one thread, on the two small workloads (one step each)
+    from paper_2506_01986_amd import configs, synth
+    single = {}
+    oracle.threads(1)
+    try:
+        for name in ("tiny_fp32", "llama2_7b_b1"):
+            w = synth.make(configs.get(name))
+            secs, _ = _oracle_step(w)
+            single[name] = {"value": round(w.total_nodes / secs, 2), "unit": "tokens/s",
+                            "seconds_per_step": round(secs, 4)}
+    finally:
+        oracle.threads(cores)
     return {"value": wl.total_nodes / mean, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": f"the whole step on the same workload ({wl.total_nodes} tree tokens, all stages, fp64), "
-                      f"{reps} repetitions",
-            "seconds": round(total, 3), "seconds_per_step": round(mean, 3),
+                      f"{reps} repetitions on {cores} threads; single_thread: one step of the tiny and 7B-shaped "
+                      f"workloads on one thread",
+            "cpu_model": cpu_model(), "seconds": round(total, 3), "seconds_per_step": round(mean, 3),
             "stage_seconds": {n: round(float(t) / reps, 3)
                               for n, t in zip(["medusa_topk", "tree_attn", "accept", "kv_compact"], stage_tot)},
+            "single_thread": single,
             **({"budget_plan_us": out} if out else {})}
+
+
+def cpu_model():
+    """The host CPU's model name (as lscpu reports it, from /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def _oracle_step(wl):
@@ -429,61 +462,75 @@ def main():
     torch.cuda.synchronize()
 
     names = ["medusa_topk", "tree_attn", "accept", "kv_compact"]
-    stages = [step.medusa_topk, step.tree_attn, step.accept, step.kv_compact]
-    # The same step through the four stage calls (acceptance and compaction
-    # separate): K steps, events at the two ends; timed first, so that the
-    # timed step below runs with the clocks in their steady state.
-    print("[bench] four-call step", file=sys.stderr, flush=True)
-    u_begin, u_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # Replicas of every per-step buffer (queries, pool, base logits, outputs,
+    # workspace; the head weights are shared and streamed past the caches
+    # anyway): steps rotated over them find none of their data in the 256 MB
+    # MALL, as in a full model, where the other layers' weights and caches
+    # pass through it between two steps of one layer.
+    mall = 256 << 20
+    nrep = max(3, -(-2 * mall // step.step_bytes()) + 1)
+    reps = [step] + [step.replica() for _ in range(nrep - 1)]
+    for r in reps[1:]:
+        for _ in range(3):
+            r.run_fused()
     torch.cuda.synchronize()
-    u_begin.record()
-    for _ in range(args.steps):
-        step.run()
-    u_end.record()
-    torch.cuda.synchronize()
-    unfused_ms = u_begin.elapsed_time(u_end) / args.steps
-    # Timed region: exactly K steps (projection and top-k, attention, acceptance
-    # with the compaction fused in: every stage of the path), HIP events on the
-    # kernels' stream at its two ends only (events between stages would add
-    # their own packets to the step).
-    print("[bench] timing", file=sys.stderr, flush=True)
-    t_begin, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    t_begin.record()
-    for _ in range(args.steps):
-        step.run_fused()
-    t_end.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    ms = t_begin.elapsed_time(t_end) / args.steps
-    # Per-stage breakdown (for the stage table and the roofline): another K
-    # four-call steps with an event after every stage.
-    print("[bench] stage breakdown", file=sys.stderr, flush=True)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    for k in range(args.steps):
-        ev[k][0].record()
-        for j, fn in enumerate(stages):
-            fn()
-            ev[k][j + 1].record()
-    torch.cuda.synchronize()
-    per_stage = np.array([[ev[k][j].elapsed_time(ev[k][j + 1]) for j in range(4)] for k in range(args.steps)])
-    # Attention with cold caches: a 1 GiB write before each call evicts the
-    # pool from the 256 MB MALL (within the step loop it stays there: the head
-    # weights stream past it nontemporally).
-    print("[bench] attention with cold caches", file=sys.stderr, flush=True)
-    scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-    cold_ev = []
-    for k in range(args.steps):
-        scratch.fill_(k & 0xFF)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def events(n):
+        return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+    def loop_ms(fn_of_k):
+        """K calls of fn_of_k(k), HIP events on the kernels' stream at the two ends only."""
+        e0, e1 = events(2)
+        torch.cuda.synchronize()
         e0.record()
-        step.tree_attn()
+        for k in range(args.steps):
+            fn_of_k(k)
         e1.record()
-        cold_ev.append((e0, e1))
-    torch.cuda.synchronize()
-    cold = np.array([a.elapsed_time(b) for a, b in cold_ev])
-    del scratch
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    def stage_table(rotate):
+        """K four-call steps with an event after every stage: [K, 4] ms."""
+        ev = [events(5) for _ in range(args.steps)]
+        for k in range(args.steps):
+            r = reps[k % nrep] if rotate else step
+            ev[k][0].record()
+            for j, fn in enumerate([r.medusa_topk, r.tree_attn, r.accept, r.kv_compact]):
+                fn()
+                ev[k][j + 1].record()
+        torch.cuda.synchronize()
+        return np.array([[ev[k][j].elapsed_time(ev[k][j + 1]) for j in range(4)] for k in range(args.steps)])
+
+    # The same step through the four stage calls (acceptance and compaction
+    # separate), rotated over the replicas; timed first, so that the timed
+    # step below runs with the clocks in their steady state.
+    print("[bench] four-call step", file=sys.stderr, flush=True)
+    unfused_ms = loop_ms(lambda k: reps[k % nrep].run())
+    print("[bench] warm steps (one replica)", file=sys.stderr, flush=True)
+    unfused_warm_ms = loop_ms(lambda k: step.run())
+    warm_ms = loop_ms(lambda k: step.run_fused())
+    # Timed region (the headline): exactly K steps (projection and top-k,
+    # attention, acceptance with the compaction fused in: every stage of the
+    # path), step k on replica k mod R, HIP events on the kernels' stream at
+    # its two ends only (events between stages would add their own packets).
+    print("[bench] timing", file=sys.stderr, flush=True)
+    w0 = time.perf_counter()
+    ms = loop_ms(lambda k: reps[k % nrep].run_fused())
+    wall = time.perf_counter() - w0
+    # Per-stage breakdown: K four-call steps with an event after every stage,
+    # rotated (cold, as the headline) and on one replica (warm).
+    print("[bench] stage breakdown", file=sys.stderr, flush=True)
+    per_stage = stage_table(True)
+    per_stage_warm = stage_table(False)
+    # Typical acceptance (App. A.1, Medusa's default): the fused step and the
+    # acceptance stage in that mode, rotated like the headline.
+    print("[bench] typical acceptance", file=sys.stderr, flush=True)
+    for r in reps:
+        r.mode = sm.TYPICAL
+    typ_ms = loop_ms(lambda k: reps[k % nrep].run_fused())
+    typ_stage = stage_table(True)[:, 2]
+    for r in reps:
+        r.mode = sm.GREEDY
     # The same step captured once in a HIP graph and replayed K times (no
     # per-launch host work; the kernels and their arguments are those above).
     print("[bench] graph replay", file=sys.stderr, flush=True)
@@ -492,34 +539,33 @@ def main():
         step.run_fused()
     graph.replay()
     torch.cuda.synchronize()
-    g_begin, g_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    g_begin.record()
-    for _ in range(args.steps):
-        graph.replay()
-    g_end.record()
-    torch.cuda.synchronize()
-    graph_ms = g_begin.elapsed_time(g_end) / args.steps
+    graph_ms = loop_ms(lambda k: graph.replay())
     del graph
     acc = step.accept_len.cpu().numpy()
     byts = algorithmic_bytes(wl, acc)
     st = {}
     for j, n in enumerate(names):
-        t = float(per_stage[:, j].mean())
+        t, tw = float(per_stage[:, j].mean()), float(per_stage_warm[:, j].mean())
         gbs = byts[n] / (t * 1e-3) / 1e9
         st[n] = {"ms": round(t, 5), "ms_p10": round(float(np.percentile(per_stage[:, j], 10)), 5),
                  "ms_p90": round(float(np.percentile(per_stage[:, j], 90)), 5),
-                 "algorithmic_bytes": int(byts[n]), "GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+                 "algorithmic_bytes": int(byts[n]), "GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+                 "ms_warm": round(tw, 5), "hbm_frac_warm": round(byts[n] / (tw * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     fl = attention_flops(wl)
     st["tree_attn"]["flops"] = fl
     st["tree_attn"]["TFLOPs"] = round(fl / (st["tree_attn"]["ms"] * 1e-3) / 1e12, 1)
     st["tree_attn"]["mfma_frac"] = round(st["tree_attn"]["TFLOPs"] / MFMA_PEAK_TFLOPS[cfg.dtype], 4)
-    tc = float(np.median(cold))
-    st["tree_attn"]["cold_caches"] = {"ms": round(tc, 5), "GBps": round(byts["tree_attn"] / (tc * 1e-3) / 1e9, 1),
-                                      "TFLOPs": round(fl / (tc * 1e-3) / 1e12, 1)}
+    st["tree_attn"]["mfma_frac_warm"] = round(fl / (st["tree_attn"]["ms_warm"] * 1e-3) / 1e12
+                                              / MFMA_PEAK_TFLOPS[cfg.dtype], 4)
     ab = byts["tree_attn"] + byts["kv_compact"]
-    at = (per_stage[:, 1] + per_stage[:, 3]).mean()
-    st["tree_attn+kv_compact"] = {"ms": round(float(at), 5), "GBps": round(ab / (at * 1e-3) / 1e9, 1),
-                                  "hbm_frac": round(ab / (at * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    for key, tab in (("tree_attn+kv_compact", per_stage), ("tree_attn+kv_compact_warm", per_stage_warm)):
+        at = float((tab[:, 1] + tab[:, 3]).mean())
+        st[key] = {"ms": round(at, 5), "GBps": round(ab / (at * 1e-3) / 1e9, 1),
+                   "hbm_frac": round(ab / (at * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    tt = float(typ_stage.mean())
+    st["accept_typical"] = {"ms": round(tt, 5), "algorithmic_bytes": int(byts["accept"]),
+                            "GBps": round(byts["accept"] / (tt * 1e-3) / 1e9, 1),
+                            "hbm_frac": round(byts["accept"] / (tt * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     dom = max(names, key=lambda n: st[n]["ms"])
     if DOMINANT_KERNEL.get(dom) == "head_logits_packed" and step.head_layout == sm.HEADS_PACKED:
         print("[bench] projection kernel alone", file=sys.stderr, flush=True)
@@ -560,12 +606,22 @@ def main():
         "roofline": roofline,
         "accepted_tokens_per_s": round(float(np.sum(acc + 1)) / (ms * 1e-3), 1),
         "wall_ms_per_step": round(wall / args.steps * 1e3, 5),
+        "caches": {"headline": f"cold: step k runs on replica k mod {nrep} of the per-step buffers "
+                               f"({step.step_bytes()} bytes each; the MALL holds 256 MB)",
+                   "replicas": nrep, "replica_bytes": step.step_bytes()},
+        "warm": {"ms_per_step": round(warm_ms, 5), "value": round(wl.total_nodes / (warm_ms * 1e-3), 1),
+                 "note": "the same step, every step on one replica (its pool stays in the MALL)"},
+        "typical": {"ms_per_step": round(typ_ms, 5), "value": round(wl.total_nodes / (typ_ms * 1e-3), 1),
+                    "accept_stage_ms": st["accept_typical"]["ms"], "temperature": step.temperature,
+                    "eps": step.eps, "delta": step.delta},
         "ms_per_step_with_stage_events": round(float(per_stage.sum(axis=1).mean()), 5),
-        "graph": {"ms_per_step": round(graph_ms, 5), "value": round(wl.total_nodes / (graph_ms * 1e-3), 1)},
+        "graph": {"ms_per_step": round(graph_ms, 5), "value": round(wl.total_nodes / (graph_ms * 1e-3), 1),
+                  "note": "one replica (warm)"},
         "step_calls": ["specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept_compact"],
         "four_call_step": {"calls": ["specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept",
                                      "specmemo_kv_compact"],
-                           "ms_per_step": round(unfused_ms, 5), "value": round(wl.total_nodes / (unfused_ms * 1e-3), 1)},
+                           "ms_per_step": round(unfused_ms, 5), "value": round(wl.total_nodes / (unfused_ms * 1e-3), 1),
+                           "ms_per_step_warm": round(unfused_warm_ms, 5)},
         "stages": st,
     }
     if not args.copy_calibration:       # a counter run keeps the calibration copy the only large copy
@@ -581,7 +637,7 @@ def main():
         pr = padded_report(torch, cfg, wl, step, args.steps)
         pr["kv_bytes_all_layers_compacted"] = int((np.sum(wl.lens) + wl.total_nodes) * 2 * cfg.n_kv * cfg.head_dim
                                                   * cfg.elem_bytes * cfg.layers)
-        pr["step_time_vs_compaction"] = round(pr["ms_per_step"] / unfused_ms, 4)   # both four-call steps
+        pr["step_time_vs_compaction"] = round(pr["ms_per_step"] / unfused_warm_ms, 4)   # both four-call, warm
         result["padded"] = pr
     if not args.no_decode and cfg.dtype == "bf16":
         print("[bench] multi-step decode", file=sys.stderr, flush=True)

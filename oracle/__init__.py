@@ -44,6 +44,12 @@ def lib():
     return _lib
 
 
+def threads(n: int = 0) -> int:
+    """Threads of the oracle's parallel loops: n >= 1 sets them; returns the
+    count in use."""
+    return int(lib().oracle_threads(int(n)))
+
+
 def _dt(x: np.ndarray) -> int:
     if x.dtype == np.float32:
         return 0
@@ -172,6 +178,17 @@ def accept_typical(logits, node_tok, node_off, parent, depth, path_stride: int,
     if edges:
         return acc, path, nxt, lp, lt
     return acc, path, nxt
+
+
+def softmax_stats(logits, temperature: float):
+    """(lse, H) of each row x = z / T in float64: log sum exp x and the
+    entropy of softmax(x)."""
+    rows, vocab = logits.shape
+    lse = np.empty(rows, np.float64)
+    ent = np.empty(rows, np.float64)
+    lib().oracle_softmax_stats(_dt(logits), rows, vocab, _p(np.ascontiguousarray(logits)),
+                               C.c_double(temperature), _p(lse), _p(ent))
+    return lse, ent
 
 
 def kv_compact(K, V, seq_base, seq_len, accept_len, path):

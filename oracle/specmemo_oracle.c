@@ -34,6 +34,7 @@
  * accepted nodes the larger summed log-probability wins, then the lower id.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -47,6 +48,12 @@ static double widen(const void *p, int dt, int64_t i) {
   float f;
   memcpy(&f, &bits, sizeof f);
   return (double)f;
+}
+
+/* Threads of the parallel loops: n >= 1 sets them; returns the count in use. */
+int oracle_threads(int n) {
+  if (n > 0) omp_set_num_threads(n);
+  return omp_get_max_threads();
 }
 
 /* Order of (value, id) pairs used by top-k and argmax: larger value first,
@@ -227,15 +234,13 @@ void oracle_accept_greedy(int dt, int B, const int *node_off, const int *parent,
  * next_tok = argmax z_cur.  Optional per-node outputs (index = global node,
  * root entries unused): log pi of the edge into the node and the log threshold
  * of that edge. */
-void oracle_accept_typical(int dt, int B, const int *node_off, const int *parent, const int *depth,
-                           int vocab, const void *logits, const int *node_tok, double temperature,
-                           double eps, double delta, int path_stride, int *accept_len, int *path,
-                           int *next_tok, double *edge_logpi, double *edge_logthr) {
-  int total = node_off[B];
-  double *lse = (double *)malloc(sizeof(double) * total);
-  double *ent = (double *)malloc(sizeof(double) * total);
+/* Softmax statistics of each row x = z / T of typical acceptance (App. A.1):
+ * lse = log sum_v exp(x_v) and the entropy H = -sum_v pi_v log pi_v of
+ * pi = softmax(x). */
+void oracle_softmax_stats(int dt, int rows, int vocab, const void *logits, double temperature, double *lse,
+                          double *ent) {
 #pragma omp parallel for schedule(dynamic, 4)
-  for (int u = 0; u < total; ++u) {
+  for (int u = 0; u < rows; ++u) {
     double m = -INFINITY;
     for (int v = 0; v < vocab; ++v) {
       double x = widen(logits, dt, (int64_t)u * vocab + v) / temperature;
@@ -252,6 +257,16 @@ void oracle_accept_typical(int dt, int B, const int *node_off, const int *parent
     lse[u] = l;
     ent[u] = hsum;
   }
+}
+
+void oracle_accept_typical(int dt, int B, const int *node_off, const int *parent, const int *depth,
+                           int vocab, const void *logits, const int *node_tok, double temperature,
+                           double eps, double delta, int path_stride, int *accept_len, int *path,
+                           int *next_tok, double *edge_logpi, double *edge_logthr) {
+  int total = node_off[B];
+  double *lse = (double *)malloc(sizeof(double) * total);
+  double *ent = (double *)malloc(sizeof(double) * total);
+  oracle_softmax_stats(dt, total, vocab, logits, temperature, lse, ent);
   for (int b = 0; b < B; ++b) {
     int o = node_off[b], N = node_off[b + 1] - o;
     int *acc = (int *)malloc(sizeof(int) * N);

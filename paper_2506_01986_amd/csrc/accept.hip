@@ -265,51 +265,109 @@ __global__ __launch_bounds__(64) void accept_walk_compact(AcceptArgs a, CompactA
 }
 
 // Typical mode, pass 1: per row u, x = z_u / T: lse_u = log sum exp x and
-// H_u = lse_u - sum softmax(x) * x.
-template <int DT>
-__global__ __launch_bounds__(256) void row_softmax_stats(AcceptArgs a) {
-  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t base = (int64_t)u * a.vocab;
-  float m = -INFINITY, s = 0.f, t = 0.f;
-  for (int v = tid; v < a.vocab; v += 256) {
-    const float x = ld<DT>(a.logits, base + v) * a.inv_temp;
-    if (x > m) {
-      const float r = expf(m - x);
-      s *= r;
-      t *= r;
-      m = x;
-    }
-    const float e = expf(x - m);
-    s += e;
-    t += e * x;
-  }
-  auto merge = [](float &m1, float &s1, float &t1, float m2, float s2, float t2) {
-    const float M = fmaxf(m1, m2);
-    if (M == -INFINITY) return;
-    const float r1 = expf(m1 - M), r2 = expf(m2 - M);
-    s1 = s1 * r1 + s2 * r2;
-    t1 = t1 * r1 + t2 * r2;
-    m1 = M;
-  };
+// H_u = -sum pi log pi with pi = softmax(x).  In base 2, with y = x log2(e),
+// M = max y, e_v = 2^(y_v - M), s = sum e and t = sum e (y - M):
+// lse = (M + log2 s) ln 2 and H = (log2 s - t / s) ln 2.  Exponents below
+// -128 are clamped there: their weights (< 2^-128 of the largest) change
+// neither sum in fp32.  One block per row; the block's maximum, then the two
+// sums, reduced over waves with DPP / permlane steps and LDS.
+__device__ __forceinline__ float block_max(float v, float *red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  v = wave_max(v);
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  v = red[0];
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1)
-    merge(m, s, t, __shfl_xor(m, off), __shfl_xor(s, off), __shfl_xor(t, off));
-  __shared__ float sm[4], ss[4], st[4];
+  for (int w = 1; w < kWaves; ++w) v = fmaxf(v, red[w]);
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  v += dpp_f<0x140>(v);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  return sum_with_other_half(v);
+}
+
+__device__ __forceinline__ void finish_stats(const AcceptArgs &a, int u, float M, float s, float t, float *red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  s = wave_sum(s);
+  t = wave_sum(t);
+  __syncthreads();   // every wave has read the maximum
   if (lane == 0) {
-    sm[wave] = m;
-    ss[wave] = s;
-    st[wave] = t;
+    red[wave] = s;
+    red[kWaves + wave] = t;
   }
   __syncthreads();
-  if (tid == 0) {
-    m = sm[0];
-    s = ss[0];
-    t = st[0];
-    for (int w = 1; w < 4; ++w) merge(m, s, t, sm[w], ss[w], st[w]);
-    const float lse = m + logf(s);
-    a.stats[2 * (int64_t)u] = lse;
-    a.stats[2 * (int64_t)u + 1] = lse - t / s;
+  if (threadIdx.x == 0) {
+    float S = 0.f, T = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      S += red[w];
+      T += red[kWaves + w];
+    }
+    const float ln2 = 0.6931471805599453f, l2s = __log2f(S);
+    a.stats[2 * (int64_t)u] = (M + l2s) * ln2;
+    a.stats[2 * (int64_t)u + 1] = (l2s - T / S) * ln2;
   }
+}
+
+// Weight and its exponent of one logit z: d = max(z c - M, -128), 2^d.
+__device__ __forceinline__ void stat_term(float z, float c, float M, float &s, float &t) {
+  const float d = fmaxf(fmaf(z, c, -M), -128.f);
+  const float e = fast_exp2(d);
+  s += e;
+  t = fmaf(e, d, t);
+}
+
+template <int DT>
+__global__ __launch_bounds__(kNT) void row_softmax_stats(AcceptArgs a) {
+  __shared__ float red[2 * kWaves];
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const int64_t base = (int64_t)u * a.vocab;
+  const float c = a.inv_temp * 1.4426950408889634f;   // y = z c
+  float s = 0.f, t = 0.f;
+  if (DT == 1 && (a.vocab & 7) == 0 && a.vocab <= kArgMaxVocab) {
+    // the row stays in registers: eight 16-byte loads per thread, all in flight
+    const uint4 *p = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(a.logits) + base);
+    const int nch = a.vocab / 8;
+    uint4 w[kArgU];
+#pragma unroll
+    for (int k = 0; k < kArgU; ++k) {
+      const int ch = k * kNT + tid;
+      w[k] = ch < nch ? p[ch] : uint4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};   // -inf
+    }
+    float mz = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < kArgU; ++k) {
+      const uint32_t ws[4] = {w[k].x, w[k].y, w[k].z, w[k].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mz = fmaxf(mz, fmaxf(__uint_as_float(ws[e] << 16), __uint_as_float(ws[e] & 0xFFFF0000u)));
+    }
+    const float M = block_max(mz, red) * c;
+#pragma unroll
+    for (int k = 0; k < kArgU; ++k) {
+      if (k * kNT + tid < nch) {
+        const uint32_t ws[4] = {w[k].x, w[k].y, w[k].z, w[k].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          stat_term(__uint_as_float(ws[e] << 16), c, M, s, t);
+          stat_term(__uint_as_float(ws[e] & 0xFFFF0000u), c, M, s, t);
+        }
+      }
+    }
+    finish_stats(a, u, M, s, t, red);
+    return;
+  }
+  // any dtype and vocabulary: two passes over the row
+  float mz = -INFINITY;
+  for (int v = tid; v < a.vocab; v += kNT) mz = fmaxf(mz, ld<DT>(a.logits, base + v));
+  const float M = block_max(mz, red) * c;
+  for (int v = tid; v < a.vocab; v += kNT) stat_term(ld<DT>(a.logits, base + v), c, M, s, t);
+  finish_stats(a, u, M, s, t, red);
 }
 
 // Typical mode, pass 2, by one block: the edges of sequence b's tree, the
@@ -496,9 +554,9 @@ hipError_t launch_accept_rows(int dt, const AcceptArgs &a, int total_nodes, hipS
     else
       hipLaunchKernelGGL(row_argbest_all<0>, dim3(total_nodes), dim3(kNT), 0, st, a);
   } else if (dt == 1) {
-    hipLaunchKernelGGL(row_softmax_stats<1>, dim3(total_nodes), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(row_softmax_stats<1>, dim3(total_nodes), dim3(kNT), 0, st, a);
   } else {
-    hipLaunchKernelGGL(row_softmax_stats<0>, dim3(total_nodes), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(row_softmax_stats<0>, dim3(total_nodes), dim3(kNT), 0, st, a);
   }
   return hipGetLastError();
 }

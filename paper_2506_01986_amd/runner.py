@@ -87,6 +87,26 @@ class VerifyStep:
         self.ws_bytes = ws
         self.ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=device)
 
+    def replica(self) -> "VerifyStep":
+        """Another step over the same workload that shares the head weights,
+        trees and hidden states but owns copies of every per-step buffer
+        (queries, pool, lengths, base logits, outputs, workspace).  Steps
+        rotated over enough replicas find none of their data in the caches."""
+        import copy
+        r = copy.copy(self)
+        for name in ("q", "k", "v", "seq_len", "out", "topk_ids", "topk_vals", "node_tok", "accept_len", "path",
+                     "next_tok", "ws", "base_logits", "logits", "key_valid", "pos"):
+            t = getattr(self, name)
+            if t is not None:
+                setattr(r, name, t.clone())
+        r.kv = sm.KVPool(r.k, r.v, r.seq_len, self.wl.seq_base, self.wl.seq_cap, self.wl.lens)
+        return r
+
+    def step_bytes(self) -> int:
+        """Device bytes a replica owns (what one step touches besides the heads)."""
+        ts = (self.q, self.k, self.v, self.out, self.base_logits, self.ws, self.topk_ids, self.node_tok)
+        return int(sum(t.numel() * t.element_size() for t in ts if t is not None))
+
     def set_base_logits(self, stored: np.ndarray):
         self.base_logits = to_device(stored, self.cfg.dtype, self.device)
 

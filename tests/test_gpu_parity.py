@@ -417,6 +417,91 @@ def test_acceptance_small_vocab_random(torch_cuda):
         assert checked > B // 2
 
 
+def _typical_rows(rng, trees, vocab, dtype, T, eps, delta):
+    """Unplanted N(0, 1) logit rows for typical acceptance, with distinct
+    sibling tokens; along one walk per tree the chosen child's token is
+    placed just above its edge threshold and one sibling's just below, at
+    margins of 2e-4 .. 0.2 in log-probability (fp32 keeps them; bf16 rounds
+    them to its grid).  The placement reads the oracle's row statistics."""
+    node_off = np.concatenate([[0], np.cumsum([t.n for t in trees])]).astype(np.int32)
+    N = int(node_off[-1])
+    z = rng.standard_normal((N, vocab)).astype(np.float32)
+    tok = np.zeros(N, np.int32)
+    placed = []                                   # (row u, token, margin)
+    margins = [2e-4, 5e-4, 1e-3, 3e-3, 0.02, 0.2]
+    for b, t in enumerate(trees):
+        o = int(node_off[b])
+        for u in range(t.n):
+            kids = synth.children(t, u)
+            if kids:
+                tok[o + np.array(kids)] = rng.choice(vocab, size=len(kids), replace=False)
+        u = 0
+        while synth.children(t, u):
+            kids = synth.children(t, u)
+            c = kids[int(rng.integers(len(kids)))]
+            m = float(rng.choice(margins))
+            placed.append((o + u, int(tok[o + c]), m))
+            if len(kids) > 1:
+                sib = next(k for k in kids if k != c)
+                placed.append((o + u, int(tok[o + sib]), -float(rng.choice(margins))))
+            u = c
+    for _ in range(4):                            # lse and H move slightly with each placed value
+        lse, H = oracle.softmax_stats(z, T)
+        for u, v, m in placed:
+            lthr = min(np.log(eps), np.log(delta) - H[u])
+            z[u, v] = np.float32(T * (lthr + m + lse[u]))
+    return (z if dtype == "fp32" else synth.to_bf16_bits(z)), tok, node_off
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_typical_full_vocab(torch_cuda, dtype):
+    """Typical acceptance (App. A.1) at the 70B-shaped batch's size: ten
+    64-node trees, vocabulary 32000, unplanted rows.  The per-row statistics
+    the kernel leaves in the workspace (lse and entropy of softmax(z / T))
+    must match the oracle's, and the accepted lengths, paths and next tokens
+    must be bit-exact for every sequence whose edges all lie more than 1e-4
+    (log units) from their thresholds (the guard of the fp32 decision)."""
+    import torch
+    from paper_2506_01986_amd import specmemo as sm
+    from paper_2506_01986_amd.runner import to_device
+    T, eps, delta = 0.7, 0.09, 0.3
+    rng = np.random.default_rng(70)
+    trees = [synth.t64() for _ in range(10)]
+    lg, tok, node_off = _typical_rows(rng, trees, 32000, dtype, T, eps, delta)
+    parent = np.concatenate([t.parent for t in trees])
+    depth = np.concatenate([t.depth for t in trees])
+    rank = np.concatenate([t.rank for t in trees])
+    tr = sm.Trees(node_off, parent, depth, rank, device="cuda")
+    B, N, stride = len(trees), int(node_off[-1]), 5
+    dt = sm.FP32 if dtype == "fp32" else sm.BF16
+    ws = torch.empty(sm.workspace_bytes(sm.WS_ACCEPT, dt, tr, None, sm.TYPICAL), dtype=torch.uint8, device="cuda")
+    out = [torch.full((B,), -7, dtype=torch.int32, device="cuda"),
+           torch.full((B, stride), -7, dtype=torch.int32, device="cuda"),
+           torch.full((B,), -7, dtype=torch.int32, device="cuda")]
+    say(f"[typical] {dtype}: B={B} rows={N} vocab=32000")
+    sm.accept(dt, tr, 32000, sm.TYPICAL, to_device(lg, dtype, "cuda"), torch.from_numpy(tok).cuda(), out[0], out[1],
+              stride, out[2], temperature=T, eps=eps, delta=delta, ws=ws, ws_bytes=ws.numel())
+    torch.cuda.synchronize()
+    stats = ws[:8 * N].view(torch.float32).cpu().numpy().reshape(N, 2).astype(np.float64)
+    lse, H = oracle.softmax_stats(lg, T)
+    e_lse, e_H = np.abs(stats[:, 0] - lse).max(), np.abs(stats[:, 1] - H).max()
+    say(f"[typical]   max |lse err| {e_lse:.3g}, max |H err| {e_H:.3g}, H in [{H.min():.3f}, {H.max():.3f}]")
+    assert e_lse <= 1e-4 and e_H <= 1e-4
+    ra, rp, rn, lp, lt = oracle.accept_typical(lg, tok, node_off, parent, depth, stride, T, eps, delta, edges=True)
+    ga, gp, gn = (o.cpu().numpy() for o in out)
+    checked = 0
+    for b in range(B):
+        o, n1 = node_off[b], node_off[b + 1]
+        if np.abs(lp[o + 1:n1] - lt[o + 1:n1]).min() < 1e-4:
+            continue
+        checked += 1
+        assert ga[b] == ra[b] and np.array_equal(gp[b], rp[b]) and gn[b] == rn[b], (b, ga[b], ra[b])
+    margins = np.abs(lp - lt)[np.isfinite(lp)]
+    say(f"[typical]   accepted {(ra + 1).tolist()}, compared {checked}/{B}, smallest edge margin {margins.min():.2g}")
+    assert checked == B
+    assert ra.max() >= 2                          # the placed walks reach past the first level
+
+
 def _argbest_rows(rng, vocab, n):
     """Logit rows (float32, exactly representable in bf16) that stress the arg-best order."""
     rows = []

@@ -298,6 +298,23 @@ def test_greedy_acceptance_equals_brute_force(int_logits):
         assert path[0, :ra + 1].tolist() == rp and np.all(path[0, ra + 1:] == -1)
 
 
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_softmax_stats_equal_library_logsumexp_and_entropy(dtype):
+    rng = np.random.default_rng(41)
+    raw = (rng.standard_normal((6, 32000)) * np.array([[1.0], [3.0], [0.1], [1.0], [8.0], [1.0]])).astype(np.float32)
+    raw[3, 17] = 200.0                                    # one dominant token: entropy near 0
+    raw[5] = 2.5                                          # uniform row: lse = x + log w, H = log w
+    z = synth._store(raw.reshape(-1), dtype).reshape(raw.shape)
+    x64 = f64(z, dtype)
+    for T in (0.7, 1.0, 1.5):
+        lse, ent = oracle.softmax_stats(z, T)
+        assert np.allclose(lse, scipy.special.logsumexp(x64 / T, axis=1), rtol=1e-13, atol=1e-12)
+        assert np.allclose(ent, scipy.stats.entropy(scipy.special.softmax(x64 / T, axis=1), axis=1),
+                           rtol=1e-11, atol=1e-12)
+        assert abs(ent[5] - np.log(32000)) < 1e-12 and abs(lse[5] - (2.5 / T + np.log(32000))) < 1e-12
+        assert ent[3] < 1e-10
+
+
 def test_typical_acceptance_equals_brute_force():
     rng = np.random.default_rng(5)
     for i in range(300):
