@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SPECMEMO_ABI_VERSION 7
+#define SPECMEMO_ABI_VERSION 8
 #define SPECMEMO_MAX_TREE_NODES 128 /* nodes per sequence's tree */
 #define SPECMEMO_MAX_DEPTH 15       /* tree depth (= Medusa heads) */
 #define SPECMEMO_MAX_TOPK 32        /* top-k per head */
@@ -199,6 +199,22 @@ size_t specmemo_packed_heads_bytes(specmemo_dtype dt, int32_t n_heads, int32_t v
 int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
                        int32_t n_q, float scale, const void *q, void *out, void *ws,
                        size_t ws_bytes, void *stream);
+
+/* (b) without a workspace argument, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation.  The split-KV partial results that specmemo_tree_attn
+ * keeps in `ws` go to a scratch array of SPECMEMO_ATTN_STATIC_SCRATCH_BYTES
+ * (32 MiB) that the library holds on each device it runs on, from the
+ * library's load until the process ends; the call itself allocates nothing.
+ * A batch whose split needs more (specmemo_workspace_bytes(SPECMEMO_WS_ATTN,
+ * ...) > 32 MiB) is rejected with SPECMEMO_E_WORKSPACE before anything is
+ * enqueued; every default split fits.  All calls on one device share that
+ * array, which keeps the last call's contents: calls that can overlap on one
+ * device (other streams, other threads) race, and the caller must order them.
+ * Arguments, checks and results are those of specmemo_tree_attn. */
+#define SPECMEMO_ATTN_STATIC_SCRATCH_BYTES ((size_t)32 << 20)
+int specmemo_tree_attn_noalloc(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
+                               int32_t n_q, float scale, const void *q, void *out, void *stream);
 
 /* (c) Acceptance (App. A.1: each candidate token must pass a threshold,
  * verification is cumulative along the sequence, the longest verified

@@ -18,6 +18,8 @@
 
 using namespace specmemo;
 
+static_assert(kAttnStaticScratchBytes == SPECMEMO_ATTN_STATIC_SCRATCH_BYTES, "static scratch size of the ABI");
+
 namespace {
 thread_local std::string g_err;
 }  // namespace
@@ -505,8 +507,11 @@ int specmemo_medusa_resblock(specmemo_dtype dt, int32_t B, int32_t hidden, int32
 namespace {
 
 // Tree attention with an optional pad-token mask (padded batching).
+// static_scratch: the partials go to the library's static scratch array
+// (specmemo_tree_attn_noalloc) instead of the caller's workspace.
 int tree_attn_impl(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, const uint32_t *key_valid,
-                   int32_t n_q, float scale, const void *q, void *out, void *ws, size_t ws_bytes, void *stream) {
+                   int32_t n_q, float scale, const void *q, void *out, void *ws, size_t ws_bytes, void *stream,
+                   bool static_scratch = false) {
   TreeInfo ti;
   int rc;
   if ((rc = check_attn_args(dt, t, kv, n_q, &ti))) return rc;
@@ -549,6 +554,14 @@ int tree_attn_impl(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv
   }
   AttnPlan p;
   plan_attn(ti, t, kv, n_q, &p);
+  if (static_scratch) {
+    if (p.ws_bytes > kAttnStaticScratchBytes)
+      return fail(SPECMEMO_E_WORKSPACE, "this batch needs %zu bytes of scratch; the static scratch holds %zu", p.ws_bytes,
+                  kAttnStaticScratchBytes);
+    hipError_t e = attn_static_scratch(&ws);
+    if (e != hipSuccess) return hip_status(e, "static scratch address");
+    ws_bytes = kAttnStaticScratchBytes;
+  }
   if (p.ws_bytes) {
     if (!al(ws, 16) || ws_bytes < p.ws_bytes)
       return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", p.ws_bytes,
@@ -579,6 +592,11 @@ extern "C" {
 int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, int32_t n_q, float scale,
                        const void *q, void *out, void *ws, size_t ws_bytes, void *stream) {
   return tree_attn_impl(dt, t, kv, nullptr, n_q, scale, q, out, ws, ws_bytes, stream);
+}
+
+int specmemo_tree_attn_noalloc(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv, int32_t n_q,
+                               float scale, const void *q, void *out, void *stream) {
+  return tree_attn_impl(dt, t, kv, nullptr, n_q, scale, q, out, nullptr, 0, stream, true);
 }
 
 int64_t specmemo_key_mask_words(int64_t cap_total) {

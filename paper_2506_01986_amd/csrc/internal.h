@@ -85,6 +85,10 @@ __host__ __device__ constexpr int64_t attn_partial_floats(int rows_per_block) {
   return (int64_t)rows_per_block * (kAttnHeadDim / 2 + 2);
 }
 hipError_t launch_tree_attn_bf16(const AttnArgs &a, int rows_per_block, hipStream_t st);
+// Static scratch of the allocation-free attention entry point: its size, and
+// this device's address of it (looked up once per device, on first use).
+constexpr size_t kAttnStaticScratchBytes = size_t(32) << 20;
+hipError_t attn_static_scratch(void **ptr);
 hipError_t launch_tree_attn_f32(const AttnArgs &a, int node_begin, int node_count, hipStream_t st);
 
 // ---- acceptance ------------------------------------------------------------------

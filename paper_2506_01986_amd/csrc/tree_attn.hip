@@ -24,6 +24,8 @@
 // A sequence with several KV chunks writes per-chunk partials (unnormalised O,
 // running max, running sum) to the workspace, merged in a fixed order by
 // tree_attn_combine (deterministic, no atomics).
+#include <mutex>
+
 #include "device.h"
 #include "internal.h"
 
@@ -625,6 +627,33 @@ hipError_t launch_tree_attn_bf16(const AttnArgs &a, int rows_per_block, hipStrea
   else
     launch_bf16<false>(a, rows_per_block, st);
   return hipGetLastError();
+}
+
+// Scratch of the allocation-free entry point (specmemo_tree_attn_noalloc): the
+// split-KV partial results live in this file-scope device array, of which each
+// device holds its own copy from module load until the process ends.  Host
+// code never uses the array's name as an address: it takes the device address
+// that hipGetSymbolAddress returns, once per device with that device current.
+static __device__ __align__(256) uint8_t scratch[kAttnStaticScratchBytes];
+
+hipError_t attn_static_scratch(void **ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_tree_attn_f32(const AttnArgs &a, int node_begin, int node_count, hipStream_t st) {

@@ -78,6 +78,7 @@ def load():
         lib.specmemo_packed_heads_bytes.argtypes = [i32, i32, i32, i32]
         lib.specmemo_packed_heads_bytes.restype = C.c_size_t
         lib.specmemo_tree_attn.argtypes = [i32, PT, PK, i32, f32, vp, vp, vp, sz, vp]
+        lib.specmemo_tree_attn_noalloc.argtypes = [i32, PT, PK, i32, f32, vp, vp, vp]
         lib.specmemo_accept.argtypes = [i32, PT, i32, i32, f32, f32, f32, vp, vp, vp, vp, i32, vp, vp, sz, vp]
         lib.specmemo_kv_compact.argtypes = [i32, PT, PK, vp, vp, i32, vp]
         lib.specmemo_accept_compact.argtypes = [i32, PT, PK, i32, i32, f32, f32, f32, vp, vp, vp, vp, i32, vp, vp, sz, vp]
@@ -86,7 +87,7 @@ def load():
         lib.specmemo_last_error.restype = C.c_char_p
         lib.specmemo_abi_version.restype = C.c_int32
         for f in ("specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact",
-                  "specmemo_accept_compact"):
+                  "specmemo_accept_compact", "specmemo_tree_attn_noalloc"):
             getattr(lib, f).restype = C.c_int
         i64 = C.c_int64
         u64 = C.c_uint64
@@ -257,6 +258,15 @@ def tree_attn(dt: int, trees: Trees, kv: KVPool, n_q: int, q, out, scale: float 
     ts, ks = trees.struct(), kv.struct()
     _check(load().specmemo_tree_attn(dt, C.byref(ts), C.byref(ks), n_q, scale, _ptr(q), _ptr(out), _ptr(ws),
                                      ws_bytes, _stream(stream)))
+
+
+STATIC_SCRATCH_BYTES = 32 << 20
+
+
+def tree_attn_noalloc(dt: int, trees: Trees, kv: KVPool, n_q: int, q, out, scale: float = 0.0, stream=None):
+    ts, ks = trees.struct(), kv.struct()
+    _check(load().specmemo_tree_attn_noalloc(dt, C.byref(ts), C.byref(ks), n_q, scale, _ptr(q), _ptr(out),
+                                             _stream(stream)))
 
 
 def accept(dt: int, trees: Trees, vocab: int, mode: int, base_logits, node_tok, accept_len, path, path_stride: int,

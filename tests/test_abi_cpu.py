@@ -31,7 +31,7 @@ def test_library_loads_and_exports_every_declared_function():
     assert {"specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert sm.abi_version() == 7
+    assert sm.abi_version() == 8
 
 
 class FakeTrees(sm.Trees):
@@ -274,3 +274,35 @@ def test_fused_acceptance_and_compaction_errors():
     bad.seq_len = FAKE + 2                                                # misaligned device seq_len
     expect("E_ARG", fused, bad)
     expect("E_DTYPE", fused, FakeKV([10, 10], [26, 26], [0, 30], d=64))   # bf16 needs d = 128
+
+
+@cpu_only
+def test_noalloc_attention_checks_and_scratch_limit():
+    """The allocation-free attention call validates like the workspace form,
+    and a split that would need more than the static scratch is rejected
+    before any HIP call (a fixed 64-key chunk over long sequences: the
+    tuning variable is read once per process, so the check runs in a child)."""
+    import os
+    import subprocess
+    import sys
+    bad = synth.Tree(synth.t16().parent.copy(), synth.t16().depth.copy(), synth.t16().rank.copy())
+    bad.parent[5] = 7
+    expect("E_TREE", sm.tree_attn_noalloc, sm.BF16, FakeTrees([bad]), FakeKV([10], [100], [0], d=128), 4, FAKE, FAKE)
+    expect("E_ARG", sm.tree_attn_noalloc, sm.BF16, FakeTrees([synth.t16()]), FakeKV([10], [100], [0]), 3, FAKE, FAKE)
+    expect("E_BUDGET", sm.tree_attn_noalloc, sm.BF16, FakeTrees([synth.t16()]), FakeKV([90], [100], [0]), 4, FAKE,
+           FAKE)
+    child = (
+        "import numpy as np\n"
+        "from tests import test_abi_cpu as t\n"
+        "from paper_2506_01986_amd import specmemo as sm, synth\n"
+        "trees = t.FakeTrees([synth.t64()] * 4)\n"
+        "kv = t.FakeKV([1 << 22] * 4, [(1 << 22) + 64] * 4, [i * ((1 << 22) + 64) for i in range(4)], n_kv=8)\n"
+        "need = sm.workspace_bytes(sm.WS_ATTN, sm.BF16, trees, kv, 64)\n"
+        "assert need > sm.STATIC_SCRATCH_BYTES, need\n"
+        "msg = t.expect('E_WORKSPACE', sm.tree_attn_noalloc, sm.BF16, trees, kv, 64, t.FAKE, t.FAKE)\n"
+        "assert 'static scratch' in msg, msg\n"
+        "print('ok', need)\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", child], cwd=root, capture_output=True, text=True, timeout=120,
+                       env={**os.environ, "SPECMEMO_ATTN_CHUNK": "64", "HIP_VISIBLE_DEVICES": ""})
+    assert r.returncode == 0 and r.stdout.startswith("ok"), r.stdout + r.stderr
