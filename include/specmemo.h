@@ -235,7 +235,7 @@ int specmemo_tree_attn_noalloc(specmemo_dtype dt, const specmemo_trees *t, const
  * node ids root..chosen, -1 padded, path_stride >= max tree depth + 1;
  * next_tok[B] = argmax of the chosen node's row (ties: lower id).
  * ws: SPECMEMO_WS_ACCEPT bytes (greedy: one int32 per node; typical: two
- * floats per node). */
+ * floats and one int32 per node). */
 int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab,
                     specmemo_accept_mode mode, float temperature, float eps, float delta,
                     const void *base_logits, const int32_t *node_tok, int32_t *accept_len,

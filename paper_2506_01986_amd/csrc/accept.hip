@@ -292,26 +292,36 @@ __device__ __forceinline__ float wave_sum(float v) {
   return sum_with_other_half(v);
 }
 
-__device__ __forceinline__ void finish_stats(const AcceptArgs &a, int u, float M, float s, float t, float *red) {
+// Block sums of s and t, then lse and H; the lowest id holding the row's
+// maximum (`cand`: this thread's) is the row's arg-best token, the next token
+// if the row's node ends the accepted path.
+__device__ __forceinline__ void finish_stats(const AcceptArgs &a, int u, float M, float s, float t, uint32_t cand,
+                                             float *red) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   s = wave_sum(s);
   t = wave_sum(t);
+  cand = wave_reduce_u32<false>(cand);
   __syncthreads();   // every wave has read the maximum
   if (lane == 0) {
     red[wave] = s;
     red[kWaves + wave] = t;
+    red[2 * kWaves + wave] = __uint_as_float(cand);
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     float S = 0.f, T = 0.f;
+    uint32_t best = 0xFFFFFFFFu;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
       S += red[w];
       T += red[kWaves + w];
+      const uint32_t c = __float_as_uint(red[2 * kWaves + w]);
+      best = c < best ? c : best;
     }
     const float ln2 = 0.6931471805599453f, l2s = __log2f(S);
     a.stats[2 * (int64_t)u] = (M + l2s) * ln2;
     a.stats[2 * (int64_t)u + 1] = (l2s - T / S) * ln2;
+    a.best[u] = (int)best;
   }
 }
 
@@ -325,7 +335,7 @@ __device__ __forceinline__ void stat_term(float z, float c, float M, float &s, f
 
 template <int DT>
 __global__ __launch_bounds__(kNT) void row_softmax_stats(AcceptArgs a) {
-  __shared__ float red[2 * kWaves];
+  __shared__ float red[3 * kWaves];
   const int u = blockIdx.x, tid = threadIdx.x;
   const int64_t base = (int64_t)u * a.vocab;
   const float c = a.inv_temp * 1.4426950408889634f;   // y = z c
@@ -347,84 +357,105 @@ __global__ __launch_bounds__(kNT) void row_softmax_stats(AcceptArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) mz = fmaxf(mz, fmaxf(__uint_as_float(ws[e] << 16), __uint_as_float(ws[e] & 0xFFFF0000u)));
     }
-    const float M = block_max(mz, red) * c;
+    const float zmax = block_max(mz, red), M = zmax * c;
+    uint32_t cand = 0xFFFFFFFFu;
 #pragma unroll
     for (int k = 0; k < kArgU; ++k) {
       if (k * kNT + tid < nch) {
         const uint32_t ws[4] = {w[k].x, w[k].y, w[k].z, w[k].w};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          stat_term(__uint_as_float(ws[e] << 16), c, M, s, t);
-          stat_term(__uint_as_float(ws[e] & 0xFFFF0000u), c, M, s, t);
+        for (int e = 0; e < 8; ++e) {
+          const float z = __uint_as_float(e & 1 ? ws[e >> 1] & 0xFFFF0000u : ws[e >> 1] << 16);
+          stat_term(z, c, M, s, t);
+          const uint32_t id = 8u * (uint32_t)(k * kNT + tid) + (uint32_t)e;
+          cand = z == zmax && id < cand ? id : cand;   // -0 == +0: the lower id wins
         }
       }
     }
-    finish_stats(a, u, M, s, t, red);
+    finish_stats(a, u, M, s, t, cand, red);
     return;
   }
   // any dtype and vocabulary: two passes over the row
   float mz = -INFINITY;
   for (int v = tid; v < a.vocab; v += kNT) mz = fmaxf(mz, ld<DT>(a.logits, base + v));
-  const float M = block_max(mz, red) * c;
-  for (int v = tid; v < a.vocab; v += kNT) stat_term(ld<DT>(a.logits, base + v), c, M, s, t);
-  finish_stats(a, u, M, s, t, red);
+  const float zmax = block_max(mz, red), M = zmax * c;
+  uint32_t cand = 0xFFFFFFFFu;
+  for (int v = tid; v < a.vocab; v += kNT) {
+    const float z = ld<DT>(a.logits, base + v);
+    stat_term(z, c, M, s, t);
+    cand = z == zmax && (uint32_t)v < cand ? (uint32_t)v : cand;
+  }
+  finish_stats(a, u, M, s, t, cand, red);
 }
 
-// Typical mode, pass 2, by one block: the edges of sequence b's tree, the
-// cumulative acceptance and the path pick; writes accept_len, path and
-// next_tok and returns the accepted length, with the path in s_path for the
+// Typical mode, pass 2, by one block: the edges of sequence b's tree (one
+// thread per node: the edge from its parent), the cumulative acceptance and
+// path score level by level (score[c] = score[parent] + log pi, as the path
+// is walked from the root), and the pick: the deepest accepted node, then the
+// larger score, then the lower id, as one 64-bit key maximum over the nodes.
+// Writes accept_len, path and next_tok (the picked row's arg-best token from
+// pass 1) and returns the accepted length, with the path in s_path for the
 // whole block.
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t o = __shfl_xor(v, off);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
 template <int DT>
 __device__ __forceinline__ int typical_pick(const AcceptArgs &a, int b, int *s_path) {
-  __shared__ float sv[kWaves];
-  __shared__ int si[kWaves];
-  __shared__ float lp[kMaxNodes];
-  __shared__ int pass[kMaxNodes];
-  __shared__ float score[kMaxNodes];
-  __shared__ int ok[kMaxNodes];
-  __shared__ int par[kMaxNodes], dep[kMaxNodes];
-  __shared__ int s_best;
-  const int tid = threadIdx.x;
+  __shared__ float lp[kMaxNodes], score[kMaxNodes];
+  __shared__ int pass[kMaxNodes], ok[kMaxNodes], par[kMaxNodes], dep[kMaxNodes];
+  __shared__ uint64_t s_key[kWaves];
+  static_assert(kNT >= kMaxNodes, "one thread per tree node");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
-  for (int c = tid; c < N; c += kNT) {
-    const int u = a.parent[n0 + c];
-    par[c] = u;
-    dep[c] = a.depth[n0 + c];
-    if (c == 0) continue;
-    const float lse = a.stats[2 * (int64_t)(n0 + u)], H = a.stats[2 * (int64_t)(n0 + u) + 1];
-    const int tok = a.node_tok[n0 + c];
-    const bool valid = tok >= 0 && tok < a.vocab;   // an out-of-range token never passes
-    const float x = valid ? ld<DT>(a.logits, (int64_t)(n0 + u) * a.vocab + tok) * a.inv_temp - lse : -INFINITY;
-    const float thr = fminf(a.log_eps, a.log_delta - H);
-    lp[c] = x;
-    pass[c] = valid && x > thr;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    // parent[c] < c: one pass in node order makes acceptance and path scores cumulative.
-    ok[0] = 1;
-    score[0] = 0.f;
-    int best = 0;
-    for (int c = 1; c < N; ++c) {
-      const int u = par[c];
-      ok[c] = ok[u] && pass[c];
-      score[c] = score[u] + lp[c];
-      if (ok[c]) {
-        const int dc = dep[c], db = dep[best];
-        if (dc > db || (dc == db && score[c] > score[best])) best = c;
-      }
+  int my_dep = 0;
+  if (tid < N) {
+    const int u = a.parent[n0 + tid];
+    par[tid] = u;
+    dep[tid] = my_dep = a.depth[n0 + tid];
+    if (tid == 0) {
+      ok[0] = 1;
+      score[0] = 0.f;
+    } else {
+      const float lse = a.stats[2 * (int64_t)(n0 + u)], H = a.stats[2 * (int64_t)(n0 + u) + 1];
+      const int tok = a.node_tok[n0 + tid];
+      const bool valid = tok >= 0 && tok < a.vocab;   // an out-of-range token never passes
+      const float x = valid ? ld<DT>(a.logits, (int64_t)(n0 + u) * a.vocab + tok) * a.inv_temp - lse : -INFINITY;
+      const float thr = fminf(a.log_eps, a.log_delta - H);
+      lp[tid] = x;
+      pass[tid] = valid && x > thr;
     }
-    s_best = best;
   }
+  // level d: every node at depth d extends its parent's result (parents sit at d - 1)
+  for (int d = 1; __syncthreads_or(tid < N && my_dep >= d); ++d)
+    if (tid < N && my_dep == d) {
+      const int u = par[tid];
+      ok[tid] = ok[u] && pass[tid];
+      score[tid] = score[u] + lp[tid];
+    }
+  // key: depth, then the score's order-preserving bits, then 127 - id (lower ids win)
+  uint64_t key = 0;
+  if (tid < N && ok[tid]) {
+    const uint32_t sb = __float_as_uint(score[tid]);
+    const uint32_t sk = (sb & 0x80000000u) ? ~sb : sb | 0x80000000u;
+    key = (uint64_t)(my_dep + 1) << 40 | (uint64_t)sk << 8 | (uint64_t)(kMaxNodes - 1 - tid);
+  }
+  key = wave_max_u64(key);
+  if (lane == 0) s_key[wave] = key;
   __syncthreads();
-  const int best = s_best;
-  float v;
-  int tok;
-  row_argbest<DT>(a.logits, n0 + best, a.vocab, sv, si, v, tok);
+  key = s_key[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) key = s_key[w] > key ? s_key[w] : key;
+  const int best = kMaxNodes - 1 - (int)(key & 0xFF);
   const int len = dep[best];
   if (tid == 0) {
     a.accept_len[b] = len;
-    a.next_tok[b] = tok;
+    a.next_tok[b] = a.best[n0 + best];
     int32_t *p = a.path + (int64_t)b * a.path_stride;
     for (int j = 0; j < a.path_stride; ++j) p[j] = -1;
     for (int u = best, j = len; u >= 0 && j >= 0; u = par[u], --j) {

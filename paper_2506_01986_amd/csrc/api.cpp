@@ -324,10 +324,11 @@ int accept_args(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, specm
   if (mode == SPECMEMO_ACCEPT_TYPICAL) {
     if (!(temperature > 0.f) || !(eps > 0.f) || !(delta > 0.f) || !std::isfinite(temperature))
       return fail(SPECMEMO_E_ARG, "typical mode needs temperature, eps, delta > 0");
-    const size_t need = (size_t)ti->total * 2 * sizeof(float);
+    const size_t need = (size_t)ti->total * (2 * sizeof(float) + sizeof(int32_t));
     if (!al(ws, 16) || ws_bytes < need)
       return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
     a.stats = static_cast<float *>(ws);
+    a.best = reinterpret_cast<int32_t *>(a.stats + 2 * (size_t)ti->total);
     a.inv_temp = 1.0f / temperature;
     a.log_eps = std::log(eps);
     a.log_delta = std::log(delta);
@@ -382,7 +383,7 @@ size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo
   }
   if (which == SPECMEMO_WS_PAD) return 256;   // the batch's uniform acceptance length
   if (which == SPECMEMO_WS_ACCEPT) {
-    return n_q_or_heads == SPECMEMO_ACCEPT_TYPICAL ? (size_t)ti.total * 2 * sizeof(float)
+    return n_q_or_heads == SPECMEMO_ACCEPT_TYPICAL ? (size_t)ti.total * (2 * sizeof(float) + sizeof(int32_t))
                                                    : (size_t)ti.total * sizeof(int32_t);
   }
   return 0;

@@ -98,7 +98,7 @@ struct AcceptArgs {
   int32_t vocab, mode, path_stride, B;
   float inv_temp, log_eps, log_delta;
   float *stats;            // typical: [sum N][2] (lse, entropy) of z / T
-  int32_t *best;           // greedy: [sum N] arg-best token of each node's row
+  int32_t *best;           // [sum N] arg-best token of each node's row (typical: after stats)
   int32_t *accept_len, *path, *next_tok;
 };
 hipError_t launch_accept(int dt, const AcceptArgs &a, int total_nodes, hipStream_t st);

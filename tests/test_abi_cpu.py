@@ -149,7 +149,7 @@ def test_workspace_errors_and_sizes():
     need = sm.workspace_bytes(sm.WS_TOPK, sm.BF16, t, None, 3, 1000)
     assert need >= 1 * 3 * 1000 * 4                           # the fp32 logits
     expect("E_WORKSPACE", topk, t, ws_bytes=1 * 3 * 1000 * 4 - 4)
-    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.TYPICAL, 0) == 16 * 2 * 4
+    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.TYPICAL, 0) == 16 * (2 * 4 + 4)
     assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.GREEDY, 0) == 16 * 4
     with pytest.raises(sm.SpecmemoError) as e:       # greedy keeps one arg-best token per node
         sm.accept(sm.BF16, t, 1000, sm.GREEDY, FAKE, FAKE, FAKE, FAKE, 4, FAKE, ws=FAKE, ws_bytes=60, stream=0)
@@ -266,7 +266,7 @@ def test_fused_acceptance_and_compaction_errors():
     ok_kv = FakeKV([10, 10], [26, 26], [0, 30])
     assert "path_stride" in expect("E_ARG", fused, ok_kv, stride=2)
     expect("E_WORKSPACE", fused, ok_kv, ws_bytes=4 * 31)                  # one int32 per node: 32 needed
-    expect("E_WORKSPACE", fused, ok_kv, mode=sm.TYPICAL, ws_bytes=4 * 32)  # typical: two floats per node
+    expect("E_WORKSPACE", fused, ok_kv, mode=sm.TYPICAL, ws_bytes=4 * 32)  # typical: two floats and an int per node
     expect("E_ARG", fused, ok_kv, mode=sm.TYPICAL, temperature=-1.0)
     expect("E_BUDGET", fused, FakeKV([10, 10], [25, 26], [0, 30]))       # 10 + 16 > 25
     expect("E_BUDGET", fused, FakeKV([10, 10], [26, 26], [0, 20]))       # slabs overlap

@@ -486,7 +486,7 @@ def test_typical_full_vocab(torch_cuda, dtype):
     lse, H = oracle.softmax_stats(lg, T)
     e_lse, e_H = np.abs(stats[:, 0] - lse).max(), np.abs(stats[:, 1] - H).max()
     say(f"[typical]   max |lse err| {e_lse:.3g}, max |H err| {e_H:.3g}, H in [{H.min():.3f}, {H.max():.3f}]")
-    assert e_lse <= 1e-4 and e_H <= 1e-4
+    assert e_lse <= 2e-5 and e_H <= 2e-5               # fp32 sums over 32000 terms: a few 1e-6
     ra, rp, rn, lp, lt = oracle.accept_typical(lg, tok, node_off, parent, depth, stride, T, eps, delta, edges=True)
     ga, gp, gn = (o.cpu().numpy() for o in out)
     checked = 0
