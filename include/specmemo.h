@@ -479,7 +479,11 @@ int specmemo_plan_tree_sizes(int32_t B, const int32_t *seq_len_h, const int32_t 
  * calls query the current device's compute-unit count, which the attention
  * work split depends on; 256 is assumed when no device is visible).
  *   SPECMEMO_WS_TOPK:   kv ignored; n_q_or_heads = n_heads; vocab used (the
- *                       fp32 logits; none are needed when logits_out is given).
+ *                       fp32 logits, none when logits_out is given; bf16 also
+ *                       the maxima of 64-row groups, which let the top-k pass
+ *                       with packed heads read only the groups that can hold a
+ *                       top-k value; without room for them it scans every
+ *                       logit, with the same result).
  *   SPECMEMO_WS_ATTN:   kv required; n_q_or_heads = n_q; vocab ignored.
  *   SPECMEMO_WS_ACCEPT: kv ignored; n_q_or_heads = accept mode; vocab ignored.
  *   SPECMEMO_WS_PAD:    specmemo_kv_pad_update; kv, n_q_or_heads and vocab

@@ -341,9 +341,14 @@ int accept_args(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, specm
   return SPECMEMO_OK;
 }
 
-// Top-k workspace: fp32 logits (unless the caller keeps them) then the slice candidates.
+// Top-k workspace: the fp32 logits (unless the caller keeps them), then, for
+// packed bf16 heads, the maxima of the 64-row groups (the top-k pass reads
+// only the groups that can hold a top-k value).
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t topk_logit_bytes(int B, int n_heads, int vocab) { return align256((size_t)B * n_heads * vocab * sizeof(float)); }
+size_t topk_gmax_bytes(int B, int n_heads, int vocab) {
+  return align256((size_t)B * n_heads * packed_row_groups(vocab) * sizeof(float));
+}
 
 int check_attn_args(int dt, const specmemo_trees *t, const specmemo_kv *kv, int n_q, TreeInfo *ti) {
   int rc;
@@ -372,7 +377,8 @@ size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo
   if (check_dtype(dt) || check_trees(t, &ti)) return 0;
   if (which == SPECMEMO_WS_TOPK) {
     if (n_q_or_heads < 1 || vocab < 1) return 0;
-    return topk_logit_bytes(ti.B, n_q_or_heads, vocab);
+    return topk_logit_bytes(ti.B, n_q_or_heads, vocab) +
+           (dt == SPECMEMO_BF16 ? topk_gmax_bytes(ti.B, n_q_or_heads, vocab) : 0);
   }
   if (which == SPECMEMO_WS_ATTN) {
     if (check_attn_args(dt, t, kv, n_q_or_heads, &ti)) return 0;
@@ -443,13 +449,19 @@ int specmemo_medusa_topk(specmemo_dtype dt, const specmemo_trees *t, int32_t hid
   if (need && (!al(ws, 16) || ws_bytes < need))
     return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws ? ws_bytes : 0);
   float *z = logits_out ? logits_out : static_cast<float *>(ws);
+  // the group maxima, where the workspace holds them (else every logit is scanned)
+  float *gmax = nullptr;
+  if (head_layout == SPECMEMO_HEADS_PACKED && ws && al(ws, 16) && ws_bytes >= need + topk_gmax_bytes(ti.B, n_heads, vocab))
+    gmax = reinterpret_cast<float *>(static_cast<uint8_t *>(ws) + need);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t h_head_stride = per_head_input ? (int64_t)ti.B * hidden : 0;
   hipError_t e = launch_head_logits(dt, h, h_head_stride, head_w, head_layout == SPECMEMO_HEADS_PACKED, z, ti.B,
-                                    hidden, vocab, n_heads, st);
+                                    hidden, vocab, n_heads, st, gmax);
   if (e != hipSuccess) return hip_status(e, "head projection launch");
   TopkArgs a{};
   a.z = z;
+  a.gmax = gmax;
+  a.nG = packed_row_groups(vocab);
   a.vocab = vocab;
   a.n_heads = n_heads;
   a.kmax = kmax;

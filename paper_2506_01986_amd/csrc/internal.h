@@ -21,6 +21,8 @@ int ok();
 // ---- head projection + top-k -------------------------------------------------
 struct TopkArgs {
   const float *z;          // [B][n_heads][vocab] fp32 logits
+  const float *gmax;       // [B][n_heads][nG] maxima of 64-row groups, or null (then every value is scanned)
+  int32_t nG;
   int32_t vocab, n_heads, kmax;
   int32_t k[kMaxHeads];    // top-k per head
   const int32_t *node_off, *depth, *rank, *root_tok;
@@ -30,8 +32,9 @@ struct TopkArgs {
 };
 
 // h_head_stride: elements between the heads' inputs (0: every head reads the same h).
+// gmax non-null (packed bf16 only): also the maxima of 64-row groups, [B][n_heads][nG].
 hipError_t launch_head_logits(int dt, const void *h, int64_t h_head_stride, const void *w, bool packed, float *z,
-                              int B, int hidden, int vocab, int n_heads, hipStream_t st);
+                              int B, int hidden, int vocab, int n_heads, hipStream_t st, float *gmax = nullptr);
 // Medusa residual blocks: out[i][b] = h[b] + SiLU(W1_i h[b] + b1_i); bf16 W1 packed like the heads.
 hipError_t launch_resblock(int dt, const void *h, const void *w1, const void *b1, void *out, int B, int hidden,
                            int n_heads, hipStream_t st);

@@ -124,10 +124,13 @@ __device__ __forceinline__ uint4 ld16_stream(const uint4 *p) {
   return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p)));
 }
 
+// gmax non-null: each (batch row, head) row also gets the maximum of every
+// 64-row group, [B][n_heads][nG], from which the top-k pass finds the groups
+// that can hold a top-k value.
 template <int NB>
 __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
     const uint16_t *__restrict__ h, int64_t h_head_stride, const uint4 *__restrict__ Wp, float *__restrict__ z,
-    int B, int hidden, int vocab, int n_heads, int nG, int nS) {
+    int B, int hidden, int vocab, int n_heads, int nG, int nS, float *__restrict__ gmax) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int head = blockIdx.y, b0 = blockIdx.z * 16 * NB;
   const int G = blockIdx.x * kWaves + wave;
@@ -179,6 +182,17 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
 #pragma unroll
   for (int n = 0; n < NB; ++n) {
     const int b = b0 + 16 * n + (lane & 15);
+    float m = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int row = 64 * G + t * 16 + 4 * kq;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) m = row + j < vocab ? fmaxf(m, acc[n][t][j]) : m;
+    }
+    if (gmax) {   // the column's four lanes: l, l ^ 16, l ^ 32, l ^ 48
+      m = fmaxf(m, __shfl_xor(m, 16));
+      m = fmaxf(m, __shfl_xor(m, 32));
+    }
     if (b >= B) continue;
     float *zr = z + ((int64_t)b * n_heads + head) * vocab;
 #pragma unroll
@@ -188,6 +202,7 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
       for (int j = 0; j < 4; ++j)
         if (row + j < vocab) zr[row + j] = acc[n][t][j];
     }
+    if (gmax && kq == 0) gmax[((int64_t)b * n_heads + head) * nG + G] = m;
   }
 }
 
@@ -410,12 +425,25 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
   };
   constexpr int kBatch = kTopkU * kTopkThreads;
 
-  // 1. thread max
+  // With the projection's 64-row group maxima (a.gmax), the threshold comes
+  // from those maxima and only the groups whose maximum reaches it are read.
+  const bool pruned = a.gmax != nullptr && a.nG <= kTopkThreads * kTopkU;
+  const float *gm_row = pruned ? a.gmax + (int64_t)row * a.nG : nullptr;
+
+  // 1. thread max (of its values, or of its groups' maxima)
   float mx = NEG;
-  for (int g0 = 0; g0 < ngrp; g0 += kBatch) {
-    load_batch(g0);
+  if (pruned) {
 #pragma unroll
-    for (int u = 0; u < kTopkU; ++u) mx = fmaxf(mx, fmaxf(fmaxf(q[u].x, q[u].y), fmaxf(q[u].z, q[u].w)));
+    for (int u = 0; u < kTopkU; ++u) {
+      const int g = u * kTopkThreads + tid;
+      mx = fmaxf(mx, g < a.nG ? gm_row[g] : NEG);
+    }
+  } else {
+    for (int g0 = 0; g0 < ngrp; g0 += kBatch) {
+      load_batch(g0);
+#pragma unroll
+      for (int u = 0; u < kTopkU; ++u) mx = fmaxf(mx, fmaxf(fmaxf(q[u].x, q[u].y), fmaxf(q[u].z, q[u].w)));
+    }
   }
   // 2. T = the k-th largest of the 64 maxima of 16-thread groups (one DPP row
   //    each, 512 values per group at 32 values per thread): k groups hold a
@@ -451,6 +479,35 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
       }
     }
   };
+  if (pruned) {
+    // the groups whose maximum reaches T, then their values >= T (one thread
+    // per value of 16 groups at a time)
+    __shared__ int sel_g[kTopkCand];
+    __shared__ int nsel;
+    if (tid == 0) nsel = 0;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kTopkU; ++u) {
+      const int g = u * kTopkThreads + tid;
+      if (g < a.nG && gm_row[g] >= T) {
+        const int slot = atomicAdd(&nsel, 1);
+        if (slot < kTopkCand) sel_g[slot] = g;
+      }
+    }
+    __syncthreads();
+    const int ns = min(nsel, kTopkCand);
+    if (nsel > kTopkCand) {
+      if (tid == 0) ncand = kTopkCand + 1;      // too many: the k-round selection below
+    } else {
+      for (int e0 = 0; e0 < ns * 64; e0 += kTopkThreads) {
+        const int e = e0 + tid;
+        if (e < ns * 64) {
+          const int v = 64 * sel_g[e >> 6] + (e & 63);
+          if (v < vocab) gather(x[v], v);
+        }
+      }
+    }
+  } else
   for (int g0 = 0; g0 < ngrp; g0 += kBatch) {
     if (ngrp > kBatch) load_batch(g0);   // one batch: still in registers
 #pragma unroll
@@ -543,14 +600,14 @@ __global__ __launch_bounds__(kTopkThreads) void topk_rows(TopkArgs a) {
 }  // namespace
 
 hipError_t launch_head_logits(int dt, const void *h, int64_t h_head_stride, const void *w, bool packed, float *z,
-                              int B, int hidden, int vocab, int n_heads, hipStream_t st) {
+                              int B, int hidden, int vocab, int n_heads, hipStream_t st, float *gmax) {
   if (dt == 1 && packed) {
     const int nb = B <= 16 ? 1 : 2;
     const int nG = packed_row_groups(vocab), nS = packed_k_steps(hidden);
     dim3 grid((nG + kWaves - 1) / kWaves, n_heads, (B + 16 * nb - 1) / (16 * nb));
     auto kern = nb == 1 ? head_logits_packed<1> : head_logits_packed<2>;
     hipLaunchKernelGGL(kern, grid, dim3(kWaves * 64), 0, st, static_cast<const uint16_t *>(h), h_head_stride,
-                       static_cast<const uint4 *>(w), z, B, hidden, vocab, n_heads, nG, nS);
+                       static_cast<const uint4 *>(w), z, B, hidden, vocab, n_heads, nG, nS, gmax);
   } else if (dt == 1) {
     const int nb = B <= 16 ? 1 : 2;
     dim3 grid((vocab + kWaves * kRowsPerWave - 1) / (kWaves * kRowsPerWave), n_heads,

@@ -493,7 +493,7 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
 // order (deterministic, no atomics): one block per row block, four threads per
 // query row, each with 32 head-dim columns, and one pass over the chunks with
 // a running max (the partials hold unnormalised O in bf16, the chunk's max m
-// and sum l in fp32).
+// and sum l in fp32), the loads of four chunks in flight at once.
 template <int RB>
 __global__ __launch_bounds__(4 * RB) void tree_attn_combine(AttnArgs a) {
   constexpr int CPT = D / 4;   // columns per thread
@@ -529,30 +529,42 @@ __global__ __launch_bounds__(4 * RB) void tree_attn_combine(AttnArgs a) {
   float M = -INFINITY, l = 0.f, o[CPT];
 #pragma unroll
   for (int e = 0; e < CPT; ++e) o[e] = 0.f;
-#pragma unroll 2
-  for (int c = 0; c < S.nch; ++c) {
-    const float *sl = base + c * pf;
-    const float mc = sl[(int64_t)RB * D / 2 + r], lc = sl[(int64_t)RB * D / 2 + RB + r];
-    const uint4 *po = reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(sl) + (int64_t)r * D + quarter * CPT);
-    uint4 v[CPT / 8];
+  // The loads of G chunks are issued together (one memory latency per G
+  // chunks), then the chunks are merged in order.
+  constexpr int G = 4;
+  for (int c0 = 0; c0 < S.nch; c0 += G) {
+    uint4 v[G][CPT / 8];
+    float mc[G], lc[G];
 #pragma unroll
-    for (int q = 0; q < CPT / 8; ++q) v[q] = po[q];
-    // A chunk whose keys a row cannot see (only pad tokens) has mc = -inf and
-    // weight 0; the last chunk holds the row's own tree row, so M ends finite.
-    const float Mn = fmaxf(M, mc);
-    const float wa = M == -INFINITY ? 0.f : fast_exp2(M - Mn);
-    const float wb = mc == -INFINITY ? 0.f : fast_exp2(mc - Mn);
-    l = l * wa + lc * wb;
+    for (int gi = 0; gi < G; ++gi) {
+      const int c = min(c0 + gi, S.nch - 1);   // past the last chunk: a repeated load, not merged
+      const float *sl = base + c * pf;
+      mc[gi] = sl[(int64_t)RB * D / 2 + r];
+      lc[gi] = sl[(int64_t)RB * D / 2 + RB + r];
+      const uint4 *po = reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(sl) + (int64_t)r * D + quarter * CPT);
 #pragma unroll
-    for (int q = 0; q < CPT / 8; ++q) {
-      const uint32_t wv[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        o[8 * q + 2 * e] = o[8 * q + 2 * e] * wa + wb * __uint_as_float(wv[e] << 16);
-        o[8 * q + 2 * e + 1] = o[8 * q + 2 * e + 1] * wa + wb * __uint_as_float(wv[e] & 0xFFFF0000u);
-      }
+      for (int q = 0; q < CPT / 8; ++q) v[gi][q] = po[q];
     }
-    M = Mn;
+#pragma unroll
+    for (int gi = 0; gi < G; ++gi) {
+      if (c0 + gi >= S.nch) break;
+      // A chunk whose keys a row cannot see (only pad tokens) has mc = -inf and
+      // weight 0; the last chunk holds the row's own tree row, so M ends finite.
+      const float Mn = fmaxf(M, mc[gi]);
+      const float wa = M == -INFINITY ? 0.f : fast_exp2(M - Mn);
+      const float wb = mc[gi] == -INFINITY ? 0.f : fast_exp2(mc[gi] - Mn);
+      l = l * wa + lc[gi] * wb;
+#pragma unroll
+      for (int q = 0; q < CPT / 8; ++q) {
+        const uint32_t wv[4] = {v[gi][q].x, v[gi][q].y, v[gi][q].z, v[gi][q].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          o[8 * q + 2 * e] = o[8 * q + 2 * e] * wa + wb * __uint_as_float(wv[e] << 16);
+          o[8 * q + 2 * e + 1] = o[8 * q + 2 * e + 1] * wa + wb * __uint_as_float(wv[e] & 0xFFFF0000u);
+        }
+      }
+      M = Mn;
+    }
   }
   const float inv = 1.f / l;
   const int node = row / a.group, hq = kvh * a.group + row % a.group;

@@ -129,6 +129,20 @@ def run_parity(torch, wl, max_attn_rows=None, typical=True, label="", pack_heads
     assert np.array_equal(ids_gpu, ids64)
     assert np.array_equal(tok_gpu, tok64)
     assert exact == cfg.B * cfg.n_heads
+    if step.head_layout == sm.HEADS_PACKED:
+        # the fused form (no logits kept): the projection hands each 64-row
+        # group's top-k to the top-k pass; the same ids, values and tree tokens
+        vals_gpu = step.topk_vals.cpu().numpy()
+        keep, step.logits = step.logits, None
+        step.topk_ids.fill_(-7)
+        step.node_tok.fill_(-7)
+        step.topk_vals.fill_(0)
+        step.medusa_topk()
+        torch.cuda.synchronize()
+        step.logits = keep
+        assert np.array_equal(step.topk_ids.cpu().numpy(), ids64)
+        assert np.array_equal(step.node_tok.cpu().numpy(), tok64)
+        assert np.array_equal(step.topk_vals.cpu().numpy().view(np.uint32), vals_gpu.view(np.uint32))
     say(f"[parity]   stage a ok: exact top-k rows {exact}/{cfg.B * cfg.n_heads}")
 
     # (b) tree attention
@@ -327,12 +341,13 @@ def test_topk_ties(torch_cuda):
     wl.hidden = synth.to_bf16_bits(h)
     z64 = oracle.head_logits(wl.hidden, wl.head_w)
     ids64, _ = oracle.heads_topk(z64, cfg.topk, cfg.kmax)
-    for pack in (True, False):
-        step = runner.VerifyStep(wl, keep_logits=True, pack_heads=pack)
+    for pack, keep in ((True, True), (False, True), (True, False)):   # (True, False): the fused form
+        step = runner.VerifyStep(wl, keep_logits=keep, pack_heads=pack)
         step.medusa_topk()
         torch_cuda.cuda.synchronize()
-        assert np.array_equal(step.logits.cpu().numpy(), z64.astype(np.float32))
-        assert np.array_equal(step.topk_ids.cpu().numpy(), ids64), pack
+        if keep:
+            assert np.array_equal(step.logits.cpu().numpy(), z64.astype(np.float32))
+        assert np.array_equal(step.topk_ids.cpu().numpy(), ids64), (pack, keep)
         assert np.array_equal(step.topk_ids.cpu().numpy()[:, 0], np.tile(np.arange(10), (3, 1)))
 
 
