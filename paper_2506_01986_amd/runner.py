@@ -81,11 +81,14 @@ class VerifyStep:
             pos = [int(kv_flags[int(wl.seq_base[b]):int(wl.seq_base[b]) + int(wl.lens[b])].sum()) for b in range(B)]
             self.pos = torch.tensor(pos, dtype=torch.int32, device=device)
         ws = max(sm.workspace_bytes(sm.WS_TOPK, self.dt, self.trees, None, nh, cfg.vocab),
-                 sm.workspace_bytes(sm.WS_ATTN, self.dt, self.trees, self.kv, cfg.n_q),
-                 sm.workspace_bytes(sm.WS_ACCEPT, self.dt, self.trees, None, mode),
+                 sm.workspace_bytes(sm.WS_ACCEPT, self.dt, self.trees, None, sm.TYPICAL),
                  sm.workspace_bytes(sm.WS_PAD, self.dt, self.trees, None, 0) if key_valid is not None else 0)
         self.ws_bytes = ws
         self.ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=device)
+        # the attention has a workspace of its own: it may run concurrently with the projection
+        self.ws_attn_bytes = max(sm.workspace_bytes(sm.WS_ATTN, self.dt, self.trees, self.kv, cfg.n_q), 16)
+        self.ws_attn = torch.empty(self.ws_attn_bytes, dtype=torch.uint8, device=device)
+        self.side_box = [None]    # the second stream of run_overlapped, shared with replicas
 
     def replica(self) -> "VerifyStep":
         """Another step over the same workload that shares the head weights,
@@ -95,7 +98,7 @@ class VerifyStep:
         import copy
         r = copy.copy(self)
         for name in ("q", "k", "v", "seq_len", "out", "topk_ids", "topk_vals", "node_tok", "accept_len", "path",
-                     "next_tok", "ws", "base_logits", "logits", "key_valid", "pos"):
+                     "next_tok", "ws", "ws_attn", "base_logits", "logits", "key_valid", "pos"):
             t = getattr(self, name)
             if t is not None:
                 setattr(r, name, t.clone())
@@ -104,7 +107,7 @@ class VerifyStep:
 
     def step_bytes(self) -> int:
         """Device bytes a replica owns (what one step touches besides the heads)."""
-        ts = (self.q, self.k, self.v, self.out, self.base_logits, self.ws, self.topk_ids, self.node_tok)
+        ts = (self.q, self.k, self.v, self.out, self.base_logits, self.ws, self.ws_attn, self.topk_ids, self.node_tok)
         return int(sum(t.numel() * t.element_size() for t in ts if t is not None))
 
     def set_base_logits(self, stored: np.ndarray):
@@ -119,8 +122,8 @@ class VerifyStep:
                        head_layout=self.head_layout)
 
     def tree_attn(self, stream=None):
-        sm.tree_attn(self.dt, self.trees, self.kv, self.cfg.n_q, self.q, self.out, ws=self.ws,
-                     ws_bytes=self.ws_bytes, stream=stream)
+        sm.tree_attn(self.dt, self.trees, self.kv, self.cfg.n_q, self.q, self.out, ws=self.ws_attn,
+                     ws_bytes=self.ws_attn_bytes, stream=stream)
 
     def accept(self, stream=None):
         sm.accept(self.dt, self.trees, self.cfg.vocab, self.mode, self.base_logits, self.node_tok,
@@ -144,8 +147,8 @@ class VerifyStep:
         self.seq_len.copy_(torch.from_numpy(self.wl.lens.copy()))
 
     def tree_attn_padded(self, stream=None):
-        sm.tree_attn_padded(self.dt, self.trees, self.kv, self.key_valid, self.cfg.n_q, self.q, self.out, ws=self.ws,
-                            ws_bytes=self.ws_bytes, stream=stream)
+        sm.tree_attn_padded(self.dt, self.trees, self.kv, self.key_valid, self.cfg.n_q, self.q, self.out,
+                            ws=self.ws_attn, ws_bytes=self.ws_attn_bytes, stream=stream)
 
     def kv_pad_update(self, stream=None):
         sm.kv_pad_update(self.dt, self.trees, self.kv, self.accept_len, self.path, self.path_stride, self.key_valid,
@@ -162,6 +165,25 @@ class VerifyStep:
         self.medusa_topk(stream)
         self.tree_attn(stream)
         self.accept_compact(stream)
+
+    def run_overlapped(self):
+        """The fused step with the attention on a second stream, concurrent
+        with the head projection and top-k.  The two stages share no data: the
+        attention reads queries and K/V, the projection hidden states and head
+        weights.  The side stream first waits for the main stream (the
+        previous step's compaction rewrites K/V rows the attention reads), and
+        the main stream waits for the attention before the acceptance and
+        compaction.  Both streams have the default priority."""
+        main = torch.cuda.current_stream(self.device)
+        if self.side_box[0] is None:
+            self.side_box[0] = torch.cuda.Stream(device=self.device)
+        side = self.side_box[0]
+        side.wait_stream(main)
+        with torch.cuda.stream(side):
+            self.tree_attn()
+        self.medusa_topk()
+        main.wait_stream(side)
+        self.accept_compact()
 
     def run_padded(self, stream=None):
         """The step of the padded-batching variant: pad tokens masked in

@@ -575,7 +575,7 @@ def test_greedy_argbest_rows(torch_cuda, vocab):
         assert np.array_equal(acc.cpu().numpy(), ra) and np.array_equal(path.cpu().numpy(), rp)
 
 
-@pytest.mark.parametrize("fused", [False, True], ids=["four_calls", "accept_compact"])
+@pytest.mark.parametrize("fused", [False, True, "overlapped"], ids=["four_calls", "accept_compact", "overlapped"])
 def test_graph_replay(torch_cuda, fused):
     """The calls of a step (four, or three with acceptance and compaction
     fused) captured in one HIP graph.  Every replay, with eager work between
@@ -605,11 +605,18 @@ def test_graph_replay(torch_cuda, fused):
             t.fill_(-7)
         step.out.zero_()
 
-    run = step.run_fused if fused else step.run
+    run = step.run_overlapped if fused == "overlapped" else step.run_fused if fused else step.run
     restore_and_poison()
-    run()
+    step.run_fused() if fused == "overlapped" else run()    # the overlapped step must equal the serial one
     torch.cuda.synchronize()
     ref = [t.clone() for t in outs]
+    if fused == "overlapped":
+        for r in range(3):
+            restore_and_poison()
+            run()
+            torch.cuda.synchronize()
+            for i, (a, b) in enumerate(zip(ref, outs)):
+                assert torch.equal(a.contiguous().view(torch.uint8), b.contiguous().view(torch.uint8)), ("eager", r, i)
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         run()
