@@ -195,7 +195,10 @@ size_t specmemo_packed_heads_bytes(specmemo_dtype dt, int32_t n_heads, int32_t v
  * rows (else SPECMEMO_E_BUDGET); fp32 requires
  * head_dim <= 128 and head_dim % 4 == 0.  n_q % n_kv == 0.  Rows of the slab
  * past L_b + N_b are never read.  ws: at least
- * specmemo_workspace_bytes(SPECMEMO_WS_ATTN, ...) bytes (may be 0). */
+ * specmemo_workspace_bytes(SPECMEMO_WS_ATTN, ...) bytes (the partial results
+ * of KV ranges split across work items; with more than 32 sequences also the
+ * per-sequence descriptors and the work map of the single launch, written
+ * into ws by the call's own kernels; may be 0). */
 int specmemo_tree_attn(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv *kv,
                        int32_t n_q, float scale, const void *q, void *out, void *ws,
                        size_t ws_bytes, void *stream);
@@ -485,7 +488,9 @@ int specmemo_plan_tree_sizes(int32_t B, const int32_t *seq_len_h, const int32_t 
  *                       top-k value; without room for them it scans every
  *                       logit, with the same result).
  *   SPECMEMO_WS_ATTN:   kv required; n_q_or_heads = n_q; vocab ignored.
- *   SPECMEMO_WS_ACCEPT: kv ignored; n_q_or_heads = accept mode; vocab ignored.
+ *   SPECMEMO_WS_ACCEPT: kv ignored; n_q_or_heads = accept mode; vocab ignored
+ *                       (with more than 32 sequences it includes the
+ *                       compaction descriptors of specmemo_accept_compact).
  *   SPECMEMO_WS_PAD:    specmemo_kv_pad_update; kv, n_q_or_heads and vocab
  *                       ignored.
  * Returns 0 for invalid arguments as well as when no workspace is needed;

@@ -14,7 +14,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "_build")
 LIB = os.path.join(OUT, "libspecmemo.so")
-SOURCES = ["api.cpp", "budget.cpp", "medusa_topk.hip", "tree_attn.hip", "accept.hip", "kv_compact.hip"]
+SOURCES = ["api.cpp", "budget.cpp", "medusa_topk.hip", "tree_attn.hip", "accept.hip", "kv_compact.hip",
+           "upload.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

@@ -259,7 +259,7 @@ __global__ __launch_bounds__(64) void accept_walk_compact(AcceptArgs a, CompactA
   int src[kMaxPath];
 #pragma unroll
   for (int j = 0; j < kMaxPath; ++j) src[j] = __builtin_amdgcn_readlane(p_mine, j);
-  const CompactSeq S = c.seq[s];
+  const CompactSeq S = c.tab ? c.tab[s] : c.seq[s];
   move_rows(c, S, kvh, which, len, src, threadIdx.x, 64);
   if (writer && threadIdx.x == 0) c.seq_len[b] = S.L + len + 1;
 }
@@ -485,7 +485,7 @@ __global__ __launch_bounds__(kNT) void accept_typical_compact(AcceptArgs a, Comp
   int src[kMaxPath];
 #pragma unroll
   for (int j = 0; j < kMaxPath; ++j) src[j] = j <= len ? s_path[j] : -1;
-  const CompactSeq S = c.seq[s];
+  const CompactSeq S = c.tab ? c.tab[s] : c.seq[s];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (int p = wave; p < 2 * c.n_kv; p += kWaves) move_rows(c, S, p >> 1, p & 1, len, src, lane, 64);
   if (threadIdx.x == 0) c.seq_len[b] = S.L + len + 1;

@@ -151,6 +151,11 @@ struct AttnPlan {
   std::vector<std::vector<int>> xcd_cum;      // per launch: [8][nseq + 1]
   std::vector<std::vector<int>> xcd_ccum;     // per launch: [8][nseq + 1], combine blocks
   size_t ws_bytes = 0;
+  // Table mode (more sequences than kernel arguments hold): one launch, the
+  // descriptors and every block's item in the workspace at these offsets.
+  bool table = false;
+  std::vector<AttnItem> map, cmap;
+  size_t map_off = 0, cmap_off = 0, part_off = 0;
 };
 
 // Compute units of the current device (256 on MI355X; also the fallback when no
@@ -217,6 +222,76 @@ void attn_chunks(std::vector<AttnSeq> &grp, int n_kv, int slots) {
   }
 }
 
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Table mode: the item of every attention and combine block, decoded on the
+// host in the order the kernels' own decoding uses (XCD order: block 8 k + x
+// is the k-th block of XCD x; otherwise launch order), padding blocks marked
+// with sequence 0xFFFF.
+void attn_table_maps(const std::vector<AttnSeq> &grp, const std::vector<int> &cum, const std::vector<int> &ccum,
+                     bool xcd_order, int items, int citems, std::vector<AttnItem> *map, std::vector<AttnItem> *cmap) {
+  const int ns = (int)grp.size();
+  // largest s with c[x][s] <= k (c non-decreasing in s)
+  auto last_le = [&](const std::vector<int> &c, int x, int k) {
+    int s = 0;
+    for (int lo = 0, hi = ns - 1; lo <= hi;) {
+      const int mid = (lo + hi) / 2;
+      if (c[x * (ns + 1) + mid] <= k) s = mid, lo = mid + 1;
+      else hi = mid - 1;
+    }
+    return s;
+  };
+  const AttnItem pad{0xFFFF, 0, 0, 0};
+  map->assign(items, pad);
+  for (int bid = 0; bid < items; ++bid) {
+    int s, kvh, ch, rb;
+    if (xcd_order) {
+      const int x = bid & 7, k = bid >> 3;
+      if (k >= cum[x * (ns + 1) + ns]) continue;
+      s = last_le(cum, x, k);
+      const AttnSeq &S = grp[s];
+      const int kk = k - cum[x * (ns + 1) + s], per_unit = S.nch * S.nrb;
+      kvh = ((x - (S.unit0 & 7)) & 7) + 8 * (kk / per_unit);
+      const int local = kk % per_unit;
+      ch = local / S.nrb;
+      rb = local % S.nrb;
+    } else {
+      s = 0;
+      while (s + 1 < ns && grp[s + 1].item0 <= bid) ++s;
+      const AttnSeq &S = grp[s];
+      int local = bid - S.item0;
+      rb = local % S.nrb;
+      local /= S.nrb;
+      ch = local % S.nch;
+      kvh = local / S.nch;
+    }
+    (*map)[bid] = AttnItem{(uint16_t)s, (uint16_t)kvh, (uint16_t)ch, (uint16_t)rb};
+  }
+  cmap->assign(citems, pad);
+  for (int idx = 0; idx < citems; ++idx) {
+    int s, kvh, rb;
+    if (xcd_order) {
+      const int x = idx & 7, k = idx >> 3;
+      if (k >= ccum[x * (ns + 1) + ns]) continue;
+      s = last_le(ccum, x, k);
+      const AttnSeq &S = grp[s];
+      const int kk = k - ccum[x * (ns + 1) + s];
+      kvh = ((x - (S.unit0 & 7)) & 7) + 8 * (kk / S.nrb);
+      rb = kk % S.nrb;
+    } else {
+      s = -1;
+      for (int i = 0; i < ns; ++i)
+        if (grp[i].nch > 1 && grp[i].citem0 <= idx) s = i;
+      if (s < 0) continue;
+      const AttnSeq &S = grp[s];
+      const int local = idx - S.citem0;
+      kvh = local / S.nrb;
+      rb = local % S.nrb;
+    }
+    (*cmap)[idx] = AttnItem{(uint16_t)s, (uint16_t)kvh, 0, (uint16_t)rb};
+  }
+}
+
 void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *kv, int n_q, AttnPlan *p) {
   const int g = n_q / kv->n_kv;
   const int max_rows = ti.max_nodes * g;
@@ -231,9 +306,11 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
   std::iota(order.begin(), order.end(), 0);
   std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return kv->seq_len_h[x] > kv->seq_len_h[y]; });
   const int64_t pf = attn_partial_floats(RB);
-  for (size_t i0 = 0; i0 < order.size(); i0 += kMaxSeqPerLaunch) {
+  p->table = ti.B > kMaxSeqPerLaunch;
+  const size_t per_launch = p->table ? order.size() : (size_t)kMaxSeqPerLaunch;
+  for (size_t i0 = 0; i0 < order.size(); i0 += per_launch) {
     std::vector<AttnSeq> grp;
-    for (size_t i = i0; i < std::min(order.size(), i0 + kMaxSeqPerLaunch); ++i) {
+    for (size_t i = i0; i < std::min(order.size(), i0 + per_launch); ++i) {
       const int b = order[i];
       AttnSeq s{};
       s.base = kv->seq_base_h[b];
@@ -289,9 +366,25 @@ void plan_attn(const TreeInfo &ti, const specmemo_trees *t, const specmemo_kv *k
     // busiest XCD's blocks, surplus blocks exit at once.
     p->items.push_back(p->xcd_order ? 8 * *std::max_element(per_xcd, per_xcd + 8) : item);
     p->citems.push_back(p->xcd_order ? 8 * *std::max_element(cper_xcd, cper_xcd + 8) : citem);
-    p->ws_bytes = std::max(p->ws_bytes, (size_t)part * (size_t)pf * sizeof(float));
+    if (p->table) {
+      attn_table_maps(grp, cum, ccum, p->xcd_order, p->items.back(), p->citems.back(), &p->map, &p->cmap);
+      p->map_off = align256(grp.size() * sizeof(AttnSeq));
+      p->cmap_off = p->map_off + align256(p->map.size() * sizeof(AttnItem));
+      p->part_off = p->cmap_off + align256(p->cmap.size() * sizeof(AttnItem));
+    }
+    p->ws_bytes = std::max(p->ws_bytes, p->part_off + (size_t)part * (size_t)pf * sizeof(float));
   }
 }
+
+// Workspace of the acceptance: greedy one int32 per node; typical two floats
+// and one int32 per node (aligned to 256 bytes for what follows it).
+size_t accept_ws_bytes(const TreeInfo &ti, int mode) {
+  return align256(mode == SPECMEMO_ACCEPT_TYPICAL ? (size_t)ti.total * (2 * sizeof(float) + sizeof(int32_t))
+                                                  : (size_t)ti.total * sizeof(int32_t));
+}
+// The fused acceptance and compaction of more than kMaxSeqPerLaunch
+// sequences keeps their compaction descriptors after the acceptance's part.
+size_t compact_table_bytes(int B) { return B > kMaxSeqPerLaunch ? align256((size_t)B * sizeof(CompactSeq)) : 0; }
 
 // Validation and kernel arguments of the acceptance (nothing is launched).
 int accept_args(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, specmemo_accept_mode mode, float temperature,
@@ -344,7 +437,6 @@ int accept_args(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, specm
 // Top-k workspace: the fp32 logits (unless the caller keeps them), then, for
 // packed bf16 heads, the maxima of the 64-row groups (the top-k pass reads
 // only the groups that can hold a top-k value).
-size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t topk_logit_bytes(int B, int n_heads, int vocab) { return align256((size_t)B * n_heads * vocab * sizeof(float)); }
 size_t topk_gmax_bytes(int B, int n_heads, int vocab) {
   return align256((size_t)B * n_heads * packed_row_groups(vocab) * sizeof(float));
@@ -388,10 +480,7 @@ size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo
     return p.ws_bytes;
   }
   if (which == SPECMEMO_WS_PAD) return 256;   // the batch's uniform acceptance length
-  if (which == SPECMEMO_WS_ACCEPT) {
-    return n_q_or_heads == SPECMEMO_ACCEPT_TYPICAL ? (size_t)ti.total * (2 * sizeof(float) + sizeof(int32_t))
-                                                   : (size_t)ti.total * sizeof(int32_t);
-  }
+  if (which == SPECMEMO_WS_ACCEPT) return accept_ws_bytes(ti, n_q_or_heads) + compact_table_bytes(ti.B);
   return 0;
 }
 
@@ -581,17 +670,30 @@ int tree_attn_impl(specmemo_dtype dt, const specmemo_trees *t, const specmemo_kv
                   ws ? ws_bytes : 0);
   }
   a.part = static_cast<float *>(ws);
+  if (p.table) {   // one launch: descriptors and block maps go to the workspace first
+    uint8_t *w = static_cast<uint8_t *>(ws);
+    hipError_t e = upload_table(p.groups[0].data(), p.groups[0].size() * sizeof(AttnSeq), w, st);
+    if (e == hipSuccess) e = upload_table(p.map.data(), p.map.size() * sizeof(AttnItem), w + p.map_off, st);
+    if (e == hipSuccess) e = upload_table(p.cmap.data(), p.cmap.size() * sizeof(AttnItem), w + p.cmap_off, st);
+    if (e != hipSuccess) return hip_status(e, "descriptor upload");
+    a.tab = reinterpret_cast<const AttnSeq *>(w);
+    a.map = reinterpret_cast<const AttnItem *>(w + p.map_off);
+    a.cmap = reinterpret_cast<const AttnItem *>(w + p.cmap_off);
+    a.part = reinterpret_cast<float *>(w + p.part_off);
+  }
   for (size_t gi = 0; gi < p.groups.size(); ++gi) {
     a.nseq = (int)p.groups[gi].size();
-    for (int i = 0; i < a.nseq; ++i) a.seq[i] = p.groups[gi][i];
+    if (!p.table)
+      for (int i = 0; i < a.nseq; ++i) a.seq[i] = p.groups[gi][i];
     a.items = p.items[gi];
     a.citems = p.citems[gi];
     a.xcd_order = p.xcd_order ? 1 : 0;
-    for (int x = 0; x < 8; ++x)
-      for (int i = 0; i <= a.nseq; ++i) {
-        a.xcd_cum[x][i] = p.xcd_cum[gi][x * (a.nseq + 1) + i];
-        a.xcd_ccum[x][i] = p.xcd_ccum[gi][x * (a.nseq + 1) + i];
-      }
+    if (!p.table)
+      for (int x = 0; x < 8; ++x)
+        for (int i = 0; i <= a.nseq; ++i) {
+          a.xcd_cum[x][i] = p.xcd_cum[gi][x * (a.nseq + 1) + i];
+          a.xcd_ccum[x][i] = p.xcd_ccum[gi][x * (a.nseq + 1) + i];
+        }
     hipError_t e = launch_tree_attn_bf16(a, p.rb, st);
     if (e != hipSuccess) return hip_status(e, "tree attention launch");
   }
@@ -772,9 +874,30 @@ int specmemo_accept_compact(specmemo_dtype dt, const specmemo_trees *t, const sp
                        path_stride, next_tok, ws, ws_bytes, &ti, &a);
   if (rc) return rc;
   if ((rc = compact_args(dt, t, kv, accept_len, path, path_stride, ti, &c))) return rc;
+  // more sequences than kernel arguments hold: their descriptors go to the
+  // workspace, after the acceptance's part, and one launch covers the batch
+  const bool table = ti.B > kMaxSeqPerLaunch;
+  const size_t acc_bytes = accept_ws_bytes(ti, mode);
+  if (table && ws_bytes < acc_bytes + compact_table_bytes(ti.B))
+    return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu",
+                acc_bytes + compact_table_bytes(ti.B), ws_bytes);
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = launch_accept_rows(dt, a, ti.total, st);
   if (e != hipSuccess) return hip_status(e, "acceptance launch");
+  if (table) {
+    std::vector<CompactSeq> tab(ti.B);
+    for (int b = 0; b < ti.B; ++b)
+      tab[b] = CompactSeq{kv->seq_base_h[b], kv->seq_len_h[b], t->node_off_h[b + 1] - t->node_off_h[b],
+                          kv->seq_cap_h[b], t->node_off_h[b]};
+    uint8_t *w = static_cast<uint8_t *>(ws) + acc_bytes;
+    if ((e = upload_table(tab.data(), tab.size() * sizeof(CompactSeq), w, st)) != hipSuccess)
+      return hip_status(e, "descriptor upload");
+    c.tab = reinterpret_cast<const CompactSeq *>(w);
+    c.nseq = ti.B;
+    c.b0 = 0;
+    if ((e = launch_accept_compact(dt, a, c, st)) != hipSuccess) return hip_status(e, "acceptance and compaction launch");
+    return ok();
+  }
   for (int b0 = 0; b0 < ti.B; b0 += kMaxSeqPerLaunch) {
     compact_group(t, kv, b0, ti.B, &c);
     if ((e = launch_accept_compact(dt, a, c, st)) != hipSuccess) return hip_status(e, "acceptance and compaction launch");

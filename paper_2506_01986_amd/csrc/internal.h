@@ -13,6 +13,12 @@ constexpr int kMaxPath = 16;           // max depth + 1
 constexpr int kMaxTopk = 32;
 constexpr int kMaxHeads = 15;
 
+// Host tables written into device memory by kernels whose arguments carry up
+// to kUploadWords words each (csrc/upload.hip); bytes may be any size, dst
+// 4-byte aligned.
+constexpr int kUploadWords = 1000;
+hipError_t upload_table(const void *src, size_t bytes, void *dst, hipStream_t st);
+
 // Error reporting of the C ABI: `fail` records the message that
 // specmemo_last_error returns and passes `code` through; `ok` clears it.
 int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
@@ -59,6 +65,10 @@ struct AttnSeq {
   int32_t unit0;     // first (sequence, KV head) unit of this sequence in the launch
 };
 
+struct AttnItem {
+  uint16_t s, kvh, ch, rb;
+};
+
 struct AttnArgs {
   const void *q;
   void *out;
@@ -66,6 +76,12 @@ struct AttnArgs {
   const int32_t *parent;
   const uint32_t *key_valid;   // padded batching: bit r of the pool's row r, 0 = pad token; null: no pads
   float *part;             // partial results workspace
+  // Table mode (more than kMaxSeqPerLaunch sequences): the descriptors of all
+  // the launch's sequences and the decoded item of every block live in the
+  // workspace (written by upload_table before the launch); null otherwise.
+  const AttnSeq *tab;
+  const AttnItem *map;     // attention blocks: sequence, KV head, chunk, row block (seq 0xFFFF: padding)
+  const AttnItem *cmap;    // combine blocks: sequence, KV head, row block
   int64_t cap_total;
   int32_t n_q, n_kv, group, head_dim;
   float scale_log2;        // scale * log2(e)
@@ -121,6 +137,7 @@ struct CompactSeq {
   int32_t L, N, cap, node0;   // node0: global id of the root node
 };
 struct CompactArgs {
+  const CompactSeq *tab;   // table mode: all sequences' descriptors in device memory (seq[] unused)
   void *k, *v;
   int64_t cap_total;
   int32_t n_kv, row_dwords, path_stride, nseq, b0;

@@ -85,6 +85,16 @@ __device__ __forceinline__ AttnSeq pick_seq(const AttnSeq &d, int s) {
 // the number of XCD x's blocks before sequence s; blocks past the busiest
 // XCD's work are padding.
 __device__ __forceinline__ bool decode_item(const AttnArgs &a, int bid, Item &it, AttnSeq &S) {
+  if (a.map) {   // table mode: the host decoded every block's item (same order as below)
+    const AttnItem m = a.map[bid];
+    if (m.s == 0xFFFF) return false;
+    it.s = m.s;
+    it.kvh = m.kvh;
+    it.ch = m.ch;
+    it.rb = m.rb;
+    S = a.tab[m.s];
+    return true;
+  }
   const int lane = threadIdx.x & 63;
   const int x = bid & 7, k = bid >> 3;
   AttnSeq mine{};
@@ -499,12 +509,18 @@ __global__ __launch_bounds__(4 * RB) void tree_attn_combine(AttnArgs a) {
   constexpr int CPT = D / 4;   // columns per thread
   const int idx = blockIdx.x, lane = threadIdx.x & 63;
   const int x = idx & 7, k = idx >> 3;
-  AttnSeq mine{};
-  if (lane < kMaxSeqPerLaunch) mine = a.seq[lane];
-  const int ccum = lane <= kMaxSeqPerLaunch ? a.xcd_ccum[x][lane] : 0;
   int kvh, rb;
   AttnSeq S;
-  if (a.xcd_order) {
+  AttnSeq mine{};
+  if (!a.cmap && lane < kMaxSeqPerLaunch) mine = a.seq[lane];
+  const int ccum = !a.cmap && lane <= kMaxSeqPerLaunch ? a.xcd_ccum[x][lane] : 0;
+  if (a.cmap) {   // table mode: the host decoded every block's row block
+    const AttnItem m = a.cmap[idx];
+    if (m.s == 0xFFFF) return;
+    S = a.tab[m.s];
+    kvh = m.kvh;
+    rb = m.rb;
+  } else if (a.xcd_order) {
     // the k-th combine item of XCD x, on the XCD that computed its chunks
     if (k >= rl(ccum, a.nseq)) return;   // padding block
     const int s = find_seq(a.nseq, ccum, k);

@@ -149,8 +149,13 @@ def test_workspace_errors_and_sizes():
     need = sm.workspace_bytes(sm.WS_TOPK, sm.BF16, t, None, 3, 1000)
     assert need >= 1 * 3 * 1000 * 4                           # the fp32 logits
     expect("E_WORKSPACE", topk, t, ws_bytes=1 * 3 * 1000 * 4 - 4)
-    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.TYPICAL, 0) == 16 * (2 * 4 + 4)
-    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.GREEDY, 0) == 16 * 4
+    # typical: two floats and an int per node; greedy: one int per node (256-byte granules)
+    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.TYPICAL, 0) == 256 >= 16 * (2 * 4 + 4)
+    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, t, None, sm.GREEDY, 0) == 256 >= 16 * 4
+    # more than 32 sequences: the fused acceptance and compaction keeps their descriptors too
+    many = FakeTrees([synth.t16()] * 40)
+    assert sm.workspace_bytes(sm.WS_ACCEPT, sm.BF16, many, None, sm.GREEDY, 0) == \
+        -(-(40 * 16 * 4) // 256) * 256 + -(-(40 * 24) // 256) * 256
     with pytest.raises(sm.SpecmemoError) as e:       # greedy keeps one arg-best token per node
         sm.accept(sm.BF16, t, 1000, sm.GREEDY, FAKE, FAKE, FAKE, FAKE, 4, FAKE, ws=FAKE, ws_bytes=60, stream=0)
     assert e.value.name == "E_WORKSPACE"

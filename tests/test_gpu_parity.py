@@ -255,7 +255,7 @@ EDGES = {
     "mha_b17": (edge_cfg(B=17, n_q=2, n_kv=2, hidden=64, vocab=520),
                 lambda r: [synth.random_tree(r, int(r.integers(1, 65))) for _ in range(17)],
                 list(range(0, 17 * 70, 70))),
-    # more than 32 sequences: several launch groups
+    # more than 32 sequences: one launch with the descriptors in the workspace
     "b40": (edge_cfg(B=40, n_q=4, n_kv=2, hidden=32, vocab=256, topk=(4, 3, 2, 2)),
             lambda r: [synth.random_tree(r, int(r.integers(1, 20)), max_kids=2) for _ in range(40)],
             [int(x) for x in np.random.default_rng(5).integers(0, 300, 40)]),
@@ -276,7 +276,11 @@ EDGES = {
     # multi-query attention: 64 query heads on one KV head, 8192 query rows per sequence
     "mqa64": (edge_cfg(B=2, n_q=64, n_kv=1, hidden=64, vocab=300),
               lambda r: [synth.random_tree(r, 128), synth.t16()], [300, 2000]),
-    # the largest batch (4096 sequences: 128 launch groups per stage), the smallest hidden size
+    # more than 32 sequences, some long enough to split: one launch (descriptor table in the workspace)
+    "b36_split": (edge_cfg(B=36, n_q=8, n_kv=2, hidden=32, vocab=256),
+                  lambda r: [synth.random_tree(r, int(r.integers(1, 65))) for _ in range(36)],
+                  [5000, 3000] + [int(x) for x in np.random.default_rng(7).integers(0, 1500, 34)]),
+    # the largest batch (4096 sequences, one launch per stage), the smallest hidden size
     "b4096": (edge_cfg(B=4096, n_q=1, n_kv=1, hidden=8, vocab=16, n_heads=1, topk=(4,)),
               lambda r: [synth.random_tree(r, int(r.integers(1, 6)), max_depth=1, max_kids=4) for _ in range(4096)],
               [int(x) for x in np.random.default_rng(6).integers(0, 31, 4096)]),
@@ -648,11 +652,13 @@ def test_run_to_run_determinism(torch_cuda):
                            b.view(torch.uint8) if b.dtype != torch.int32 else b)
 
 
-@pytest.mark.parametrize("env", [{"SPECMEMO_ATTN_ROWS": "64"}, {"SPECMEMO_ATTN_ROWS": "256"},
-                                 {"SPECMEMO_ATTN_XCD": "0"}, {"SPECMEMO_ATTN_CHUNK": "256"},
-                                 {"SPECMEMO_ATTN_CHUNK": "0"}],
-                         ids=["rows64", "rows256", "no_xcd_order", "chunk256", "no_split"])
-def test_attention_tuning_overrides(torch_cuda, env):
+@pytest.mark.parametrize("env,many", [({"SPECMEMO_ATTN_ROWS": "64"}, False), ({"SPECMEMO_ATTN_ROWS": "256"}, False),
+                                      ({"SPECMEMO_ATTN_XCD": "0"}, False), ({"SPECMEMO_ATTN_CHUNK": "256"}, False),
+                                      ({"SPECMEMO_ATTN_CHUNK": "0"}, False), ({}, True),
+                                      ({"SPECMEMO_ATTN_XCD": "0"}, True), ({"SPECMEMO_ATTN_CHUNK": "256"}, True)],
+                         ids=["rows64", "rows256", "no_xcd_order", "chunk256", "no_split", "b40_table",
+                              "b40_table_no_xcd_order", "b40_table_chunk256"])
+def test_attention_tuning_overrides(torch_cuda, env, many):
     """The attention's tuning variables (read once per process) change the
     work split, not the result: each runs in a child process of its own,
     one after the other, against the oracle."""
@@ -661,7 +667,7 @@ def test_attention_tuning_overrides(torch_cuda, env):
     import sys
     child = os.path.join(os.path.dirname(os.path.abspath(__file__)), "attn_override_check.py")
     say(f"[override] {env}")
-    r = subprocess.run([sys.executable, child], env={**os.environ, **env}, capture_output=True, text=True,
-                       timeout=240)
+    r = subprocess.run([sys.executable, child] + (["many"] if many else []), env={**os.environ, **env},
+                       capture_output=True, text=True, timeout=240)
     say(r.stdout.strip())
     assert r.returncode == 0, r.stdout + r.stderr[-3000:]
