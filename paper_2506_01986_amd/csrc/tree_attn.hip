@@ -25,6 +25,7 @@
 // running max, running sum) to the workspace, merged in a fixed order by
 // tree_attn_combine (deterministic, no atomics).
 #include <mutex>
+#include <type_traits>
 
 #include "device.h"
 #include "internal.h"
@@ -306,8 +307,7 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) vro[i] = (4 * h + tj) * (D * 2) + 64 * (i ^ tj) + 16 * te + 8 * (tq & 1);
 
-  auto qk = [&](int j, f32x16 (&Sc)[2]) {
-    const uint8_t *ks = kring[j % SLOTS];
+  auto qk = [&](const uint8_t *ks, f32x16 (&Sc)[2]) {
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -450,21 +450,30 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   };
 
   // Iteration j needs tile j; after its barrier every wave is done with tile
-  // j-1, whose slots take tile j+SLOTS-1.
-  for (int j = 0; j < ntiles; ++j) {
+  // j-1, whose slots take tile j+SLOTS-1.  The loop is unrolled by the ring
+  // depth, so that every slot address is a constant (the LDS reads then take
+  // it as their immediate offset instead of a vector add per read).
+  auto tile = [&](int j, auto slot_c) {
+    constexpr int slot = decltype(slot_c)::value;
     // loads issued after tile j: tile j+1 (3 slots), two operands
     wait_loads(SLOTS == 3 && j + 1 < ntiles ? 2 : 0);
     ring_barrier();
     if (j + SLOTS - 1 < ntiles) {
-      issue_k(j + SLOTS - 1);
-      issue_v(j + SLOTS - 1);
+      issue(Kb, true, kring[(slot + SLOTS - 1) % SLOTS], j + SLOTS - 1);
+      issue(Vb, false, vring[(slot + SLOTS - 1) % SLOTS], j + SLOTS - 1);
     }
     f32x16 Sc[2];
     uint32_t pk[4][4];
-    qk(j, Sc);
+    qk(kring[slot], Sc);
     softmax_head(j, Sc);
     softmax_tail(Sc, pk);
-    pv(vring[j % SLOTS], pk);
+    pv(vring[slot], pk);
+  };
+  for (int j = 0; j < ntiles; j += SLOTS) {
+    tile(j, std::integral_constant<int, 0>{});
+    if (j + 1 < ntiles) tile(j + 1, std::integral_constant<int, 1>{});
+    if constexpr (SLOTS == 3)
+      if (j + 2 < ntiles) tile(j + 2, std::integral_constant<int, 2>{});
   }
 
   const float ltot = sum_with_other_half(lsum);
