@@ -116,6 +116,7 @@ __global__ __launch_bounds__(kWaves * 64) void head_logits_bf16(
 // group's nS * 4 KB contiguously, one 1 KB operand tile per load instruction,
 // and contracts each tile against the 16 hidden states of its batch tile.
 constexpr int kPackedUnroll = 4;   // k steps (4 KB each) issued before their MFMAs
+constexpr int kHidChunk = 16;      // k steps of hidden states staged in LDS at a time (two batch tiles)
 
 // Weights are read once per step: nontemporal loads keep them from displacing
 // the hidden states and logits in the caches.
@@ -131,51 +132,127 @@ template <int NB>
 __global__ __launch_bounds__(kWaves * 64) void head_logits_packed(
     const uint16_t *__restrict__ h, int64_t h_head_stride, const uint4 *__restrict__ Wp, float *__restrict__ z,
     int B, int hidden, int vocab, int n_heads, int nG, int nS, float *__restrict__ gmax) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, b0 = blockIdx.z * 16 * NB;
   const int G = blockIdx.x * kWaves + wave;
-  if (G >= nG) return;
+  const bool active = G < nG;
   const int kq = lane >> 4;
-  const uint4 *wp = Wp + (int64_t)(head * nG + G) * nS * 4 * 64 + lane;
-  bool bvalid[NB];
-  const uint16_t *hp[NB];
-#pragma unroll
-  for (int n = 0; n < NB; ++n) {
-    const int b = b0 + 16 * n + (lane & 15);
-    bvalid[n] = b < B;
-    hp[n] = h + head * h_head_stride + (int64_t)(bvalid[n] ? b : 0) * hidden + kq * 8;
-  }
+  const uint4 *wp = Wp + (int64_t)(head * (int64_t)nG + (active ? G : 0)) * nS * 4 * 64 + lane;
   f32x4 acc[NB][4];
 #pragma unroll
   for (int n = 0; n < NB; ++n)
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[n][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto step = [&](const uint4 (&a)[4], int s) {
-    const int k = 32 * s + 8 * kq;
+  if constexpr (NB == 1) {
+    // One batch tile: each wave reads its hidden-state fragments itself.
+    if (!active) return;
+    bool bvalid[NB];
+    const uint16_t *hp[NB];
 #pragma unroll
     for (int n = 0; n < NB; ++n) {
-      const bf16x8 bv = __builtin_bit_cast(bf16x8, ld16_or_zero(bvalid[n] && k < hidden, hp[n] + 32 * s));
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-        acc[n][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[t]), bv, acc[n][t], 0, 0, 0);
+      const int b = b0 + 16 * n + (lane & 15);
+      bvalid[n] = b < B;
+      hp[n] = h + head * h_head_stride + (int64_t)(bvalid[n] ? b : 0) * hidden + kq * 8;
     }
-  };
-  int s = 0;
-  for (; s + kPackedUnroll <= nS; s += kPackedUnroll) {
-    uint4 a[kPackedUnroll][4];
+    auto step = [&](const uint4 (&a)[4], int s) {
+      const int k = 32 * s + 8 * kq;
 #pragma unroll
-    for (int u = 0; u < kPackedUnroll; ++u)
+      for (int n = 0; n < NB; ++n) {
+        const bf16x8 bv = __builtin_bit_cast(bf16x8, ld16_or_zero(bvalid[n] && k < hidden, hp[n] + 32 * s));
 #pragma unroll
-      for (int t = 0; t < 4; ++t) a[u][t] = ld16_stream(wp + ((s + u) * 4 + t) * 64);
+        for (int t = 0; t < 4; ++t)
+          acc[n][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[t]), bv, acc[n][t], 0, 0, 0);
+      }
+    };
+    int s = 0;
+    for (; s + kPackedUnroll <= nS; s += kPackedUnroll) {
+      uint4 a[kPackedUnroll][4];
 #pragma unroll
-    for (int u = 0; u < kPackedUnroll; ++u) step(a[u], s + u);
-  }
-  for (; s < nS; ++s) {
-    uint4 a[4];
+      for (int u = 0; u < kPackedUnroll; ++u)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) a[t] = ld16_stream(wp + (s * 4 + t) * 64);
-    step(a, s);
+        for (int t = 0; t < 4; ++t) a[u][t] = ld16_stream(wp + ((s + u) * 4 + t) * 64);
+#pragma unroll
+      for (int u = 0; u < kPackedUnroll; ++u) step(a[u], s + u);
+    }
+    for (; s < nS; ++s) {
+      uint4 a[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) a[t] = ld16_stream(wp + (s * 4 + t) * 64);
+      step(a, s);
+    }
+  } else {
+    // Two batch tiles: the second hidden-state gather per k step made the
+    // vector cache the bottleneck, so the block's waves share their hidden
+    // states through LDS: chunks of kHidChunk k steps (two buffers) in the B
+    // operand's lane order, one 1 KB piece per (step, batch tile), read with
+    // one conflict-free 16-byte LDS read per step and tile.  Entry e of a
+    // piece holds row e % 16, columns 32 (step) + 8 (e / 16) .. +8; rows past
+    // B, columns past hidden and steps past nS are zero.  Waves past the last
+    // row group still stage hidden states and meet the barriers.
+    constexpr int kPieces = kHidChunk * NB * 64;
+    constexpr int kPer = kPieces / (kWaves * 64);
+    __shared__ uint4 hsh[2][kPieces];
+    const uint16_t *hbase = h + head * h_head_stride;
+    uint4 hreg[kPer];
+    auto hfetch = [&](int c) {
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        const int q = tid + i * kWaves * 64;
+        const int kk = q & 3, row = (q >> 2) & 15, pn = q >> 6;
+        const int n = pn % NB, sl = pn / NB;
+        const int st = c * kHidChunk + sl, b = b0 + 16 * n + row, k = 32 * st + 8 * kk;
+        const bool ok = b < B && k < hidden && st < nS;
+        const uint4 v = *reinterpret_cast<const uint4 *>(hbase + (int64_t)(b < B ? b : 0) * hidden + min(k, hidden - 8));
+        hreg[i] = ok ? v : uint4{0u, 0u, 0u, 0u};
+      }
+    };
+    auto hstore = [&](int buf) {
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        const int q = tid + i * kWaves * 64;
+        hsh[buf][(q >> 6) * 64 + (q & 3) * 16 + ((q >> 2) & 15)] = hreg[i];
+      }
+    };
+    auto step = [&](const uint4 (&a)[4], const uint4 *hb, int sl) {
+#pragma unroll
+      for (int n = 0; n < NB; ++n) {
+        const bf16x8 bv = __builtin_bit_cast(bf16x8, hb[(sl * NB + n) * 64 + lane]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          acc[n][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[t]), bv, acc[n][t], 0, 0, 0);
+      }
+    };
+    const int nch = (nS + kHidChunk - 1) / kHidChunk;
+    hfetch(0);
+    hstore(0);
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+      if (c + 1 < nch) hfetch(c + 1);
+      const uint4 *hb = hsh[c & 1];
+      const int s0 = c * kHidChunk, s1 = min(nS, s0 + kHidChunk);
+      if (active) {
+        int s = s0;
+        for (; s + kPackedUnroll <= s1; s += kPackedUnroll) {
+          uint4 a[kPackedUnroll][4];
+#pragma unroll
+          for (int u = 0; u < kPackedUnroll; ++u)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) a[u][t] = ld16_stream(wp + ((s + u) * 4 + t) * 64);
+#pragma unroll
+          for (int u = 0; u < kPackedUnroll; ++u) step(a[u], hb, s - s0 + u);
+        }
+        for (; s < s1; ++s) {
+          uint4 a[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) a[t] = ld16_stream(wp + (s * 4 + t) * 64);
+          step(a, hb, s - s0);
+        }
+      }
+      if (c + 1 < nch) hstore((c + 1) & 1);
+      __syncthreads();
+    }
+    if (!active) return;
   }
 
   // C layout: lane holds column (batch) lane&15, rows 4*(lane>>4) + 0..3 of each tile.
