@@ -132,7 +132,7 @@ int hip_status(hipError_t e, const char *what) {
 
 // ---- tree attention planning ------------------------------------------------------
 constexpr int kMaxSlabRows = 1 << 23;   // bf16 attention: slab bytes below 2^31
-constexpr int kMinChunk = 256;      // fewest keys per chunk when splitting the KV range
+constexpr int kMinChunk = 160;      // fewest keys per chunk when splitting the KV range
 
 // Tuning overrides (they change the work split, never the result beyond
 // rounding): SPECMEMO_ATTN_CHUNK = fixed
