@@ -405,12 +405,13 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
   return v;
 }
 
-template <int DT>
-__device__ __forceinline__ int typical_pick(const AcceptArgs &a, int b, int *s_path) {
+template <int DT, int NT>
+__device__ __forceinline__ int typical_pick(const AcceptArgs &a, int b, int *s_path, bool write_out) {
+  constexpr int NW = NT / 64;
   __shared__ float lp[kMaxNodes], score[kMaxNodes];
   __shared__ int pass[kMaxNodes], ok[kMaxNodes], par[kMaxNodes], dep[kMaxNodes];
-  __shared__ uint64_t s_key[kWaves];
-  static_assert(kNT >= kMaxNodes, "one thread per tree node");
+  __shared__ uint64_t s_key[NW];
+  static_assert(NT >= kMaxNodes, "one thread per tree node");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
   int my_dep = 0;
@@ -450,16 +451,18 @@ __device__ __forceinline__ int typical_pick(const AcceptArgs &a, int b, int *s_p
   __syncthreads();
   key = s_key[0];
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) key = s_key[w] > key ? s_key[w] : key;
+  for (int w = 1; w < NW; ++w) key = s_key[w] > key ? s_key[w] : key;
   const int best = kMaxNodes - 1 - (int)(key & 0xFF);
   const int len = dep[best];
   if (tid == 0) {
-    a.accept_len[b] = len;
-    a.next_tok[b] = a.best[n0 + best];
     int32_t *p = a.path + (int64_t)b * a.path_stride;
-    for (int j = 0; j < a.path_stride; ++j) p[j] = -1;
+    if (write_out) {
+      a.accept_len[b] = len;
+      a.next_tok[b] = a.best[n0 + best];
+      for (int j = 0; j < a.path_stride; ++j) p[j] = -1;
+    }
     for (int u = best, j = len; u >= 0 && j >= 0; u = par[u], --j) {
-      p[j] = u;
+      if (write_out) p[j] = u;
       s_path[j] = u;
     }
   }
@@ -471,24 +474,28 @@ __device__ __forceinline__ int typical_pick(const AcceptArgs &a, int b, int *s_p
 template <int DT>
 __global__ __launch_bounds__(kNT) void accept_typical(AcceptArgs a) {
   __shared__ int s_path[kMaxPath];
-  typical_pick<DT>(a, blockIdx.x, s_path);
+  typical_pick<DT, kNT>(a, blockIdx.x, s_path, true);
 }
 
-// Acceptance and compaction in one pass: one block per sequence of a launch
-// group picks the path, then its waves move the accepted rows of the 2 n_kv
-// (KV head, K|V) slabs.
+// Acceptance and compaction in one pass: one block per (sequence, KV head,
+// K|V) picks the sequence's path (a few LDS rounds over at most kMaxNodes
+// nodes, repeated per block so that no block waits for another) and moves
+// the accepted rows of its slab; the block of (KV head 0, K) writes the
+// acceptance outputs and the new length.
+constexpr int kPickNT = kMaxNodes;   // one thread per tree node
+
 template <int DT>
-__global__ __launch_bounds__(kNT) void accept_typical_compact(AcceptArgs a, CompactArgs c) {
+__global__ __launch_bounds__(kPickNT) void accept_typical_compact(AcceptArgs a, CompactArgs c) {
   __shared__ int s_path[kMaxPath];
-  const int s = blockIdx.x, b = c.b0 + s;
-  const int len = typical_pick<DT>(a, b, s_path);
+  const int s = blockIdx.x, kvh = blockIdx.y, which = blockIdx.z, b = c.b0 + s;
+  const bool writer = kvh == 0 && which == 0;
+  const int len = typical_pick<DT, kPickNT>(a, b, s_path, writer);
   int src[kMaxPath];
 #pragma unroll
   for (int j = 0; j < kMaxPath; ++j) src[j] = j <= len ? s_path[j] : -1;
   const CompactSeq S = c.tab ? c.tab[s] : c.seq[s];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int p = wave; p < 2 * c.n_kv; p += kWaves) move_rows(c, S, p >> 1, p & 1, len, src, lane, 64);
-  if (threadIdx.x == 0) c.seq_len[b] = S.L + len + 1;
+  move_rows(c, S, kvh, which, len, src, threadIdx.x, kPickNT);
+  if (writer && threadIdx.x == 0) c.seq_len[b] = S.L + len + 1;
 }
 
 // ---- sampled next token ---------------------------------------------------------
@@ -608,9 +615,9 @@ hipError_t launch_accept_compact(int dt, const AcceptArgs &a, const CompactArgs 
   if (a.mode == 0)
     hipLaunchKernelGGL(accept_walk_compact, dim3(c.nseq, c.n_kv, 2), dim3(64), 0, st, a, c);
   else if (dt == 1)
-    hipLaunchKernelGGL(accept_typical_compact<1>, dim3(c.nseq), dim3(kNT), 0, st, a, c);
+    hipLaunchKernelGGL(accept_typical_compact<1>, dim3(c.nseq, c.n_kv, 2), dim3(kPickNT), 0, st, a, c);
   else
-    hipLaunchKernelGGL(accept_typical_compact<0>, dim3(c.nseq), dim3(kNT), 0, st, a, c);
+    hipLaunchKernelGGL(accept_typical_compact<0>, dim3(c.nseq, c.n_kv, 2), dim3(kPickNT), 0, st, a, c);
   return hipGetLastError();
 }
 
