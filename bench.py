@@ -622,9 +622,10 @@ def main():
                  "note": "the same step, every step on one replica (its pool stays in the MALL)"},
         "overlapped_step": {"ms_per_step": round(over_ms, 5), "ms_per_step_warm": round(warm_over_ms, 5),
                             "note": "the attention on a second stream, concurrent with the projection and top-k "
-                                    "(they share no data), rotated like the headline; the two kernels then "
-                                    "share the compute units and the projection's stream slows by about the "
-                                    "attention's time"},
+                                    "(they share no data in this synthetic step; in a full model the queries "
+                                    "come from the tree tokens), rotated like the headline; the two kernels "
+                                    "then share the compute units and the projection's stream slows by about "
+                                    "the attention's time"},
         "typical": {"ms_per_step": round(typ_ms, 5), "value": round(wl.total_nodes / (typ_ms * 1e-3), 1),
                     "accept_stage_ms": st["accept_typical"]["ms"], "temperature": step.temperature,
                     "eps": step.eps, "delta": step.delta},

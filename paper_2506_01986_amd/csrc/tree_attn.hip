@@ -181,14 +181,24 @@ __device__ __forceinline__ int vswz(int r, int c) { return c ^ ((r & 3) << 2); }
 
 // WAVES waves per block, 32 query rows per wave (one per lane pair l, l^32);
 // K and V each have a SLOTS-deep ring of 64-key tiles filled by direct loads;
-// iteration j computes S, the weights and O for tile j, its two 32-key
-// products S^T = K Q^T being independent accumulation chains.
+// iteration j computes S, the weights and O for tile j.
+// KSPLIT = 1: every wave takes both 32-key halves of a tile (its two products
+// S^T = K Q^T being independent accumulation chains); RB = 32 WAVES rows.
+// KSPLIT = 2: the waves form two groups over the same RB = 16 WAVES rows, the
+// first taking keys 0-31 of every tile and the second keys 32-63, each with
+// its own online softmax; the two groups' (m, l, O) are merged through LDS at
+// the end.  With few rows per K/V tile (multi-head attention: 64 rows per
+// (sequence, head)) this halves each wave's chain per tile and keeps two
+// waves on every SIMD.
 // MINB: blocks that must fit on one compute unit (bounds the registers).
 // PAD: the cache holds pad tokens (padded batching), flagged in a.key_valid.
-template <int WAVES, int SLOTS, int MINB, bool PAD>
+template <int WAVES, int SLOTS, int MINB, bool PAD, int KSPLIT>
 __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   static_assert(SLOTS == 2 || SLOTS == 3, "ring depth");
-  constexpr int RB = 32 * WAVES;
+  static_assert(KSPLIT == 1 || KSPLIT == 2, "key split");
+  constexpr int RW = WAVES / KSPLIT;          // waves per key group
+  constexpr int RB = 32 * RW;
+  constexpr int NSB = 2 / KSPLIT;             // 32-key sub-blocks per wave and tile
   constexpr int TILE = TK * D * 2;            // bytes of one K or V tile (16 KB)
   constexpr int IPW = TILE / 1024 / WAVES;    // 1 KB direct loads per wave per tile and operand
   __shared__ __attribute__((aligned(1024))) uint8_t kring[SLOTS][TILE];
@@ -197,11 +207,13 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   // does not fill and the first loop barrier frees again.
   int *const par = reinterpret_cast<int *>(vring[SLOTS - 1]);
   static_assert(WAVES * 64 >= kMaxNodes && kMaxNodes * 4 <= TILE, "one thread per tree node");
+  static_assert(KSPLIT == 1 || RW * 64 * 64 * 4 <= SLOTS * TILE, "merge buffer fits the K ring");
 
   Item it;
   AttnSeq S;
   if (!decode_item(a, blockIdx.x, it, S)) return;   // padding block: no work, no barrier reached
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rwave = wave % RW, ksb = wave / RW;     // row group and key group of this wave
   const int h = lane >> 5;              // which half of the wave
   const int L = S.L, N = S.N, g = a.group;
   const int rows = N * g;
@@ -263,7 +275,7 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
       issue_v(t);
     }
   const int pn = tid < N ? a.parent[S.node0 + tid] : -1;
-  const int my_row = it.rb * RB + wave * 32 + (lane & 31);
+  const int my_row = it.rb * RB + rwave * 32 + (lane & 31);
   const bool row_ok = my_row < rows;
   const int node = row_ok ? my_row / g : 0;
   const int hq = it.kvh * g + (row_ok ? my_row % g : 0);
@@ -306,25 +318,28 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   int vro[D / 32];
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) vro[i] = (4 * h + tj) * (D * 2) + 64 * (i ^ tj) + 16 * te + 8 * (tq & 1);
+  // First 32-key sub-block of this wave's keys in a tile.
+  const int sb0 = ksb * NSB;
 
-  auto qk = [&](const uint8_t *ks, f32x16 (&Sc)[2]) {
+  auto qk = [&](const uint8_t *ks, f32x16 (&Sc)[NSB]) {
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
+    for (int sb = 0; sb < NSB; ++sb)
 #pragma unroll
       for (int r2 = 0; r2 < 16; ++r2) Sc[sb][r2] = 0.f;
+    const uint8_t *kw = ks + sb0 * 32 * (D * 2);
 #pragma unroll
     for (int k8 = 0; k8 < D / 16; ++k8)
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(ks + sb * 32 * (D * 2) + kro[k8]));
+      for (int sb = 0; sb < NSB; ++sb) {
+        const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(kw + sb * 32 * (D * 2) + kro[k8]));
         Sc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k8], Sc[sb], 0, 0, 0);
       }
-    // keep the K fragment reads just ahead of their products (two LDS reads,
-    // two products, eight times) instead of all sixteen reads up front
+    // keep the K fragment reads just ahead of their products (NSB LDS reads,
+    // NSB products, eight times) instead of all of them up front
 #pragma unroll
     for (int k8 = 0; k8 < D / 16; ++k8) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, NSB, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, NSB, 0);
     }
   };
 
@@ -354,12 +369,13 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
   const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
 
   // Scores of tile j -> bf16 weights (online softmax, lazy rescale); O += V^T P^T.
-  // Accumulator entry r of sub-block sb is key kt + 32 sb + 8 (r / 4) + 4 h + r % 4.
+  // Accumulator entry r of the wave's sub-block sb is key
+  // kt + 32 (sb0 + sb) + 8 (r / 4) + 4 h + r % 4.
   // The tree mask, for tiles that reach the tree rows or the chunk end, is
   // branch-free (bitwise tests, one select per score) so that the scores keep
   // their registers on both paths.  The weights are returned packed as the B
-  // operands of the four 16-key groups of the PV product.
-  auto softmax_head = [&](int j, f32x16 (&Sc)[2]) {   // mask, tile max, rescaling
+  // operands of the wave's 16-key groups of the PV product.
+  auto softmax_head = [&](int j, f32x16 (&Sc)[NSB]) {   // mask, tile max, rescaling
     const int kt = k0 + j * TK;
     if constexpr (PAD) {
       if (kt < L) {                      // committed keys: pad tokens take -inf
@@ -367,20 +383,20 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
         if (all != ~0ull) {              // wave-uniform: tiles without pads skip the selects
           const uint64_t bits = all >> (4 * h);
 #pragma unroll
-          for (int sb = 0; sb < 2; ++sb)
+          for (int sb = 0; sb < NSB; ++sb)
 #pragma unroll
             for (int r2 = 0; r2 < 16; ++r2)
-              Sc[sb][r2] = (bits >> (32 * sb + 8 * (r2 >> 2) + (r2 & 3))) & 1u ? Sc[sb][r2] : -INFINITY;
+              Sc[sb][r2] = (bits >> (32 * (sb0 + sb) + 8 * (r2 >> 2) + (r2 & 3))) & 1u ? Sc[sb][r2] : -INFINITY;
         }
       }
     }
     if (kt + TK > min(k1, L)) {
       const uint64_t alo = (uint64_t)anc.y << 32 | anc.x, ahi = (uint64_t)anc.w << 32 | anc.z;
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
+      for (int sb = 0; sb < NSB; ++sb)
 #pragma unroll
         for (int r2 = 0; r2 < 16; ++r2) {
-          const int t = kt + 32 * sb + 8 * (r2 >> 2) + 4 * h + (r2 & 3);
+          const int t = kt + 32 * (sb0 + sb) + 8 * (r2 >> 2) + 4 * h + (r2 & 3);
           const uint32_t rel = (uint32_t)(t - L) & 127u;
           const uint64_t word = rel < 64 ? alo : ahi;
           const bool anc_bit = (word >> (rel & 63)) & 1u;
@@ -388,7 +404,17 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
           Sc[sb][r2] = vis ? Sc[sb][r2] : -INFINITY;
         }
     }
-    const float tmax = max_with_other_half(tile_max32(Sc)) * a.scale_log2;
+    float tm;
+    if constexpr (NSB == 2) {
+      tm = tile_max32(Sc);
+    } else {
+      const f32x16 &x = Sc[0];
+      const float u0 = fmaxf(fmaxf(x[0], x[1]), x[2]), u1 = fmaxf(fmaxf(x[3], x[4]), x[5]);
+      const float u2 = fmaxf(fmaxf(x[6], x[7]), x[8]), u3 = fmaxf(fmaxf(x[9], x[10]), x[11]);
+      const float u4 = fmaxf(fmaxf(x[12], x[13]), x[14]);
+      tm = fmaxf(fmaxf(fmaxf(u0, u1), fmaxf(u2, u3)), fmaxf(u4, x[15]));
+    }
+    const float tmax = max_with_other_half(tm) * a.scale_log2;
     // Lazy rescaling: the reference max m moves only when a score exceeds it by
     // more than kRescaleSlack (log2 units), so weights stay <= 2^kRescaleSlack;
     // the branch is taken by the whole wave, rarely after the first tile.
@@ -404,12 +430,12 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
         for (int r2 = 0; r2 < 16; ++r2) O[i][r2] *= alpha;
     }
   };
-  auto softmax_tail = [&](const f32x16 (&Sc)[2], uint32_t (&pk)[4][4]) {   // weights and row sum
+  auto softmax_tail = [&](const f32x16 (&Sc)[NSB], uint32_t (&pk)[2 * NSB][4]) {   // weights and row sum
     const float m_use = m == -INFINITY ? 0.f : m;
-    // B operand of 16-key group mh = 2 sb + half: slot 8 h + s <-> key
-    // 32 sb + 16 half + 8 (s / 4) + 4 h + s % 4 (the V^T reads use the same order).
+    // B operand of local 16-key group 2 sb + half: slot 8 h + s <-> key
+    // 32 (sb0 + sb) + 16 half + 8 (s / 4) + 4 h + s % 4 (the V^T reads use the same order).
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
+    for (int sb = 0; sb < NSB; ++sb)
 #pragma unroll
       for (int half = 0; half < 2; ++half)
 #pragma unroll
@@ -420,18 +446,18 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
         }
     // Row sum of the bf16 weights that enter O (two-term dot products with ones).
 #pragma unroll
-    for (int mh = 0; mh < 4; ++mh)
+    for (int mh = 0; mh < 2 * NSB; ++mh)
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pk[mh][q]), ones, lsum, false);
   };
-  auto pv = [&](const uint8_t *vs, const uint32_t (&pk)[4][4]) {
+  auto pv = [&](const uint8_t *vs, const uint32_t (&pk)[2 * NSB][4]) {
 #pragma unroll
-    for (int mh = 0; mh < 4; ++mh) {
+    for (int mh = 0; mh < 2 * NSB; ++mh) {
       const bf16x8 pf = __builtin_bit_cast(bf16x8, uint4{pk[mh][0], pk[mh][1], pk[mh][2], pk[mh][3]});
 #pragma unroll
       for (int i = 0; i < D / 32; ++i) {
-        const uint8_t *p = vs + 16 * mh * (D * 2) + vro[i];
+        const uint8_t *p = vs + 16 * (2 * sb0 + mh) * (D * 2) + vro[i];
         const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)p);
         const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)(p + 8 * (D * 2)));
         const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
@@ -462,8 +488,8 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
       issue(Kb, true, kring[(slot + SLOTS - 1) % SLOTS], j + SLOTS - 1);
       issue(Vb, false, vring[(slot + SLOTS - 1) % SLOTS], j + SLOTS - 1);
     }
-    f32x16 Sc[2];
-    uint32_t pk[4][4];
+    f32x16 Sc[NSB];
+    uint32_t pk[2 * NSB][4];
     qk(kring[slot], Sc);
     softmax_head(j, Sc);
     softmax_tail(Sc, pk);
@@ -476,7 +502,37 @@ __global__ __launch_bounds__(WAVES * 64, MINB) void tree_attn_bf16(AttnArgs a) {
       if (j + 2 < ntiles) tile(j + 2, std::integral_constant<int, 2>{});
   }
 
-  const float ltot = sum_with_other_half(lsum);
+  float ltot = sum_with_other_half(lsum);
+  if constexpr (KSPLIT == 2) {
+    // Merge the second key group's (m, l, O) into the first's.  Every wave is
+    // past its last read of the ring (the barrier) and no tile load is in
+    // flight (the last iteration waited for all of them), so the K ring holds
+    // the second group's O, [row wave][value][lane] (conflict-free), and the
+    // V ring its m and l.
+    ring_barrier();
+    float *const mo = reinterpret_cast<float *>(kring[0]);
+    float *const ml = reinterpret_cast<float *>(vring[0]);
+    if (ksb == 1) {
+#pragma unroll
+      for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+        for (int r2 = 0; r2 < 16; ++r2) mo[(rwave * 64 + 16 * i + r2) * 64 + lane] = O[i][r2];
+      ml[(rwave * 2) * 64 + lane] = m;
+      ml[(rwave * 2 + 1) * 64 + lane] = ltot;
+    }
+    ring_barrier();
+    if (ksb == 1) return;
+    const float m1 = ml[(rwave * 2) * 64 + lane], l1 = ml[(rwave * 2 + 1) * 64 + lane];
+    const float mn = fmaxf(m, m1);
+    const float w0 = m == -INFINITY ? 0.f : fast_exp2(m - mn);
+    const float w1 = m1 == -INFINITY ? 0.f : fast_exp2(m1 - mn);
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+      for (int r2 = 0; r2 < 16; ++r2) O[i][r2] = O[i][r2] * w0 + mo[(rwave * 64 + 16 * i + r2) * 64 + lane] * w1;
+    ltot = ltot * w0 + l1 * w1;
+    m = mn;
+  }
   if (!row_ok) return;
   // O^T entry r of d-block i is d = 32 i + 8 (r / 4) + 4 h + r % 4 of this lane's row.
   if (S.nch == 1) {
@@ -646,13 +702,13 @@ namespace {
 template <bool PAD>
 void launch_bf16(const AttnArgs &a, int rows_per_block, hipStream_t st) {
   if (rows_per_block == 64) {
-    hipLaunchKernelGGL((tree_attn_bf16<2, 2, 2, PAD>), dim3(a.items), dim3(128), 0, st, a);
+    hipLaunchKernelGGL((tree_attn_bf16<4, 2, 2, PAD, 2>), dim3(a.items), dim3(256), 0, st, a);
     if (a.citems) hipLaunchKernelGGL(tree_attn_combine<64>, dim3(a.citems), dim3(256), 0, st, a);
   } else if (rows_per_block == 128) {
-    hipLaunchKernelGGL((tree_attn_bf16<4, 2, 2, PAD>), dim3(a.items), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((tree_attn_bf16<4, 2, 2, PAD, 1>), dim3(a.items), dim3(256), 0, st, a);
     if (a.citems) hipLaunchKernelGGL(tree_attn_combine<128>, dim3(a.citems), dim3(512), 0, st, a);
   } else {
-    hipLaunchKernelGGL((tree_attn_bf16<8, 3, 1, PAD>), dim3(a.items), dim3(512), 0, st, a);
+    hipLaunchKernelGGL((tree_attn_bf16<8, 3, 1, PAD, 1>), dim3(a.items), dim3(512), 0, st, a);
     if (a.citems) hipLaunchKernelGGL(tree_attn_combine<256>, dim3(a.citems), dim3(1024), 0, st, a);
   }
 }

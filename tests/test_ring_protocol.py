@@ -19,10 +19,14 @@ tiles, that under any completion times the hardware may choose:
 * no load is still in flight when the program ends;
 * the parent array is not overwritten before the ancestor walk is done.
 
+The key-split form (two key groups per row block) then writes its second
+group's (m, l, O) over the rings for the first group to merge: that needs
+every load complete and every wave's reads behind a barrier.
+
 The mutants at the bottom show that the checker rejects the plausible ways
 to get the ring wrong (a wait one tile too shallow, a load issued before the
 barrier, a third slot without the deeper wait count, the parent array in a
-slot the prologue fills).
+slot the prologue fills, the merge without its barrier).
 """
 
 import itertools
@@ -30,9 +34,12 @@ import itertools
 import pytest
 
 
-def kernel_program(ntiles, slots, *, par_slot=None, wait_later=None, issue_before_barrier=False):
+def kernel_program(ntiles, slots, *, par_slot=None, wait_later=None, issue_before_barrier=False, merge=False,
+                   merge_barrier=True):
     """Event list of one wave.  Events: ("issue", tile, op), ("wait", k),
-    ("barrier",), ("read", tile, op), ("par_write",), ("par_read",)."""
+    ("barrier",), ("read", tile, op), ("par_write",), ("par_read",), ("merge",).
+    `merge`: the key-split form, whose two key groups exchange (m, l, O)
+    through the K and V rings after the loop, behind one more barrier."""
     par_slot = slots - 1 if par_slot is None else par_slot
     if wait_later is None:
         def wait_later(j):
@@ -54,6 +61,8 @@ def kernel_program(ntiles, slots, *, par_slot=None, wait_later=None, issue_befor
         if not issue_before_barrier and nxt < ntiles:
             ev += [("issue", nxt, "K"), ("issue", nxt, "V")]
         ev += [("read", j, "K"), ("read", j, "V")]
+    if merge:
+        ev += ([("barrier",)] if merge_barrier else []) + [("merge",)]
     return ev
 
 
@@ -94,6 +103,11 @@ def check(ev, slots):
             reads.append((epoch, ("V", par_slot), -1))   # an LDS write: no load may land under it either
         elif kind == "par_read":
             reads.append((epoch, ("V", par_slot), -1))
+        elif kind == "merge":
+            # LDS writes over both rings: no load may still be landing, and
+            # every wave's reads of the rings must be behind a barrier
+            assert not pending, "merge writes while a tile load is in flight"
+            assert all(re < epoch for (re, _, _) in reads), "merge writes over a ring another wave may still read"
         else:
             raise ValueError(kind)
     assert not pending, "loads still in flight at the end of the program"
@@ -125,6 +139,17 @@ CASES = [(n, s) for s in (2, 3) for n in range(1, 9)]
 @pytest.mark.parametrize("ntiles,slots", CASES)
 def test_ring_protocol_of_the_kernel(ntiles, slots):
     check(kernel_program(ntiles, slots), slots)
+
+
+@pytest.mark.parametrize("ntiles", range(1, 9))
+def test_ring_protocol_with_key_split_merge(ntiles):
+    check(kernel_program(ntiles, 2, merge=True), 2)
+
+
+def test_mutant_merge_without_barrier_is_caught():
+    for n in range(1, 6):
+        with pytest.raises(AssertionError):
+            check(kernel_program(n, 2, merge=True, merge_barrier=False), 2)
 
 
 def test_mutant_wait_too_shallow_is_caught():
