@@ -251,7 +251,7 @@ EDGES = {
     "mixed_gqa": (edge_cfg(B=4, n_q=8, n_kv=1),
                   lambda r: [synth.random_tree(r, 128), synth.tree_from_rank_paths([()]), synth.t64(),
                              synth.chain_tree(5)], [0, 37, 64, 1]),
-    # MHA (2-wave row blocks), 17 sequences (two 16-wide batch tiles in the head GEMM)
+    # MHA (64-row items: the key-split form), 17 sequences (two 16-wide batch tiles in the head GEMM)
     "mha_b17": (edge_cfg(B=17, n_q=2, n_kv=2, hidden=64, vocab=520),
                 lambda r: [synth.random_tree(r, int(r.integers(1, 65))) for _ in range(17)],
                 list(range(0, 17 * 70, 70))),
