@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SPECMEMO_ABI_VERSION 8
+#define SPECMEMO_ABI_VERSION 9
 #define SPECMEMO_MAX_TREE_NODES 128 /* nodes per sequence's tree */
 #define SPECMEMO_MAX_DEPTH 15       /* tree depth (= Medusa heads) */
 #define SPECMEMO_MAX_TOPK 32        /* top-k per head */
@@ -255,10 +255,15 @@ int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab,
  * (seed, offset) and counter (v / 4, b, 0, 0).  Ties go to the lower id.  A
  * caller draws a fresh sample per step by changing offset.  Sequences whose
  * accept_len / path entry is out of range keep their next_tok.  temperature
- * must be positive and finite (and 1/T finite). */
+ * must be positive and finite (and 1/T finite).
+ * ws: specmemo_workspace_bytes(SPECMEMO_WS_SAMPLE, ...) bytes, 16-byte aligned
+ * (one 64-bit word per sequence and 1024-token segment of the row), or NULL:
+ * with it the draws of a row are spread over one block per segment, without
+ * it one block per sequence draws its whole row (the same token either way). */
 int specmemo_sample_next(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, float temperature,
                          uint64_t seed, uint64_t offset, const void *base_logits, const int32_t *accept_len,
-                         const int32_t *path, int32_t path_stride, int32_t *next_tok, void *stream);
+                         const int32_t *path, int32_t path_stride, int32_t *next_tok, void *ws,
+                         size_t ws_bytes, void *stream);
 
 /* (d) In-place KV compaction (Sec. 3.1 KV-cache paragraph: the preallocated
  * cache is a scratch space updated during verification; Sec. 3.3: rejected
@@ -477,6 +482,7 @@ int specmemo_plan_tree_sizes(int32_t B, const int32_t *seq_len_h, const int32_t 
 #define SPECMEMO_WS_ATTN 1
 #define SPECMEMO_WS_ACCEPT 2
 #define SPECMEMO_WS_PAD 3
+#define SPECMEMO_WS_SAMPLE 4
 
 /* Workspace bytes a call needs for these arguments (host-side; the only HIP
  * calls query the current device's compute-unit count, which the attention
@@ -493,6 +499,8 @@ int specmemo_plan_tree_sizes(int32_t B, const int32_t *seq_len_h, const int32_t 
  *                       compaction descriptors of specmemo_accept_compact).
  *   SPECMEMO_WS_PAD:    specmemo_kv_pad_update; kv, n_q_or_heads and vocab
  *                       ignored.
+ *   SPECMEMO_WS_SAMPLE: specmemo_sample_next; kv and n_q_or_heads ignored;
+ *                       vocab used.
  * Returns 0 for invalid arguments as well as when no workspace is needed;
  * the call itself reports invalid arguments. */
 size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo_trees *t,

@@ -522,66 +522,137 @@ __device__ __forceinline__ void philox4x64_10(uint64_t (&x)[4], uint64_t k0, uin
 // Gumbel-max draw from softmax(z / T) of sequence b's last accepted row: the
 // argmax over v of fmaf(z_v, 1/T, G_v), G_v = -log(-log(u_v)), u_v from
 // Philox with key (seed, offset), counter (v / 4, b, 0, 0), word v % 4, as
-// ((x >> 41) + 1/2) / 2^23 (strictly inside (0, 1), so G_v is finite).  One block per sequence (the keys cost two
-// logarithms and a Philox block per four tokens: all sixteen waves of the
-// block share the row); ties by lower token id.
+// ((x >> 41) + 1/2) / 2^23 (strictly inside (0, 1), so G_v is finite); ties by
+// lower token id.  The keys cost two logarithms per token and a Philox block
+// per four tokens, so the row is spread over many blocks: block (s, b) draws
+// the 1024 tokens of segment s of sequence b (one Philox block per thread),
+// leaves its best (key, id) in the workspace as one order-preserving 64-bit
+// word, and one wave per sequence then takes the largest word.  Without a
+// workspace one 1024-thread block per sequence does the whole row.
 constexpr int kSampleThreads = 1024;
+constexpr int kSegThreads = 256;
+constexpr int kSegTokens = 4 * kSegThreads;
 
-template <int DT>
-__global__ __launch_bounds__(kSampleThreads) void sample_next_kernel(SampleArgs a) {
-  const int b = blockIdx.x, tid = threadIdx.x;
+// Row of sequence b's last accepted node, or -1 when its accept_len / path
+// entry is out of range (next_tok is then left untouched).
+__device__ __forceinline__ int64_t sample_row(const SampleArgs &a, int b) {
   const int n0 = a.node_off[b], N = a.node_off[b + 1] - n0;
   const int acc = a.accept_len[b];
-  if (acc < 0 || acc >= a.path_stride) return;             // not an accepted path: next_tok untouched
+  if (acc < 0 || acc >= a.path_stride) return -1;
   const int node = a.path[(int64_t)b * a.path_stride + acc];
-  if (node < 0 || node >= N) return;
-  const int64_t row = (int64_t)(n0 + node) * a.vocab;
-  float best = -INFINITY;
-  int arg = a.vocab;
-  for (int q = tid; 4 * q < a.vocab; q += kSampleThreads) {
-    uint64_t x[4] = {(uint64_t)q, (uint64_t)b, 0ull, 0ull};
-    philox4x64_10(x, a.seed, a.offset);
+  if (node < 0 || node >= N) return -1;
+  return (int64_t)(n0 + node) * a.vocab;
+}
+
+// The four keys of Philox block q of sequence b, folded into (best, arg).
+template <int DT>
+__device__ __forceinline__ void sample_block(const SampleArgs &a, int b, int64_t row, int q, float &best, int &arg) {
+  uint64_t x[4] = {(uint64_t)q, (uint64_t)b, 0ull, 0ull};
+  philox4x64_10(x, a.seed, a.offset);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int v = 4 * q + j;
-      if (v < a.vocab) {
-        // 23 random bits: (k + 1/2) 2^-23 is exact in fp32 and lies in [2^-24, 1 - 2^-24]
-        const float u = ((float)(x[j] >> 41) + 0.5f) * 0x1p-23f;
-        const float g = -logf(-logf(u));
-        const float s = fmaf(ld<DT>(a.logits, row + v), a.inv_temp, g);
-        if (better(s, v, best, arg)) {
-          best = s;
-          arg = v;
-        }
+  for (int j = 0; j < 4; ++j) {
+    const int v = 4 * q + j;
+    if (v < a.vocab) {
+      // 23 random bits: (k + 1/2) 2^-23 is exact in fp32 and lies in [2^-24, 1 - 2^-24]
+      const float u = ((float)(x[j] >> 41) + 0.5f) * 0x1p-23f;
+      const float g = -logf(-logf(u));
+      const float s = fmaf(ld<DT>(a.logits, row + v), a.inv_temp, g);
+      if (better(s, v, best, arg)) {
+        best = s;
+        arg = v;
       }
     }
   }
+}
+
+// Best (key, id) of a block, in thread 0 (waves, then LDS).
+template <int NT>
+__device__ __forceinline__ void block_argbest(float &best, int &arg) {
   wave_argbest(best, arg);
-  constexpr int kW = kSampleThreads / 64;
+  constexpr int kW = NT / 64;
   __shared__ float sv[kW];
   __shared__ int si[kW];
+  const int tid = threadIdx.x;
   if ((tid & 63) == 0) {
     sv[tid >> 6] = best;
     si[tid >> 6] = arg;
   }
   __syncthreads();
-  if (tid == 0) {
+  if (tid == 0)
     for (int w = 1; w < kW; ++w)
       if (better(sv[w], si[w], best, arg)) {
         best = sv[w];
         arg = si[w];
       }
-    a.next_tok[b] = arg;
+}
+
+template <int DT>
+__global__ __launch_bounds__(kSampleThreads) void sample_next_kernel(SampleArgs a) {
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int64_t row = sample_row(a, b);
+  if (row < 0) return;
+  float best = -INFINITY;
+  int arg = a.vocab;
+  for (int q = tid; 4 * q < a.vocab; q += kSampleThreads) sample_block<DT>(a, b, row, q, best, arg);
+  block_argbest<kSampleThreads>(best, arg);
+  if (tid == 0) a.next_tok[b] = arg;
+}
+
+// The order of (key, id) as one unsigned word: larger key first (-0 counts as
+// +0), then lower id.
+__device__ __forceinline__ uint64_t sample_word(float s, int v) {
+  const uint32_t u = __float_as_uint(s == 0.f ? 0.f : s);
+  const uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return (uint64_t)k << 32 | (uint32_t)(0x7FFFFFFF - v);
+}
+
+template <int DT>
+__global__ __launch_bounds__(kSegThreads) void sample_next_segments(SampleArgs a, uint64_t *words, int nseg) {
+  const int seg = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int64_t row = sample_row(a, b);
+  if (row < 0) return;
+  float best = -INFINITY;
+  int arg = a.vocab;
+  const int q = seg * kSegThreads + tid;
+  if (4 * q < a.vocab) sample_block<DT>(a, b, row, q, best, arg);
+  block_argbest<kSegThreads>(best, arg);
+  // a segment always holds at least one token, so arg < vocab here
+  if (tid == 0) words[(int64_t)b * nseg + seg] = sample_word(best, arg);
+}
+
+__global__ __launch_bounds__(64) void sample_next_pick(SampleArgs a, const uint64_t *words, int nseg) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  if (sample_row(a, b) < 0) return;
+  uint64_t w = 0;
+  for (int s = lane; s < nseg; s += 64) {
+    const uint64_t x = words[(int64_t)b * nseg + s];
+    w = x > w ? x : w;
   }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t o = (uint64_t)(uint32_t)__shfl_xor((int)(w >> 32), off) << 32 | (uint32_t)__shfl_xor((int)w, off);
+    w = o > w ? o : w;
+  }
+  if (lane == 0) a.next_tok[b] = 0x7FFFFFFF - (int)(uint32_t)w;
 }
 
 }  // namespace
 
-hipError_t launch_sample_next(int dt, const SampleArgs &a, int B, hipStream_t st) {
-  if (dt == 1)
+int sample_segments(int vocab) { return (vocab + kSegTokens - 1) / kSegTokens; }
+
+hipError_t launch_sample_next(int dt, const SampleArgs &a, int B, uint64_t *words, hipStream_t st) {
+  if (words) {
+    const int nseg = sample_segments(a.vocab);
+    if (dt == 1)
+      hipLaunchKernelGGL(sample_next_segments<1>, dim3(nseg, B), dim3(kSegThreads), 0, st, a, words, nseg);
+    else
+      hipLaunchKernelGGL(sample_next_segments<0>, dim3(nseg, B), dim3(kSegThreads), 0, st, a, words, nseg);
+    hipLaunchKernelGGL(sample_next_pick, dim3(B), dim3(64), 0, st, a, (const uint64_t *)words, nseg);
+  } else if (dt == 1) {
     hipLaunchKernelGGL(sample_next_kernel<1>, dim3(B), dim3(kSampleThreads), 0, st, a);
-  else
+  } else {
     hipLaunchKernelGGL(sample_next_kernel<0>, dim3(B), dim3(kSampleThreads), 0, st, a);
+  }
   return hipGetLastError();
 }
 

@@ -384,6 +384,8 @@ size_t accept_ws_bytes(const TreeInfo &ti, int mode) {
 }
 // The fused acceptance and compaction of more than kMaxSeqPerLaunch
 // sequences keeps their compaction descriptors after the acceptance's part.
+// Sampled next token: one 64-bit word per (sequence, 1024-token segment).
+size_t sample_ws_bytes(int B, int vocab) { return align256((size_t)B * sample_segments(vocab) * sizeof(uint64_t)); }
 size_t compact_table_bytes(int B) { return B > kMaxSeqPerLaunch ? align256((size_t)B * sizeof(CompactSeq)) : 0; }
 
 // Validation and kernel arguments of the acceptance (nothing is launched).
@@ -480,6 +482,7 @@ size_t specmemo_workspace_bytes(int32_t which, specmemo_dtype dt, const specmemo
     return p.ws_bytes;
   }
   if (which == SPECMEMO_WS_PAD) return 256;   // the batch's uniform acceptance length
+  if (which == SPECMEMO_WS_SAMPLE) return vocab < 1 ? 0 : sample_ws_bytes(ti.B, vocab);
   if (which == SPECMEMO_WS_ACCEPT) return accept_ws_bytes(ti, n_q_or_heads) + compact_table_bytes(ti.B);
   return 0;
 }
@@ -743,7 +746,7 @@ int specmemo_accept(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, s
 
 int specmemo_sample_next(specmemo_dtype dt, const specmemo_trees *t, int32_t vocab, float temperature, uint64_t seed,
                          uint64_t offset, const void *base_logits, const int32_t *accept_len, const int32_t *path,
-                         int32_t path_stride, int32_t *next_tok, void *stream) {
+                         int32_t path_stride, int32_t *next_tok, void *ws, size_t ws_bytes, void *stream) {
   int rc;
   if ((rc = check_dtype(dt))) return rc;
   TreeInfo ti;
@@ -766,7 +769,14 @@ int specmemo_sample_next(specmemo_dtype dt, const specmemo_trees *t, int32_t voc
   a.seed = seed;
   a.offset = offset;
   a.next_tok = next_tok;
-  return hip_status(launch_sample_next(dt, a, ti.B, static_cast<hipStream_t>(stream)), "sampling launch");
+  uint64_t *words = nullptr;
+  if (ws) {
+    const size_t need = sample_ws_bytes(ti.B, vocab);
+    if (!al(ws, 16) || ws_bytes < need)
+      return fail(SPECMEMO_E_WORKSPACE, "workspace of %zu bytes needed (16-byte aligned), got %zu", need, ws_bytes);
+    words = static_cast<uint64_t *>(ws);
+  }
+  return hip_status(launch_sample_next(dt, a, ti.B, words, static_cast<hipStream_t>(stream)), "sampling launch");
 }
 
 }  // extern "C"

@@ -129,7 +129,10 @@ struct SampleArgs {
   uint64_t seed, offset;   // Philox key
   int32_t *next_tok;
 };
-hipError_t launch_sample_next(int dt, const SampleArgs &a, int B, hipStream_t st);
+// words: the workspace of the segmented form (B x sample_segments(vocab)
+// 64-bit words), or nullptr for one block per sequence.
+int sample_segments(int vocab);
+hipError_t launch_sample_next(int dt, const SampleArgs &a, int B, uint64_t *words, hipStream_t st);
 
 // ---- compaction ------------------------------------------------------------------
 struct CompactSeq {

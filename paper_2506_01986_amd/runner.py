@@ -344,7 +344,8 @@ class DecodeLoop:
         kv = sm.KVPool(self.k, self.v, seq_len, base, caps, L)
         mark("upload")
         logits = torch.empty((B, cfg.n_heads, cfg.vocab), dtype=torch.float32, device=dev) if self.keep_logits else None
-        ws_bytes = max(ws_fixed, sm.workspace_bytes(sm.WS_ATTN, self.dt, tr, kv, cfg.n_q), 16)
+        ws_bytes = max(ws_fixed, sm.workspace_bytes(sm.WS_ATTN, self.dt, tr, kv, cfg.n_q),
+                       sm.workspace_bytes(sm.WS_SAMPLE, self.dt, tr, None, 0, cfg.vocab), 16)
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
         ids = torch.empty((B, cfg.n_heads, cfg.kmax), **i32)
         tok = torch.empty(sumN, **i32)
@@ -388,7 +389,7 @@ class DecodeLoop:
         mark("accept_compact")
         if st.temperature is not None:
             sm.sample_next(self.dt, tr, cfg.vocab, st.temperature, st.sample_seed, t, lg, acc, path, self.stride, nxt,
-                           stream=s)
+                           ws=ws, ws_bytes=ws_bytes, stream=s)
         mark("sample_next")
         res_h = res.cpu().numpy()
         acc_h, nxt_h = res_h[0].copy(), res_h[1].copy()

@@ -22,7 +22,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "specmemo.h")
 FP32, BF16 = 0, 1
 GREEDY, TYPICAL = 0, 1
 HEADS_ROWMAJOR, HEADS_PACKED, HEADS_INPUT_PER_HEAD = 0, 1, 2
-WS_TOPK, WS_ATTN, WS_ACCEPT, WS_PAD = 0, 1, 2, 3
+WS_TOPK, WS_ATTN, WS_ACCEPT, WS_PAD, WS_SAMPLE = 0, 1, 2, 3, 4
 
 STATUS = {0: "OK", -1: "E_ARG", -2: "E_DTYPE", -3: "E_TREE", -4: "E_BUDGET", -5: "E_WORKSPACE", -6: "E_HIP"}
 
@@ -95,7 +95,7 @@ def load():
         lib.specmemo_head_logits.restype = C.c_int
         lib.specmemo_medusa_resblock.argtypes = [i32, i32, i32, i32, vp, vp, i32, vp, vp, vp]
         lib.specmemo_medusa_resblock.restype = C.c_int
-        lib.specmemo_sample_next.argtypes = [i32, PT, i32, f32, u64, u64, vp, vp, vp, i32, vp, vp]
+        lib.specmemo_sample_next.argtypes = [i32, PT, i32, f32, u64, u64, vp, vp, vp, i32, vp, vp, sz, vp]
         lib.specmemo_sample_next.restype = C.c_int
         lib.specmemo_key_mask_words.argtypes = [i64]
         lib.specmemo_key_mask_words.restype = i64
@@ -239,10 +239,11 @@ def medusa_resblock(dt: int, B: int, hidden: int, n_heads: int, h, w1, b1, out, 
 
 
 def sample_next(dt: int, trees: Trees, vocab: int, temperature: float, seed: int, offset: int, base_logits,
-                accept_len, path, path_stride: int, next_tok, stream=None):
+                accept_len, path, path_stride: int, next_tok, ws=None, ws_bytes: int = 0, stream=None):
     ts = trees.struct()
     _check(load().specmemo_sample_next(dt, C.byref(ts), vocab, temperature, seed, offset, _ptr(base_logits),
-                                       _ptr(accept_len), _ptr(path), path_stride, _ptr(next_tok), _stream(stream)))
+                                       _ptr(accept_len), _ptr(path), path_stride, _ptr(next_tok), _ptr(ws),
+                                       ws_bytes, _stream(stream)))
 
 
 def packed_heads_bytes(dt: int, n_heads: int, vocab: int, hidden: int) -> int:

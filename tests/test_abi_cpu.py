@@ -31,7 +31,7 @@ def test_library_loads_and_exports_every_declared_function():
     assert {"specmemo_medusa_topk", "specmemo_tree_attn", "specmemo_accept", "specmemo_kv_compact"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert sm.abi_version() == 8
+    assert sm.abi_version() == 9
 
 
 class FakeTrees(sm.Trees):
@@ -258,6 +258,14 @@ def test_projection_resblock_and_sampling_errors():
         expect("E_ARG", sm.sample_next, sm.BF16, t, 100, temp, 1, 0, FAKE, FAKE, FAKE, 4, FAKE, stream=0)
     expect("E_ARG", sm.sample_next, sm.BF16, t, 100, 1.0, 1, 0, FAKE, FAKE, FAKE, 3, FAKE, stream=0)   # stride < depth + 1
     expect("E_HIP", sm.sample_next, sm.BF16, t, 100, 1.0, 1, 0, FAKE, FAKE, FAKE, 4, FAKE, stream=0)
+    # the segmented form: one 64-bit word per 1024-token segment of each row
+    need = sm.workspace_bytes(sm.WS_SAMPLE, sm.BF16, t, None, 0, 32000)
+    assert need >= 1 * 32 * 8 and need % 256 == 0
+    assert sm.workspace_bytes(sm.WS_SAMPLE, sm.BF16, t, None, 0, 0) == 0
+    expect("E_WORKSPACE", sm.sample_next, sm.BF16, t, 32000, 1.0, 1, 0, FAKE, FAKE, FAKE, 4, FAKE, ws=FAKE,
+           ws_bytes=need - 8, stream=0)
+    expect("E_HIP", sm.sample_next, sm.BF16, t, 32000, 1.0, 1, 0, FAKE, FAKE, FAKE, 4, FAKE, ws=FAKE, ws_bytes=need,
+           stream=0)
 
 
 @cpu_only

@@ -104,10 +104,17 @@ def test_sampled_next_token(torch_cuda, temperature):
     ref, best, second = oracle.sample_next(lg, node_off, acc, path, temperature, seed, offset)
     d = lambda x: torch.from_numpy(x).to("cuda")
     nxt = torch.full((B,), -7, dtype=torch.int32, device="cuda")
-    sm.sample_next(sm.BF16, tr, vocab, temperature, seed, offset, runner.to_device(lg, "bf16", "cuda"), d(acc),
-                   d(path), n, nxt)
+    lg_d = runner.to_device(lg, "bf16", "cuda")
+    sm.sample_next(sm.BF16, tr, vocab, temperature, seed, offset, lg_d, d(acc), d(path), n, nxt)
+    # the segmented form (a workspace word per 1024-token segment) draws the same tokens
+    wsb = sm.workspace_bytes(sm.WS_SAMPLE, sm.BF16, tr, None, 0, vocab)
+    ws = torch.full((wsb,), 0xA5, dtype=torch.uint8, device="cuda")
+    nxt_seg = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    sm.sample_next(sm.BF16, tr, vocab, temperature, seed, offset, lg_d, d(acc), d(path), n, nxt_seg, ws=ws,
+                   ws_bytes=wsb)
     torch.cuda.synchronize()
     got = nxt.cpu().numpy()
+    assert np.array_equal(nxt_seg.cpu().numpy(), got)
     diff = np.nonzero(got != ref)[0]
     say(f"[decode] sampled T={temperature}: {B - len(diff)}/{B} equal, near ties {[int(b) for b in diff]}")
     for b in diff:
