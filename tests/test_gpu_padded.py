@@ -131,6 +131,10 @@ PADDED = {
     # every committed row a pad but the prompt's first
     "mostly_pads": (edge_cfg(B=2, n_q=4, n_kv=1), lambda r: [synth.t16(), synth.t64()], [40, 60], 12,
                     {0: (1, 10 ** 6), 1: (1, 10 ** 6)}),
+    # the same with one query head per KV head (64-row items: the key-split form, where one key group
+    # of a row can see nothing but pads)
+    "mha_mostly_pads": (edge_cfg(B=2, n_q=2, n_kv=2), lambda r: [synth.t16(), synth.t64()], [40, 60], 12,
+                        {0: (1, 10 ** 6), 1: (1, 10 ** 6)}),
 }
 
 
