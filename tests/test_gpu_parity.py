@@ -239,6 +239,16 @@ def test_config_parity(torch_cuda, name):
     run_parity(torch_cuda, wl, max_attn_rows=rows, full_longest=whole)
 
 
+# the same workloads drawn from other seeds (lengths, trees, values, planted walks)
+@pytest.mark.parametrize("name,seed", [("llama2_13b_b4", 101), ("llama2_70b_b10", 101), ("llama2_70b_b10", 102),
+                                       ("stress_b32", 101)])
+def test_config_parity_other_seeds(torch_cuda, name, seed):
+    cfg = configs.get(name)
+    wl = synth.make(cfg, seed=seed)
+    rows, whole = CONFIG_ROWS[name] or (None, 0)
+    run_parity(torch_cuda, wl, max_attn_rows=rows, full_longest=whole, label=f"{name} seed {seed}")
+
+
 def edge_cfg(**kw):
     base = dict(name="edge", dtype="bf16", B=3, n_q=8, n_kv=1, head_dim=128, hidden=136, vocab=1000,
                 n_heads=4, topk=(10, 10, 10, 10), tree="T64", kv_len=(1, 1), seed=77, w_std=0.05)
