@@ -47,6 +47,14 @@ STAGE_KERNELS = {"medusa_topk": ["head_logits_packed", "topk_rows"],
                  "tree_attn": ["tree_attn_bf16", "tree_attn_combine"],
                  "accept": ["row_argbest_all", "accept_walk"], "kv_compact": ["kv_compact_kernel"],
                  "accept_compact": ["row_argbest_all", "accept_walk_compact"]}
+FP32_STAGE_KERNELS = {"medusa_topk": ["head_logits_f32", "topk_rows"], "tree_attn": ["tree_attn_f32"]}
+
+
+def stage_kernels(stage, dtype):
+    """The kernels of a stage for this dtype (the fp32 workload has kernels of its own)."""
+    return FP32_STAGE_KERNELS.get(stage, STAGE_KERNELS[stage]) if dtype == "fp32" else STAGE_KERNELS[stage]
+
+
 # Sources whose text decides a stage's kernels (with the shared device.h and
 # internal.h): a counter summary is used only while their hash is unchanged.
 STAGE_SOURCES = {"medusa_topk": ["medusa_topk.hip"], "tree_attn": ["tree_attn.hip"],
@@ -586,13 +594,13 @@ def main():
                     "ms": round(kms, 5), "source_sha256_16": source_sha("head_logits_packed")}
     elif dom == "tree_attn" and cfg.dtype == "bf16":
         # attention above the ridge point (FLOP per algorithmic byte > 2.5 PFLOP/s / 8 TB/s): matrix-core bound
-        roofline = {"bound": "mfma", "kernel": dom, "kernels": STAGE_KERNELS[dom], "achieved": st[dom]["TFLOPs"],
+        roofline = {"bound": "mfma", "kernel": dom, "kernels": stage_kernels(dom, cfg.dtype), "achieved": st[dom]["TFLOPs"],
                     "peak": MFMA_PEAK_TFLOPS[cfg.dtype], "unit": "TFLOP/s", "frac": st[dom]["mfma_frac"],
                     "traffic": measured_traffic(dom, cfg.name), "algorithmic_flops": st[dom]["flops"],
                     "algorithmic_bytes": st[dom]["algorithmic_bytes"], "ms": st[dom]["ms"],
                     "source_sha256_16": source_sha(dom)}
     else:
-        roofline = {"bound": "hbm", "kernel": dom, "kernels": STAGE_KERNELS[dom], "achieved": st[dom]["GBps"],
+        roofline = {"bound": "hbm", "kernel": dom, "kernels": stage_kernels(dom, cfg.dtype), "achieved": st[dom]["GBps"],
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": st[dom]["hbm_frac"],
                     "traffic": measured_traffic(dom, cfg.name), "algorithmic_bytes": st[dom]["algorithmic_bytes"],
                     "ms": st[dom]["ms"], "source_sha256_16": source_sha(dom)}

@@ -658,7 +658,7 @@ __global__ __launch_bounds__(4 * RB) void tree_attn_combine(AttnArgs a) {
 }
 
 // fp32 path: one wave per (node, query head); lanes own head-dimension elements
-// and walk the key set one key at a time.
+// and walk the key set in order (the committed keys in batches of sixteen).
 __global__ __launch_bounds__(256) void tree_attn_f32(AttnArgs a, int node_begin, int node_count) {
   const int lane = threadIdx.x & 63;
   const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -674,23 +674,66 @@ __global__ __launch_bounds__(256) void tree_attn_f32(AttnArgs a, int node_begin,
   const bool e0 = lane < d, e1 = lane + 64 < d;
   const float q0 = e0 ? q[lane] : 0.f, q1 = e1 ? q[lane + 64] : 0.f;
   float m = -INFINITY, l = 0.f, o0 = 0.f, o1 = 0.f;
-  auto visit = [&](int64_t row) {
-    float p = (e0 ? q0 * K[row * d + lane] : 0.f) + (e1 ? q1 * K[row * d + lane + 64] : 0.f);
+  auto dot = [&](float k0, float k1) {
+    float p = q0 * k0 + q1 * k1;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) p += __shfl_xor(p, off);
+    return p;
+  };
+  auto update = [&](float p, float v0, float v1) {   // online softmax, one key
     const float s = p * a.scale;
     const float mn = fmaxf(m, s);
     const float alpha = expf(m - mn), pe = expf(s - mn);
     l = l * alpha + pe;
-    o0 = o0 * alpha + pe * (e0 ? V[row * d + lane] : 0.f);
-    o1 = o1 * alpha + pe * (e1 ? V[row * d + lane + 64] : 0.f);
+    o0 = o0 * alpha + pe * v0;
+    o1 = o1 * alpha + pe * v1;
     m = mn;
   };
-  for (int t = 0; t < S.L; ++t) {
-    const int64_t r = S.base + t;          // pad tokens (padded batching) are skipped: weight 0
-    if (!a.key_valid || ((a.key_valid[r >> 5] >> (r & 31)) & 1u)) visit(t);
+  // Committed keys sixteen at a time: the batch's row loads are issued
+  // together and its reductions are independent; the batch then moves the
+  // running max once and adds its weights.  Pad tokens (padded batching) are
+  // skipped: weight 0.
+  constexpr int KB = 16;
+  for (int t0 = 0; t0 < S.L; t0 += KB) {
+    float k0[KB], k1[KB], v0[KB], v1[KB], pp[KB];
+    bool use[KB];
+#pragma unroll
+    for (int u = 0; u < KB; ++u) {
+      const int t = min(t0 + u, S.L - 1);
+      const int64_t r = S.base + t;
+      use[u] = t0 + u < S.L && (!a.key_valid || ((a.key_valid[r >> 5] >> (r & 31)) & 1u));
+      k0[u] = e0 ? K[(int64_t)t * d + lane] : 0.f;
+      k1[u] = e1 ? K[(int64_t)t * d + lane + 64] : 0.f;
+      v0[u] = e0 ? V[(int64_t)t * d + lane] : 0.f;
+      v1[u] = e1 ? V[(int64_t)t * d + lane + 64] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < KB; ++u) pp[u] = dot(k0[u], k1[u]);
+    float mb = m;
+#pragma unroll
+    for (int u = 0; u < KB; ++u)
+      if (use[u]) mb = fmaxf(mb, pp[u] * a.scale);
+    if (mb > m) {   // m = -inf on the first visible key: alpha = 0
+      const float alpha = expf(m - mb);
+      l *= alpha;
+      o0 *= alpha;
+      o1 *= alpha;
+      m = mb;
+    }
+#pragma unroll
+    for (int u = 0; u < KB; ++u)
+      if (use[u]) {
+        const float pe = expf(pp[u] * a.scale - m);
+        l += pe;
+        o0 = fmaf(pe, v0[u], o0);
+        o1 = fmaf(pe, v1[u], o1);
+      }
   }
-  for (int u = n; u >= 0; u = a.parent[S.node0 + u]) visit(S.L + u);
+  for (int u = n; u >= 0; u = a.parent[S.node0 + u]) {   // the node's tree rows: its root path
+    const int64_t row = S.L + u;
+    const float p = dot(e0 ? K[row * d + lane] : 0.f, e1 ? K[row * d + lane + 64] : 0.f);
+    update(p, e0 ? V[row * d + lane] : 0.f, e1 ? V[row * d + lane + 64] : 0.f);
+  }
   float *out = static_cast<float *>(a.out) + ((int64_t)gnode * a.n_q + hq) * d;
   if (e0) out[lane] = o0 / l;
   if (e1) out[lane + 64] = o1 / l;
